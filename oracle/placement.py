@@ -1,0 +1,93 @@
+"""Oracle: importance-aware expert deployment (Algorithm 1, second and third
+parts; Section IV-B and IV-C).  TEST INFRASTRUCTURE ONLY.
+
+Mandatory placement, per layer:
+  * experts in non-increasing memory demand p (ties: lower index);
+  * memory-feasible servers F = {m : b_m + p <= C_m} (eq 29);
+  * Score(m) = lambda1 * b_m / C_m + lambda2 * eta_m, eta_m = number of the
+    expert's group already on m in this layer (eq 30); the expert goes to the
+    feasible server of least score (eq 31), ties to the lower server index;
+  * an expert with F empty waits; after the layer the waiting experts go to
+    the server with the largest remaining memory C_m - b_m (ties: lower index).
+  b_m (used memory) accumulates over all layers.
+
+Redundant placement, over all layers (eq 32-35), greedy:
+  * y_{m,l,g} = 1 when server m already holds an expert of group g of layer l;
+  * benefit B(m,l,j) = pi_m I_j (1 - y_{m,l,g(j)}) / p_j (eq 33) for candidates
+    with x = 0 that fit the remaining memory;
+  * repeatedly deploy the candidate of largest positive benefit (ties: lower
+    (l, m, j)), update y and b, until none is left.
+Reading of eq 32: the sum runs over the experts k of group g(j) in layer l.
+fp64 throughout.
+"""
+from __future__ import annotations
+
+from typing import List, Sequence
+
+import numpy as np
+
+
+class CapacityError(ValueError):
+    pass
+
+
+def place(group_of: Sequence[np.ndarray], importance: Sequence[np.ndarray],
+          p: Sequence[np.ndarray], C: np.ndarray, pi: np.ndarray,
+          lambda1: float = 0.5, redundancy: bool = True):
+    """Returns (x: list over layers of [M, E_l] uint8, b [M] used memory)."""
+    N = len(group_of)
+    M = len(C)
+    lambda2 = 1.0 - lambda1
+    tot_p = sum(float(np.sum(pl)) for pl in p)
+    if tot_p > float(np.sum(C)):
+        raise CapacityError("total expert memory exceeds the servers' capacity")
+    b = np.zeros(M)
+    x: List[np.ndarray] = [np.zeros((M, len(g)), dtype=np.uint8) for g in group_of]
+
+    for l in range(N):
+        g = group_of[l]
+        E = len(g)
+        order = sorted(range(E), key=lambda j: (-float(p[l][j]), j))
+        waiting = []
+        for j in order:
+            best_m, best_score = -1, None
+            for m in range(M):
+                if not (b[m] + p[l][j] <= C[m]):
+                    continue
+                eta = sum(int(x[l][m, kk]) for kk in range(E) if g[kk] == g[j])
+                score = lambda1 * b[m] / C[m] + lambda2 * eta
+                if best_score is None or score < best_score:
+                    best_m, best_score = m, score
+            if best_m < 0:
+                waiting.append(j)
+            else:
+                x[l][best_m, j] = 1
+                b[best_m] += p[l][j]
+        for j in waiting:
+            best_m = max(range(M), key=lambda m: (C[m] - b[m], -m))
+            x[l][best_m, j] = 1
+            b[best_m] += p[l][j]
+
+    if redundancy:
+        while True:
+            best = None  # (benefit, l, m, j)
+            for l in range(N):
+                g = group_of[l]
+                E = len(g)
+                for m in range(M):
+                    covered = {int(g[kk]) for kk in range(E) if x[l][m, kk]}
+                    for j in range(E):
+                        if x[l][m, j] or not (b[m] + p[l][j] <= C[m]):
+                            continue
+                        y = 1 if int(g[j]) in covered else 0
+                        B = pi[m] * importance[l][j] * (1 - y) / p[l][j]
+                        if B <= 0:
+                            continue
+                        if best is None or B > best[0]:
+                            best = (B, l, m, j)
+            if best is None:
+                break
+            _, l, m, j = best
+            x[l][m, j] = 1
+            b[m] += p[l][j]
+    return x, b
