@@ -1,0 +1,231 @@
+"""Benchmark: one OrderMoE MoE layer on one MI355X.
+
+A step is the whole layer path of one server over one batch: routing and
+server-expert selection with the dispatch list (ordermoe_route_select), then
+the local grouped SwiGLU FFN with the weighted combine
+(ordermoe_local_moe_forward).  Workload: the Mixtral-8x7B-shaped layer --
+4096 tokens of hidden 4096, 8 experts of FFN 14336, top-2, 4 simulated
+servers holding 2 experts each -- bf16, synthetic seeded inputs, inputs
+resident in HBM before the timed region.
+
+Prints one JSON line (rank 0).  Besides tokens/s it reports the roofline of
+the dominant kernel (the grouped gate/up GEMM) from its average launch time
+measured with HIP events over the timed region, and the CPU oracle timed on a
+bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def _setup(cfg, torch, om):
+    """Library-side layer: similarity build on the GPU, deployment and tables
+    on the host, expert weights of this server packed on the device."""
+    import workloads as wl
+    dev = "cuda"
+
+    def up(a):
+        t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32))
+        return (t.to(torch.bfloat16) if cfg.dtype == "bf16" else t).to(dev)
+
+    W = wl.router(cfg)
+    Xc = wl.calibration(cfg)
+    ws = torch.empty(om.ordermoe_similarity_workspace_size(Xc.shape[0], cfg.d, cfg.E),
+                     dtype=torch.uint8, device=dev)
+    model = om.ordermoe_build_similarity(up(Xc), up(W), cfg.k, cfg.theta, cfg.alpha_f, ws)
+    del ws
+    x_dep, _ = om.ordermoe_place([model["group_of"]], [model["importance"]], [np.ones(cfg.E)],
+                                 np.array(cfg.capacity), np.full(cfg.M, 1.0 / cfg.M), cfg.lambda1, 1)
+    x_dep = x_dep[0]
+    net = wl.network(cfg)
+    c = np.full(cfg.E, 6.0 * cfg.d * cfg.f)
+    dref = float(np.mean(c)) / float(np.mean(net.F))
+    z_bits = 8.0 * cfg.d * cfg.bytes_per_el
+    tabs = om.ordermoe_build_tables(model["sim"], model["group_of"], cfg.theta, x_dep, net.B,
+                                    net.tau, net.F, z_bits, c, dref, cfg.omega_T)
+    tabs_dev = {n: torch.from_numpy(np.ascontiguousarray(v)).to(dev) for n, v in tabs.items()
+                if n != "srvmask"}
+    tabs_dev["srvmask"] = torch.from_numpy(tabs["srvmask"].view(np.int32)).to(dev)
+    w_router = up(W)
+    code = om.BF16 if cfg.dtype == "bf16" else om.F32
+    layer = om.make_layer(code, cfg.d, cfg.E, cfg.k, cfg.M, 15, w_router, tabs_dev, cfg.Qbar,
+                          cfg.omega_Q, cfg.pin_local_exact, cfg.allow_sub, cfg.renorm)
+    local = [int(j) for j in np.nonzero(x_dep[cfg.m0])[0]]
+    n = len(local)
+    tdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    w_gu = torch.empty((n, 2 * cfg.f, cfg.d), dtype=tdt, device=dev)
+    w_dn = torch.empty((n, cfg.d, cfg.f), dtype=tdt, device=dev)
+    for i, j in enumerate(local):
+        g, u, dn = wl.expert(cfg, j)
+        gd, ud = up(g), up(u)
+        om.ordermoe_pack_gate_up(gd.unsqueeze(0), ud.unsqueeze(0), w_gu[i:i + 1])
+        w_dn[i] = up(dn)
+        del gd, ud
+    experts = om.make_experts(code, cfg.d, cfg.f, cfg.E, local, w_gu, w_dn)
+    X = wl.tokens(cfg)
+    st = dict(layer=layer, experts=experts, keep=(w_router, tabs_dev, w_gu, w_dn), local=local,
+              x=up(X), loc=torch.from_numpy(wl.token_locations(cfg)).to(dev),
+              qhat=torch.from_numpy(wl.accumulated_loss(cfg)).to(dev), X=X, W=W, model=model,
+              x_dep=x_dep, net=net, c=c, dref=dref, z_bits=z_bits)
+    st["out"] = om.alloc_route_out(cfg.T, cfg.k, cfg.M, dev)
+    st["out_struct"] = om.route_out_struct(st["out"])
+    st["ws_r"] = torch.empty(om.ordermoe_route_workspace_size(cfg.T, cfg.k, cfg.M), dtype=torch.uint8,
+                             device=dev)
+    st["ws_f"] = torch.empty(om.ordermoe_forward_workspace_size(experts, cfg.T, cfg.k),
+                             dtype=torch.uint8, device=dev)
+    st["y"] = torch.empty((cfg.T, cfg.d), dtype=tdt, device=dev)
+    st["ro"] = torch.empty(n + 2, dtype=torch.int32, device=dev)
+    return st
+
+
+def _step(cfg, st, om):
+    o = st["out"]
+    om.ordermoe_route_select(st["layer"], st["x"], cfg.T, st["loc"], st["qhat"], o, st["ws_r"],
+                             out_struct=st["out_struct"])
+    om.ordermoe_local_moe_forward(st["experts"], st["x"], cfg.T, cfg.k, o["w"], o["exec_k"],
+                                  o["exec_m"], st["loc"], cfg.m0, st["y"], st["ro"], st["ws_f"])
+
+
+def _cpu_baseline(cfg, st, target_s: float):
+    """The oracle as it stands on a bounded token sample of the same layer."""
+    import workloads as wl
+    from oracle import layer as olayer
+    from oracle import route, similarity, tables
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        cores = os.cpu_count() or 1
+    # the oracle's own offline model (not timed: built once per layer)
+    model = similarity.build(wl.calibration(cfg, 4096), st["W"], cfg.k, cfg.theta, cfg.alpha_f)
+    S = tables.static_cost(cfg.M, cfg.E, st["z_bits"], st["net"].B, st["net"].tau, st["c"],
+                           st["net"].F, st["dref"], cfg.omega_T)
+    experts = {}
+
+    def ew(j):
+        if j not in experts:
+            experts[j] = wl.expert(cfg, j)
+        return experts[j]
+
+    loc = wl.token_locations(cfg)
+    qh = wl.accumulated_loss(cfg)
+
+    def run(n):
+        X = st["X"][:n]
+        t0 = time.perf_counter()
+        idx, w, mg, _ = route.route(X, st["W"], cfg.k, cfg.renorm)
+        sel = olayer.select(idx, st["x_dep"], model["sim"].astype(np.float32), model["group_of"],
+                            cfg.theta, S, cfg.Qbar, cfg.omega_Q, loc[:n], qh[:n],
+                            cfg.pin_local_exact, cfg.allow_sub)
+        olayer.dispatch(sel["exec_m"], loc[:n], cfg.M)
+        olayer.server_output(X, w, sel["exec_k"], sel["exec_m"], loc[:n], cfg.m0, ew, (),
+                             np.arange(n))
+        return time.perf_counter() - t0
+
+    for j in st["local"]:
+        ew(j)
+    n = 16
+    dt = run(n)
+    while dt < target_s / 4 and n < cfg.T:
+        n = min(cfg.T, int(n * max(2.0, target_s / max(dt, 1e-3) * 0.8)))
+        dt = run(n)
+    return {"value": n / dt, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": "first %d of the %d tokens (route fp64, selection, dispatch, fp64 FFN of "
+                      "server %d); %.1f s" % (n, cfg.T, cfg.m0, dt)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: the layer runs one simulated server's experts on one "
+              "MI355X; other servers are placement masks, so --gpus %d is not supported"
+              % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import workloads as wl
+    from paper_2607_17154_amd import ordermoe as om
+    if not os.path.exists(om.LIB_PATH):
+        from paper_2607_17154_amd import build as _b
+        _b.build()
+    cfg = wl.C2
+    torch.cuda.set_device(0)
+    print("bench: setting up %s" % cfg.name, file=sys.stderr, flush=True)
+    st = _setup(cfg, torch, om)
+    torch.cuda.synchronize()
+    for _ in range(args.warmup):
+        _step(cfg, st, om)
+    torch.cuda.synchronize()
+    om.ordermoe_timing_read(reset=True)
+    om.ordermoe_timing_enable(True)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(args.steps):
+        _step(cfg, st, om)
+    e1.record()
+    torch.cuda.synchronize()
+    om.ordermoe_timing_enable(False)
+    ms = e0.elapsed_time(e1)
+    kt = om.ordermoe_timing_read(reset=True)
+    print("bench: %d steps in %.3f ms" % (args.steps, ms), file=sys.stderr, flush=True)
+
+    rows = st["ro"].cpu().numpy()
+    R = int(rows[-1])
+    counters = st["out"]["counters"].cpu().numpy()
+    gu_ms, gu_n = kt.get("gemm_gate_up", (float("nan"), 1))
+    gu_avg_s = gu_ms / gu_n / 1e3
+    gu_flops = 2.0 * R * cfg.d * (2 * cfg.f)          # gate and up projections of R rows
+    achieved = gu_flops / gu_avg_s / 1e12
+    ms_step = ms / args.steps
+    res = {
+        "metric": "MoE-layer tokens/s on 1 MI355X (route+substitute+grouped FFN); % MFMA peak",
+        "value": cfg.T * args.steps / (ms / 1e3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded; random-init expert and router weights of the layer shape)",
+        "config": {"workload": cfg.name, "tokens": cfg.T, "hidden": cfg.d, "experts": cfg.E,
+                   "ffn": cfg.f, "top_k": cfg.k, "servers": cfg.M, "server": cfg.m0,
+                   "local_experts": st["local"], "local_rows": R,
+                   "classes_LE_LS_RE_RS": [int(v) for v in counters[:4]],
+                   "flagged_tokens": int(counters[4]), "remote_transfers": int(counters[5])},
+        "roofline": {"bound": "mfma", "kernel": "gemm_gate_up", "achieved": achieved,
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
+                     "traffic": None, "flop_per_launch": gu_flops, "avg_launch_us": gu_avg_s * 1e6},
+        "kernels_avg_us": {k: v[0] / v[1] * 1e3 for k, v in sorted(kt.items())},
+        "mfma_frac_ffn": (2.0 * R * cfg.d * 3 * cfg.f) / (ms_step / 1e3) / 1e12 / PEAK_BF16_TFLOPS,
+    }
+    if not args.no_cpu_baseline:
+        print("bench: timing the CPU oracle", file=sys.stderr, flush=True)
+        res["cpu_baseline"] = _cpu_baseline(cfg, st, args.cpu_seconds)
+    print(json.dumps(res))
+
+
+if __name__ == "__main__":
+    main()

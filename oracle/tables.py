@@ -99,6 +99,7 @@ def lookahead(H: int, P: Sequence[np.ndarray], x: Sequence[np.ndarray],
     [ g_{l+1}(m', k'' | s = m) + Phi_{l+1}^{(h-1)}(m', k'') ]."""
     N = len(x)
     M = x[0].shape[0]
+    Qbar = float(np.float32(Qbar))   # the runtime budget is an fp32 quantity
 
     def g_next(l1, s, m1, k1, r1):
         q = 0.0

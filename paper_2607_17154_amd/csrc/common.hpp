@@ -1,0 +1,126 @@
+// Internal declarations shared by the library's translation units.
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+#include <string>
+
+#include "../../include/ordermoe.h"
+
+namespace ordermoe {
+
+// Thread-local error message behind ordermoe_last_error().
+void set_error(const std::string& msg);
+void clear_error();
+
+// Returns `code` after recording `msg` (for `return fail(...)` in entry points).
+int fail(int code, const std::string& msg);
+
+// Workspace carving: aligned sub-buffers taken in order from one caller buffer.
+struct Carver {
+    char* base;
+    size_t off = 0;
+    explicit Carver(void* b) : base(static_cast<char*>(b)) {}
+    template <typename T>
+    T* take(size_t count) {
+        off = (off + 255) & ~size_t(255);
+        T* p = base ? reinterpret_cast<T*>(base + off) : nullptr;
+        off += count * sizeof(T);
+        return p;
+    }
+    size_t size() const { return (off + 255) & ~size_t(255); }
+};
+
+// Brackets one kernel launch with timing events when timing is enabled.
+class KernelTimer {
+  public:
+    KernelTimer(const char* name, void* stream);
+    ~KernelTimer();
+    KernelTimer(const KernelTimer&) = delete;
+    KernelTimer& operator=(const KernelTimer&) = delete;
+
+  private:
+    const char* name_;
+    void* stream_;
+    void* start_ = nullptr;
+};
+
+// ---- kernel launchers (defined in the .hip files) ----------------------
+// All return a hipError_t value as int (0 = success).
+
+struct RouteArgs {
+    int dtype, d, E, k, M, gmax, pin, allow_sub, renorm;
+    float Qbar, cq;
+    const void* w_router;
+    const int32_t* t1_k;
+    const float* t1_q;
+    const int32_t* t1_n;
+    const uint32_t* srvmask;
+    const float* S;
+    const void* x;
+    int64_t T;
+    const uint8_t* loc_in;
+    const float* qhat_in;
+    ordermoe_route_out out;
+    // workspace
+    int32_t* blk_dst;      // [nblk][M] remote slots per destination per block
+    int64_t* blk_cnt;      // [nblk][8] per-block counters
+    int32_t* dst_base;     // [nblk][M] exclusive prefix (written by scan)
+    int nblk;
+};
+int launch_route_select(const RouteArgs& a, void* stream);
+int route_tokens_per_block();
+size_t route_smem_bytes(int E, int gmax, int M);
+
+struct ForwardArgs {
+    int dtype, d, f, E, n_local, n_shared, k;
+    int32_t lidx[ORDERMOE_MAX_EXPERTS];  // expert id -> local slot, -1 if not held
+    const void* w_gu;
+    const void* w_dn;
+    const void* w_sh_gu;
+    const void* w_sh_dn;
+    const void* x;
+    int64_t T;
+    const float* w;
+    const int32_t* exec_k;
+    const uint8_t* exec_m;
+    const uint8_t* loc_in;
+    int server;
+    void* y;
+    int32_t* row_offsets;
+    // workspace
+    int32_t* blk_rows;     // [nblk][G] rows per group per block (G = n_local + has_shared)
+    int32_t* blk_base;     // [nblk][G] first row of each group's block segment
+    int32_t* row_tok;      // [rmax] token of each row
+    float* row_w;          // [rmax] merged gate weight of each row
+    int32_t* tok_rows;     // [T][k + 1] rows of each token, -1 padded
+    int32_t* tile_info;    // [4]: tiles of the gate/up GEMM, of the down GEMM, rows, 0
+    void* act_r;           // [rmax_routed][f] routed activations
+    void* act_s;           // [T][n_shared * f] shared activations
+    void* obuf;            // [rmax][d] per-row outputs
+    int64_t rmax_routed;
+    int nblk;
+};
+int launch_local_forward(const ForwardArgs& a, void* stream);
+int forward_tokens_per_block();
+void forward_tile_shape(int dtype, int* bm_gu, int* bn_gu, int* bm_dn, int* bn_dn);
+
+struct SimArgs {
+    int dtype, d, E, k;
+    const void* x_cal;
+    int64_t T_cal;
+    const void* w_router;
+    float* sim;            // [E][E]
+    int64_t* counts;       // [E]
+    float* gram_part;      // [nchunk][128][128] per-block partial Gram matrices
+    int32_t* count_part;   // [nchunk][128] per-block activation counts
+    int nchunk;            // blocks of the partial kernel (= number of partials)
+};
+int launch_similarity(const SimArgs& a, void* stream);
+int64_t similarity_tokens_per_chunk(int E);
+int similarity_max_experts();
+
+int launch_pack_gate_up(int dtype, int n, int f, int d, const void* g, const void* u, void* out,
+                        void* stream);
+
+}  // namespace ordermoe

@@ -1,0 +1,626 @@
+// Local MoE execution of one server on gfx950: the (token, slot) pairs that
+// the selection assigned to this server are turned into expert rows, run
+// through a grouped SwiGLU FFN and combined per token.
+//
+//   rows_count_kernel    per-block row counts per group (local experts, then
+//                        the shared pseudo-expert), duplicates of one token
+//                        merged
+//   rows_scan_kernel     one block: exclusive scans over blocks, group row
+//                        offsets, tile counts of the two GEMMs
+//   rows_scatter_kernel  stable placement of every row (token order inside a
+//                        group), merged gate weight, token -> rows map
+//   ggemm_bf16<.., 0>    gate/up projection, X rows gathered through row_tok,
+//                        packed [2f][d] weights, epilogue silu(g) * u -> bf16
+//   ggemm_bf16<.., 1>    down projection of the activations, epilogue scales
+//                        each row by its gate weight -> bf16 row outputs
+//   combine_kernel       y[t] = sum of t's row outputs in slot order (fp32)
+// The GEMMs are persistent: each workgroup walks the tile list, whose length
+// is read from device memory, so no host synchronisation is needed.  Tiles of
+// one expert are ordered m-fastest so consecutive tiles share a weight tile,
+// and workgroup ids are remapped so that each XCD (and its L2) works on a
+// contiguous range of tiles.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "common.hpp"
+
+namespace ordermoe {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int FT_TB = 256;        // tokens per block in the row kernels
+constexpr int MAXG = ORDERMOE_MAX_LOCAL + 1;
+constexpr int MAXR = ORDERMOE_MAX_TOPK + 1;   // rows per token (routed + shared)
+
+struct RowsArgs {
+    int64_t T;
+    int k, E, n_local, has_shared, server;
+    const float* w;
+    const int32_t* exec_k;
+    const uint8_t* exec_m;
+    const uint8_t* loc_in;
+    int32_t lidx[ORDERMOE_MAX_EXPERTS];   // expert -> local slot (kernel argument)
+    int32_t* blk_rows;        // [nblk][G]
+    int32_t* blk_base;        // [nblk][G]
+    int32_t* row_offsets;     // [n_local + 2]
+    int32_t* row_tok;
+    float* row_w;
+    int32_t* tok_rows;        // [T][k+1]
+    int32_t* tile_info;       // [4]
+    int nblk;
+    // tile geometry for the tile counts
+    int bm_gu, bn_gu, bm_dn, bn_dn;
+    int n_gu_r, n_gu_s, n_dn;
+};
+
+// rows of one token: group ids (local slot, or n_local for the shared group)
+// and merged gate weights, in slot order of first occurrence
+__device__ inline int token_rows(const RowsArgs& a, const int32_t* s_lidx, int64_t t, int* grp,
+                                 float* wsum) {
+    int n = 0;
+    for (int s = 0; s < a.k; ++s) {
+        const int64_t o = t * a.k + s;
+        if (a.exec_m[o] != a.server) continue;
+        const int e = a.exec_k[o];
+        const int ls = (e >= 0 && e < a.E) ? s_lidx[e] : -1;
+        if (ls < 0) continue;
+        int i = 0;
+        while (i < n && grp[i] != ls) ++i;
+        if (i == n) { grp[n] = ls; wsum[n] = a.w[o]; ++n; }
+        else wsum[i] = wsum[i] + a.w[o];
+    }
+    if (a.has_shared && a.loc_in[t] == a.server) { grp[n] = a.n_local; wsum[n] = 1.0f; ++n; }
+    return n;
+}
+
+__global__ void __launch_bounds__(FT_TB) rows_count_kernel(const RowsArgs a) {
+    __shared__ int32_t s_lidx[ORDERMOE_MAX_EXPERTS];
+    __shared__ int32_t s_h[MAXG];
+    const int G = a.n_local + a.has_shared;
+    for (int i = threadIdx.x; i < a.E; i += FT_TB) s_lidx[i] = a.lidx[i];
+    for (int i = threadIdx.x; i < G; i += FT_TB) s_h[i] = 0;
+    __syncthreads();
+    const int64_t t = (int64_t)blockIdx.x * FT_TB + threadIdx.x;
+    if (t < a.T) {
+        int grp[MAXR];
+        float ws[MAXR];
+        const int n = token_rows(a, s_lidx, t, grp, ws);
+        for (int i = 0; i < n; ++i) atomicAdd(&s_h[grp[i]], 1);
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < G; i += FT_TB) a.blk_rows[(int64_t)blockIdx.x * G + i] = s_h[i];
+}
+
+constexpr int SCAN_THREADS = 1024;
+
+__global__ void __launch_bounds__(SCAN_THREADS) rows_scan_kernel(const RowsArgs a) {
+    __shared__ int32_t s_scan[SCAN_THREADS / 64];
+    __shared__ int32_t s_tot[MAXG];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int G = a.n_local + a.has_shared;
+    int32_t start = 0;
+    for (int g = 0; g < G; ++g) {
+        int32_t carry = start;
+        for (int b0 = 0; b0 < a.nblk; b0 += SCAN_THREADS) {
+            const int b = b0 + tid;
+            const int32_t v = b < a.nblk ? a.blk_rows[(int64_t)b * G + g] : 0;
+            int32_t inc = v;
+            for (int off = 1; off < 64; off <<= 1) {
+                int32_t o = __shfl_up(inc, off);
+                if (lane >= off) inc += o;
+            }
+            if (lane == 63) s_scan[wave] = inc;
+            __syncthreads();
+            int32_t wbase = 0, ctot = 0;
+            for (int w = 0; w < SCAN_THREADS / 64; ++w) {
+                if (w < wave) wbase += s_scan[w];
+                ctot += s_scan[w];
+            }
+            if (b < a.nblk) a.blk_base[(int64_t)b * G + g] = carry + wbase + inc - v;
+            carry += ctot;
+            __syncthreads();
+        }
+        if (tid == 0) s_tot[g] = carry - start;
+        start = carry;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        int32_t off = 0;
+        int64_t tiles_gu = 0, tiles_dn = 0;
+        for (int g = 0; g <= a.n_local; ++g) {
+            a.row_offsets[g] = off;
+            const int32_t R = (g < G) ? s_tot[g] : 0;
+            const bool sh = g == a.n_local;
+            if (g < G) {
+                tiles_gu += (int64_t)((R + a.bm_gu - 1) / a.bm_gu) * ((sh ? a.n_gu_s : a.n_gu_r) / a.bn_gu);
+                tiles_dn += (int64_t)((R + a.bm_dn - 1) / a.bm_dn) * (a.n_dn / a.bn_dn);
+            }
+            off += R;
+        }
+        a.row_offsets[a.n_local + 1] = off;
+        a.tile_info[0] = (int32_t)tiles_gu;
+        a.tile_info[1] = (int32_t)tiles_dn;
+        a.tile_info[2] = off;
+        a.tile_info[3] = 0;
+    }
+}
+
+__global__ void __launch_bounds__(FT_TB) rows_scatter_kernel(const RowsArgs a) {
+    __shared__ int32_t s_lidx[ORDERMOE_MAX_EXPERTS];
+    __shared__ int32_t s_wcnt[FT_TB / 64][MAXG];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int G = a.n_local + a.has_shared;
+    for (int i = tid; i < a.E; i += FT_TB) s_lidx[i] = a.lidx[i];
+    __syncthreads();
+    const int64_t t = (int64_t)blockIdx.x * FT_TB + tid;
+    int grp[MAXR], rank[MAXR];
+    float ws[MAXR];
+    const int n = t < a.T ? token_rows(a, s_lidx, t, grp, ws) : 0;
+    for (int g = 0; g < G; ++g) {
+        int has = -1;
+        for (int i = 0; i < n; ++i) if (grp[i] == g) has = i;
+        const uint64_t bal = __ballot(has >= 0);
+        if (lane == 0) s_wcnt[wave][g] = __popcll(bal);
+        if (has >= 0) rank[has] = __popcll(bal & ((1ull << lane) - 1ull));
+    }
+    __syncthreads();
+    if (t < a.T) {
+        const int stride = a.k + 1;
+        for (int i = 0; i < n; ++i) {
+            const int g = grp[i];
+            int32_t pos = a.blk_base[(int64_t)blockIdx.x * G + g] + rank[i];
+            for (int w = 0; w < wave; ++w) pos += s_wcnt[w][g];
+            a.row_tok[pos] = (int32_t)t;
+            a.row_w[pos] = ws[i];
+            a.tok_rows[t * stride + i] = pos;
+        }
+        for (int i = n; i < stride; ++i) a.tok_rows[t * stride + i] = -1;
+    }
+}
+
+// ---------------------------------------------------------------- GEMMs
+struct GemmArgs {
+    const int32_t* offsets;   // [G + 1] row offsets of the groups (device)
+    const int32_t* ntiles;    // device: number of tiles
+    int G, n_routed;          // groups; groups >= n_routed are the shared group
+    int Nr, Kr, Ns, Ks;       // N, K of routed and shared groups
+    const void* Wr;           // [n_routed][Nr][Kr]
+    const void* Ws;           // [Ns][Ks]
+    const void* X;            // mode 0: token rows [T][ldx]
+    const int32_t* row_tok;   // mode 0
+    int ldx;
+    const void* Ar;           // mode 1: routed activations [*][Kr]
+    const void* As;           // mode 1: shared activations [*][Ks]
+    void* Or;                 // mode 0: routed activations out; mode 1: row outputs [*][Nr]
+    void* Os;                 // mode 0: shared activations out; mode 1: unused
+    const float* row_w;       // mode 1
+};
+
+struct TileLoc {
+    int g, m0, n0, R, N, K, rowbase;
+};
+
+template <int BM, int BN>
+__device__ inline bool decode_tile(const GemmArgs& p, int tile, TileLoc& L) {
+    int rem = tile;
+    for (int g = 0; g < p.G; ++g) {
+        const int off = p.offsets[g];
+        const int R = p.offsets[g + 1] - off;
+        const bool sh = g >= p.n_routed;
+        const int N = sh ? p.Ns : p.Nr;
+        const int mt = (R + BM - 1) / BM;
+        const int cnt = mt * (N / BN);
+        if (rem < cnt) {
+            L.g = g; L.R = R; L.N = N; L.K = sh ? p.Ks : p.Kr; L.rowbase = off;
+            L.m0 = (rem % mt) * BM;
+            L.n0 = (rem / mt) * BN;
+            return true;
+        }
+        rem -= cnt;
+    }
+    return false;
+}
+
+__device__ inline float silu_f(float g) { return g / (1.0f + __expf(-g)); }
+
+template <int BM, int BN, int MODE>
+__global__ void __launch_bounds__(256) ggemm_bf16(const GemmArgs p) {
+    constexpr int BK = 64, LDK = BK + 8;        // padded LDS rows: conflict-free 16-B reads
+    constexpr int WM = BM / 2, WN = BN / 2;     // 2 x 2 waves
+    constexpr int FM = WM / 16, FN = WN / 16;   // 16x16 MFMA blocks per wave
+    constexpr int AV = BM * BK / 8 / 256;       // 16-B vectors per thread per K tile
+    constexpr int BV = BN * BK / 8 / 256;
+    static_assert(FN % 2 == 0, "gate/up pairs need an even number of N blocks");
+    extern __shared__ __attribute__((aligned(16))) char lds_raw[];
+    __bf16* sA = (__bf16*)lds_raw;                  // [2][BM][LDK]
+    __bf16* sB = sA + 2 * BM * LDK;                 // [2][BN][LDK]
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int total = *p.ntiles;
+    const int per_xcd = gridDim.x >> 3;
+    const int vid = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+
+    for (int tile = vid; tile < total; tile += gridDim.x) {
+        TileLoc L;
+        if (!decode_tile<BM, BN>(p, tile, L)) break;
+        const bool shared = L.g >= p.n_routed;
+        const __bf16* Bw = shared ? (const __bf16*)p.Ws
+                                  : (const __bf16*)p.Wr + (int64_t)L.g * L.N * L.K;
+        // per-thread global row pointers of this tile
+        const __bf16* arow[AV];
+        bool aok[AV];
+#pragma unroll
+        for (int v = 0; v < AV; ++v) {
+            const int id = v * 256 + tid, r = id >> 3, ch = id & 7;
+            const int row = L.m0 + r;
+            aok[v] = row < L.R;
+            const int rr = aok[v] ? row : 0;
+            if (MODE == 0) {
+                const int tok = p.row_tok[L.rowbase + rr];
+                arow[v] = (const __bf16*)p.X + (int64_t)tok * p.ldx + ch * 8;
+            } else {
+                const __bf16* base = shared ? (const __bf16*)p.As
+                                            : (const __bf16*)p.Ar + (int64_t)L.rowbase * L.K;
+                arow[v] = base + (int64_t)rr * L.K + ch * 8;
+            }
+        }
+        const __bf16* brow[BV];
+#pragma unroll
+        for (int v = 0; v < BV; ++v) {
+            const int id = v * 256 + tid, r = id >> 3, ch = id & 7;
+            brow[v] = Bw + (int64_t)(L.n0 + r) * L.K + ch * 8;
+        }
+        f32x4 acc[FM][FN];
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+        bf16x8 ra[AV], rb[BV];
+        const bf16x8 zero8 = {};
+        auto gload = [&](int k0) {
+#pragma unroll
+            for (int v = 0; v < AV; ++v) ra[v] = aok[v] ? *(const bf16x8*)(arow[v] + k0) : zero8;
+#pragma unroll
+            for (int v = 0; v < BV; ++v) rb[v] = *(const bf16x8*)(brow[v] + k0);
+        };
+        auto sstore = [&](int buf) {
+            __bf16* a = sA + buf * BM * LDK;
+            __bf16* b = sB + buf * BN * LDK;
+#pragma unroll
+            for (int v = 0; v < AV; ++v) {
+                const int id = v * 256 + tid;
+                *(bf16x8*)(a + (id >> 3) * LDK + (id & 7) * 8) = ra[v];
+            }
+#pragma unroll
+            for (int v = 0; v < BV; ++v) {
+                const int id = v * 256 + tid;
+                *(bf16x8*)(b + (id >> 3) * LDK + (id & 7) * 8) = rb[v];
+            }
+        };
+        const int KT = L.K / BK;
+        gload(0);
+        sstore(0);
+        __syncthreads();
+        for (int kt = 0; kt < KT; ++kt) {
+            if (kt + 1 < KT) gload((kt + 1) * BK);
+            const __bf16* a = sA + (kt & 1) * BM * LDK + (wm * WM + (lane & 15)) * LDK + (lane >> 4) * 8;
+            const __bf16* b = sB + (kt & 1) * BN * LDK + (wn * WN + (lane & 15)) * LDK + (lane >> 4) * 8;
+#pragma unroll
+            for (int ks = 0; ks < BK / 32; ++ks) {
+                bf16x8 af[FM], bfm[FN];
+#pragma unroll
+                for (int i = 0; i < FM; ++i) af[i] = *(const bf16x8*)(a + i * 16 * LDK + ks * 32);
+#pragma unroll
+                for (int j = 0; j < FN; ++j) bfm[j] = *(const bf16x8*)(b + j * 16 * LDK + ks * 32);
+#pragma unroll
+                for (int i = 0; i < FM; ++i)
+#pragma unroll
+                    for (int j = 0; j < FN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfm[j], acc[i][j], 0, 0, 0);
+            }
+            if (kt + 1 < KT) sstore((kt + 1) & 1);
+            __syncthreads();
+        }
+
+        // epilogue: lane holds rows (lane/16)*4 + e, column lane%16 of each block
+        const int rbase = L.m0 + wm * WM + (lane >> 4) * 4;
+        if (MODE == 0) {
+            __bf16* out = shared ? (__bf16*)p.Os : (__bf16*)p.Or;
+            const int ldo = L.N / 2;
+            const int orow0 = shared ? 0 : L.rowbase;
+            const int cbase = (L.n0 + wn * WN) / 2 + (lane & 15);
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int row = rbase + i * 16 + e;
+                    if (row < L.R) {
+#pragma unroll
+                        for (int q = 0; q < FN / 2; ++q) {
+                            const float gv = acc[i][2 * q][e], uv = acc[i][2 * q + 1][e];
+                            out[(int64_t)(orow0 + row) * ldo + cbase + q * 16] = (__bf16)(silu_f(gv) * uv);
+                        }
+                    }
+                }
+        } else {
+            __bf16* out = (__bf16*)p.Or;
+            const int ldo = L.N;
+            const int cbase = L.n0 + wn * WN + (lane & 15);
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int row = rbase + i * 16 + e;
+                    if (row < L.R) {
+                        const float wr = p.row_w[L.rowbase + row];
+#pragma unroll
+                        for (int j = 0; j < FN; ++j)
+                            out[(int64_t)(L.rowbase + row) * ldo + cbase + j * 16] = (__bf16)(acc[i][j][e] * wr);
+                    }
+                }
+        }
+    }
+}
+
+// fp32 storage: plain LDS-tiled FMA GEMM, 64 x 64 tiles, 4 x 4 outputs per thread
+template <int MODE>
+__global__ void __launch_bounds__(256) ggemm_f32(const GemmArgs p) {
+    constexpr int BM = 64, BN = 64, BK = 16;
+    __shared__ float sA[BK][BM + 4];
+    __shared__ float sB[BK][BN + 4];
+    const int tid = threadIdx.x;
+    const int tx = tid & 15, ty = tid >> 4;
+    const int total = *p.ntiles;
+    for (int tile = blockIdx.x; tile < total; tile += gridDim.x) {
+        TileLoc L;
+        if (!decode_tile<BM, BN>(p, tile, L)) break;
+        const bool shared = L.g >= p.n_routed;
+        const float* Bw = shared ? (const float*)p.Ws : (const float*)p.Wr + (int64_t)L.g * L.N * L.K;
+        float acc[4][4] = {};
+        for (int k0 = 0; k0 < L.K; k0 += BK) {
+            // A tile: 64 rows x 16 k, B tile: 64 cols x 16 k (4 elements per thread each)
+            for (int v = 0; v < 4; ++v) {
+                const int id = v * 256 + tid, r = id >> 4, kk = id & 15;
+                const int row = L.m0 + r;
+                float av = 0.f;
+                if (row < L.R) {
+                    if (MODE == 0) {
+                        const int tok = p.row_tok[L.rowbase + row];
+                        av = ((const float*)p.X)[(int64_t)tok * p.ldx + k0 + kk];
+                    } else {
+                        const float* base = shared ? (const float*)p.As
+                                                   : (const float*)p.Ar + (int64_t)L.rowbase * L.K;
+                        av = base[(int64_t)row * L.K + k0 + kk];
+                    }
+                }
+                sA[kk][r] = av;
+                sB[kk][r] = Bw[(int64_t)(L.n0 + r) * L.K + k0 + kk];
+            }
+            __syncthreads();
+#pragma unroll
+            for (int kk = 0; kk < BK; ++kk) {
+                float a4[4], b4[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) { a4[i] = sA[kk][ty * 4 + i]; b4[i] = sB[kk][tx * 4 + i]; }
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a4[i], b4[j], acc[i][j]);
+            }
+            __syncthreads();
+        }
+        if (MODE == 1) {
+            float* out = (float*)p.Or;
+            for (int i = 0; i < 4; ++i) {
+                const int row = L.m0 + ty * 4 + i;
+                if (row >= L.R) continue;
+                const float wr = p.row_w[L.rowbase + row];
+                for (int j = 0; j < 4; ++j)
+                    out[(int64_t)(L.rowbase + row) * L.N + L.n0 + tx * 4 + j] = acc[i][j] * wr;
+            }
+        }
+        if (MODE == 0) {
+            // packed rows alternate 16 gate / 16 up columns: pair them up
+            // through LDS, then write silu(g) * u
+            __shared__ float sC[BM][BN + 1];
+            for (int i = 0; i < 4; ++i)
+                for (int j = 0; j < 4; ++j) sC[ty * 4 + i][tx * 4 + j] = acc[i][j];
+            __syncthreads();
+            float* out = shared ? (float*)p.Os : (float*)p.Or;
+            const int ldo = L.N / 2;
+            for (int idx = tid; idx < BM * (BN / 2); idx += 256) {
+                const int r = idx / (BN / 2), c = idx % (BN / 2);   // activation column within tile
+                const int row = L.m0 + r;
+                if (row >= L.R) continue;
+                const int blk = c >> 4, cc = c & 15;
+                const float gv = sC[r][blk * 32 + cc], uv = sC[r][blk * 32 + 16 + cc];
+                const int orow = (shared ? 0 : L.rowbase) + row;
+                out[(int64_t)orow * ldo + L.n0 / 2 + c] = silu_f(gv) * uv;
+            }
+            __syncthreads();
+        }
+    }
+}
+
+struct CombineArgs {
+    int64_t T;
+    int d, stride, dtype;
+    const int32_t* tok_rows;
+    const void* obuf;
+    void* y;
+};
+
+__global__ void __launch_bounds__(256) combine_kernel(const CombineArgs c) {
+    const int64_t t = blockIdx.x;
+    int rows[MAXR];
+    int n = 0;
+    for (int i = 0; i < c.stride; ++i) {
+        const int r = c.tok_rows[t * c.stride + i];
+        if (r >= 0) rows[n++] = r;
+    }
+    if (c.dtype == ORDERMOE_BF16) {
+        const __bf16* O = (const __bf16*)c.obuf;
+        __bf16* Y = (__bf16*)c.y + t * c.d;
+        for (int col = threadIdx.x * 8; col < c.d; col += 256 * 8) {
+            float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+            for (int i = 0; i < n; ++i) {
+                const bf16x8 v = *(const bf16x8*)(O + (int64_t)rows[i] * c.d + col);
+#pragma unroll
+                for (int q = 0; q < 8; ++q) s[q] += (float)v[q];
+            }
+            bf16x8 o;
+#pragma unroll
+            for (int q = 0; q < 8; ++q) o[q] = (__bf16)s[q];
+            *(bf16x8*)(Y + col) = o;
+        }
+    } else {
+        const float* O = (const float*)c.obuf;
+        float* Y = (float*)c.y + t * c.d;
+        for (int col = threadIdx.x; col < c.d; col += 256) {
+            float s = 0.f;
+            for (int i = 0; i < n; ++i) s += O[(int64_t)rows[i] * c.d + col];
+            Y[col] = s;
+        }
+    }
+}
+
+
+constexpr int GU_BM = 256, GU_BN = 256, DN_BM = 256, DN_BN = 256;   // bf16 GEMM tiles
+constexpr int F32_BM = 64, F32_BN = 64;
+
+template <int BM, int BN>
+constexpr size_t bf16_gemm_lds() { return (size_t)2 * (BM + BN) * (64 + 8) * 2; }
+
+template <typename K>
+int set_lds(K kernel, size_t bytes) {
+    return (int)hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                    (int)bytes);
+}
+
+int persistent_grid(int64_t upper_tiles, int per_cu) {
+    int dev = 0, cus = 256;
+    if (hipGetDevice(&dev) == hipSuccess) {
+        int v = 0;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0) cus = v;
+    }
+    int64_t g = (int64_t)cus * per_cu;
+    if (upper_tiles < g) g = upper_tiles;
+    g = (g + 7) & ~int64_t(7);
+    return (int)(g < 8 ? 8 : g);
+}
+
+}  // namespace
+
+int forward_tokens_per_block() { return FT_TB; }
+
+void forward_tile_shape(int dtype, int* bm_gu, int* bn_gu, int* bm_dn, int* bn_dn) {
+    if (dtype == ORDERMOE_BF16) { *bm_gu = GU_BM; *bn_gu = GU_BN; *bm_dn = DN_BM; *bn_dn = DN_BN; }
+    else { *bm_gu = F32_BM; *bn_gu = F32_BN; *bm_dn = F32_BM; *bn_dn = F32_BN; }
+}
+
+int launch_local_forward(const ForwardArgs& f, void* stream) {
+    hipStream_t st = (hipStream_t)stream;
+    const int has_sh = f.n_shared > 0 ? 1 : 0;
+    const int G = f.n_local + has_sh;
+    int bm_gu, bn_gu, bm_dn, bn_dn;
+    forward_tile_shape(f.dtype, &bm_gu, &bn_gu, &bm_dn, &bn_dn);
+
+    RowsArgs r;
+    r.T = f.T; r.k = f.k; r.E = f.E; r.n_local = f.n_local; r.has_shared = has_sh; r.server = f.server;
+    r.w = f.w; r.exec_k = f.exec_k; r.exec_m = f.exec_m; r.loc_in = f.loc_in;
+    for (int i = 0; i < ORDERMOE_MAX_EXPERTS; ++i) r.lidx[i] = f.lidx[i];
+    r.blk_rows = f.blk_rows; r.blk_base = f.blk_base; r.row_offsets = f.row_offsets;
+    r.row_tok = f.row_tok; r.row_w = f.row_w; r.tok_rows = f.tok_rows; r.tile_info = f.tile_info;
+    r.nblk = f.nblk;
+    r.bm_gu = bm_gu; r.bn_gu = bn_gu; r.bm_dn = bm_dn; r.bn_dn = bn_dn;
+    r.n_gu_r = 2 * f.f; r.n_gu_s = 2 * f.n_shared * f.f; r.n_dn = f.d;
+
+    hipError_t e;
+    if (f.nblk > 0) {
+        {
+        KernelTimer kt_("rows_count", st);
+        hipLaunchKernelGGL(rows_count_kernel, dim3(f.nblk), dim3(FT_TB), 0, st, r);
+        }
+        if ((e = hipGetLastError()) != hipSuccess) return (int)e;
+    }
+    {
+        KernelTimer kt_("rows_scan", st);
+        hipLaunchKernelGGL(rows_scan_kernel, dim3(1), dim3(SCAN_THREADS), 0, st, r);
+        }
+    if ((e = hipGetLastError()) != hipSuccess) return (int)e;
+    if (f.nblk == 0) return 0;
+    {
+        KernelTimer kt_("rows_scatter", st);
+        hipLaunchKernelGGL(rows_scatter_kernel, dim3(f.nblk), dim3(FT_TB), 0, st, r);
+        }
+    if ((e = hipGetLastError()) != hipSuccess) return (int)e;
+
+    GemmArgs g;
+    g.offsets = f.row_offsets; g.G = G; g.n_routed = f.n_local;
+    g.X = f.x; g.row_tok = f.row_tok; g.ldx = f.d; g.row_w = f.row_w;
+
+    // gate/up: [rows][d] x [2f][d]^T -> activations [rows][f]
+    g.ntiles = f.tile_info + 0;
+    g.Nr = 2 * f.f; g.Kr = f.d; g.Ns = 2 * f.n_shared * f.f; g.Ks = f.d;
+    g.Wr = f.w_gu; g.Ws = f.w_sh_gu; g.Ar = nullptr; g.As = nullptr; g.Or = f.act_r; g.Os = f.act_s;
+    const int64_t rows_r = f.rmax_routed, rows_s = has_sh ? f.T : 0;
+    int64_t ub_gu = ((rows_r + bm_gu - 1) / bm_gu + f.n_local) * (2 * f.f / bn_gu) +
+                    (has_sh ? ((rows_s + bm_gu - 1) / bm_gu + 1) * (2 * f.n_shared * f.f / bn_gu) : 0);
+    int64_t ub_dn = ((rows_r + rows_s + bm_dn - 1) / bm_dn + G) * (f.d / bn_dn);
+
+    if (f.dtype == ORDERMOE_BF16) {
+        static int lds_ok = -1;
+        if (lds_ok < 0) {
+            lds_ok = set_lds(ggemm_bf16<GU_BM, GU_BN, 0>, bf16_gemm_lds<GU_BM, GU_BN>()) |
+                     set_lds(ggemm_bf16<DN_BM, DN_BN, 1>, bf16_gemm_lds<DN_BM, DN_BN>());
+        }
+        if (lds_ok) return lds_ok;
+        {
+        KernelTimer kt_("gemm_gate_up", st);
+        ggemm_bf16<GU_BM, GU_BN, 0>
+            <<<dim3(persistent_grid(ub_gu, 1)), dim3(256), bf16_gemm_lds<GU_BM, GU_BN>(), st>>>(g);
+        }
+        if ((e = hipGetLastError()) != hipSuccess) return (int)e;
+    } else {
+        {
+        KernelTimer kt_("gemm_gate_up", st);
+        ggemm_f32<0><<<dim3(persistent_grid(ub_gu, 4)), dim3(256), 0, st>>>(g);
+        }
+        if ((e = hipGetLastError()) != hipSuccess) return (int)e;
+    }
+
+    // down: activations [rows][f] x [d][f]^T -> row outputs [rows][d], scaled by the gate
+    g.ntiles = f.tile_info + 1;
+    g.Nr = f.d; g.Kr = f.f; g.Ns = f.d; g.Ks = f.n_shared * f.f;
+    g.Wr = f.w_dn; g.Ws = f.w_sh_dn; g.Ar = f.act_r; g.As = f.act_s; g.Or = f.obuf; g.Os = nullptr;
+    if (f.dtype == ORDERMOE_BF16) {
+        {
+        KernelTimer kt_("gemm_down", st);
+        ggemm_bf16<DN_BM, DN_BN, 1>
+            <<<dim3(persistent_grid(ub_dn, 1)), dim3(256), bf16_gemm_lds<DN_BM, DN_BN>(), st>>>(g);
+        }
+    } else {
+        {
+        KernelTimer kt_("gemm_down", st);
+        ggemm_f32<1><<<dim3(persistent_grid(ub_dn, 4)), dim3(256), 0, st>>>(g);
+        }
+    }
+    if ((e = hipGetLastError()) != hipSuccess) return (int)e;
+
+    CombineArgs c;
+    c.T = f.T; c.d = f.d; c.stride = f.k + 1; c.dtype = f.dtype; c.tok_rows = f.tok_rows;
+    c.obuf = f.obuf; c.y = f.y;
+    {
+        KernelTimer kt_("combine", st);
+        hipLaunchKernelGGL(combine_kernel, dim3((unsigned)f.T), dim3(256), 0, st, c);
+        }
+    if ((e = hipGetLastError()) != hipSuccess) return (int)e;
+    return 0;
+}
+
+}  // namespace ordermoe

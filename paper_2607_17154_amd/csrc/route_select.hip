@@ -1,0 +1,407 @@
+// Routing and runtime server-expert selection of one MoE layer on gfx950.
+//
+// Kernel 1 (route_select_kernel), one block per RT_TB tokens:
+//   * router logits l = x W_r^T (eq 3, one token at a time):
+//       bf16: v_mfma_f32_16x16x32_bf16, the block's 16 tokens x all experts,
+//             d split over the 4 waves, partial sums added in wave order;
+//       fp32: fp64 dot products (exact products), rounded once to fp32;
+//   * per token (16 lanes each): top-(k+1) by a 64-bit (logit, -index) key
+//     max-reduced over the lanes, gates, margin and flag;
+//   * per slot in rank order: the candidate search of eq (40)/(43) -- lane 0
+//     takes the exact candidate, lane j the (j-1)-th substitute of the LDS-
+//     staged table; each lane scans the servers holding its expert and keeps a
+//     64-bit key (J, position, remote, server); a min-reduce over the 16 lanes
+//     gives (m*, k*); the budget is updated as eq (44);
+//   * per-block counters and per-destination remote-slot counts.
+// Kernel 2 (dispatch_scan_kernel), one block: exclusive scans of the
+//   per-block destination counts, totals of the counters.
+// Kernel 3 (dispatch_scatter_kernel), one block per RT_TB tokens: stable
+//   placement of the block's remote slots into the (destination, token, slot)
+//   ordered dispatch list.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "common.hpp"
+
+namespace ordermoe {
+namespace {
+
+constexpr int RT_TB = 16;        // tokens per block
+constexpr int RT_THREADS = 256;  // 4 waves; 16 lanes per token in the token stage
+constexpr int RT_WAVES = RT_THREADS / 64;
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// order-preserving map of fp32 onto uint32
+__device__ inline uint32_t f2ord(float v) {
+    uint32_t u = __float_as_uint(v);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ inline float ord2f(uint32_t o) {
+    uint32_t u = (o & 0x80000000u) ? (o & 0x7FFFFFFFu) : ~o;
+    return __uint_as_float(u);
+}
+
+__device__ inline uint64_t shfl_xor64(uint64_t v, int mask) {
+    uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
+    lo = __shfl_xor(lo, mask, 16);
+    hi = __shfl_xor(hi, mask, 16);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+__global__ void __launch_bounds__(RT_THREADS)
+route_select_kernel(const RouteArgs a) {
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int64_t t0 = (int64_t)blockIdx.x * RT_TB;
+    const int E = a.E, d = a.d, k = a.k, M = a.M;
+    const int Epad = (E + 15) & ~15;
+
+    extern __shared__ float smem[];
+    float* s_part = smem;                               // [RT_WAVES][RT_TB][Epad]
+    float* s_logit = smem;                              // reuses partition 0 after the sum
+    int32_t* s_t1k = (int32_t*)(smem + RT_WAVES * RT_TB * Epad);   // [E][gmax]
+    float* s_t1q = (float*)(s_t1k + E * a.gmax);                   // [E][gmax]
+    int32_t* s_t1n = (int32_t*)(s_t1q + E * a.gmax);               // [E]
+    uint32_t* s_mask = (uint32_t*)(s_t1n + E);                     // [E]
+    int* s_cnt = (int*)(s_mask + E);                               // [8 + M]
+
+    // stage the candidate tables (small) and clear the block counters
+    for (int i = tid; i < E * a.gmax; i += RT_THREADS) { s_t1k[i] = a.t1_k[i]; s_t1q[i] = a.t1_q[i]; }
+    for (int i = tid; i < E; i += RT_THREADS) { s_t1n[i] = a.t1_n[i]; s_mask[i] = a.srvmask[i]; }
+    for (int i = tid; i < 8 + M; i += RT_THREADS) s_cnt[i] = 0;
+
+    // ---------------- router logits ----------------
+    if (a.dtype == ORDERMOE_BF16) {
+        const __bf16* X = (const __bf16*)a.x;
+        const __bf16* W = (const __bf16*)a.w_router;
+        const int nblk = Epad / 16;
+        const int kq = d / RT_WAVES;                 // d % 64 == 0 -> kq % 16 == 0
+        const int kbeg = wave * kq, kend = kbeg + kq;
+        const int r16 = lane & 15, kg = (lane >> 4) * 8;
+        const int64_t tok = t0 + r16;
+        const bool tok_ok = tok < a.T;
+        const __bf16* xrow = X + (tok_ok ? tok : 0) * (int64_t)d;
+        f32x4 acc[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+        const bf16x8 zero8 = {};
+        for (int kk = kbeg; kk < kend; kk += 32) {
+            bf16x8 av = tok_ok ? *(const bf16x8*)(xrow + kk + kg) : zero8;
+#pragma unroll
+            for (int nb = 0; nb < 16; ++nb) {
+                if (nb < nblk) {
+                    const int e = nb * 16 + r16;
+                    bf16x8 bv = e < E ? *(const bf16x8*)(W + (int64_t)e * d + kk + kg) : zero8;
+                    acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bv, acc[nb], 0, 0, 0);
+                }
+            }
+        }
+        // acc[nb][i] = partial logit of token (lane/16)*4 + i, expert nb*16 + lane%16
+#pragma unroll
+        for (int nb = 0; nb < 16; ++nb) {
+            if (nb < nblk) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int tr = (lane >> 4) * 4 + i;
+                    s_part[(wave * RT_TB + tr) * Epad + nb * 16 + r16] = acc[nb][i];
+                }
+            }
+        }
+        __syncthreads();
+        for (int i = tid; i < RT_TB * Epad; i += RT_THREADS) {
+            float v = s_part[i];
+            for (int w = 1; w < RT_WAVES; ++w) v += s_part[w * RT_TB * Epad + i];
+            s_logit[i] = v;
+        }
+    } else {
+        const float* X = (const float*)a.x;
+        const float* W = (const float*)a.w_router;
+        for (int p = tid; p < RT_TB * Epad; p += RT_THREADS) {
+            const int tr = p / Epad, e = p % Epad;
+            const int64_t tok = t0 + tr;
+            float v = 0.f;
+            if (tok < a.T && e < E) {
+                const float* xr = X + tok * (int64_t)d;
+                const float* wr = W + (int64_t)e * d;
+                double s = 0.0;
+                for (int i = 0; i < d; ++i) s = fma((double)xr[i], (double)wr[i], s);
+                v = (float)s;
+            }
+            s_logit[p] = v;
+        }
+    }
+    __syncthreads();
+
+    // ---------------- per-token stage: 16 lanes per token ----------------
+    const int g = lane >> 4;                 // token within the wave
+    const int j = lane & 15;                 // lane within the token group
+    const int tr = wave * 4 + g;             // token within the block
+    const int64_t t = t0 + tr;
+    const bool valid = t < a.T;
+    const float* lg = s_logit + tr * Epad;
+
+    // top-(k+1) selection by (logit desc, index asc)
+    const int kk1 = (k + 1 < E) ? k + 1 : E;
+    uint32_t removed = 0;                    // bit i: local element j + 16 i taken
+    int sel_e[ORDERMOE_MAX_TOPK + 1];
+    float sel_v[ORDERMOE_MAX_TOPK + 1];
+#pragma unroll
+    for (int r = 0; r < ORDERMOE_MAX_TOPK + 1; ++r) {
+        if (r < kk1) {
+            uint64_t best = 0;
+            for (int i = 0, e = j; e < E; ++i, e += 16) {
+                if (removed & (1u << i)) continue;
+                uint64_t key = ((uint64_t)f2ord(lg[e]) << 32) | (uint32_t)(0xFFFFu - (uint32_t)e);
+                best = key > best ? key : best;
+            }
+#pragma unroll
+            for (int off = 8; off >= 1; off >>= 1) {
+                uint64_t o = shfl_xor64(best, off);
+                best = o > best ? o : best;
+            }
+            const int e = (int)(0xFFFFu - (uint32_t)(best & 0xFFFFu));
+            sel_e[r] = e;
+            sel_v[r] = ord2f((uint32_t)(best >> 32));
+            if ((e & 15) == j) removed |= 1u << (e >> 4);
+        }
+    }
+    float mg = __builtin_inff();
+#pragma unroll
+    for (int r = 0; r < ORDERMOE_MAX_TOPK; ++r) {
+        if (r + 1 < kk1) {
+            float gap = sel_v[r] - sel_v[r + 1];
+            mg = gap < mg ? gap : mg;
+        }
+    }
+    // gates: softmax renormalised over the top-k, or over all experts
+    float den = 0.f;
+    if (a.renorm) {
+#pragma unroll
+        for (int r = 0; r < ORDERMOE_MAX_TOPK; ++r)
+            if (r < k) den += expf(sel_v[r] - sel_v[0]);
+    } else {
+        for (int e = j; e < E; e += 16) den += expf(lg[e] - sel_v[0]);
+#pragma unroll
+        for (int off = 8; off >= 1; off >>= 1) den += __shfl_xor(den, off, 16);
+    }
+
+    // server-expert selection, slots in rank order
+    const int s_loc = valid ? (int)a.loc_in[t] : 0;
+    const bool loc_ok = s_loc < M;
+    float qhat = valid ? a.qhat_in[t] : 0.f;
+    const bool subs_on = a.allow_sub && a.Qbar > 0.f;
+    const uint32_t mmask = M >= 32 ? 0xFFFFFFFFu : ((1u << M) - 1u);   // servers that exist
+    int first_m = s_loc, ncls[4] = {0, 0, 0, 0}, nremote = 0;
+    uint32_t dstmask = 0;
+#pragma unroll
+    for (int slot = 0; slot < ORDERMOE_MAX_TOPK; ++slot) {
+        if (slot >= k) break;
+        const int r = sel_e[slot];
+        int km = r, mm = s_loc;
+        float qsel = 0.f;
+        const uint32_t rmask = s_mask[r];
+        if (loc_ok && !(a.pin && ((rmask >> s_loc) & 1u))) {
+            // lane j holds candidate expert: j = 0 exact, j >= 1 substitute j-1
+            uint64_t key = ~0ull;
+            int ke = -1;
+            float qe = 0.f;
+            if (j == 0) { ke = r; qe = 0.f; }
+            else if (subs_on && j - 1 < s_t1n[r]) {
+                ke = s_t1k[r * a.gmax + j - 1];
+                qe = s_t1q[r * a.gmax + j - 1];
+                if (!(qhat + qe <= a.Qbar)) ke = -1;        // eq 40 budget test
+            }
+            if (ke >= 0 && ke < E) {
+                uint32_t ms = s_mask[ke] & mmask;
+                while (ms) {
+                    const int m = __builtin_ctz(ms);
+                    ms &= ms - 1;
+                    const float J = fmaf(a.cq, qe, a.S[((int64_t)s_loc * M + m) * E + ke]);
+                    const uint64_t cand = ((uint64_t)__float_as_uint(J) << 32) |
+                                          ((uint32_t)j << 6) | ((uint32_t)(m != s_loc) << 5) |
+                                          (uint32_t)m;
+                    key = cand < key ? cand : key;
+                }
+            }
+#pragma unroll
+            for (int off = 8; off >= 1; off >>= 1) {
+                uint64_t o = shfl_xor64(key, off);
+                key = o < key ? o : key;
+            }
+            const int pos = (int)((key >> 6) & 15u);
+            mm = (int)(key & 31u);
+            if (pos == 0) { km = r; qsel = 0.f; }
+            else { km = s_t1k[r * a.gmax + pos - 1]; qsel = s_t1q[r * a.gmax + pos - 1]; }
+        }
+        const int remote = mm != s_loc;
+        const int c = (remote << 1) | (km != r);
+        qhat = qhat + qsel;
+        if (slot == 0) first_m = mm;
+        if (valid && j == 0) {
+            const int64_t o = t * k + slot;
+            a.out.idx[o] = r;
+            a.out.w[o] = expf(sel_v[slot] - sel_v[0]) / den;
+            if (loc_ok) {
+                a.out.exec_k[o] = km;
+                a.out.exec_m[o] = (uint8_t)mm;
+                a.out.cls[o] = (uint8_t)c;
+                ncls[c]++;
+                if (remote) { nremote++; dstmask |= 1u << mm; atomicAdd(&s_cnt[8 + mm], 1); }
+            } else {
+                a.out.exec_k[o] = -1;
+                a.out.exec_m[o] = 255;
+                a.out.cls[o] = 255;
+            }
+        }
+    }
+    if (valid && j == 0) {
+        a.out.margin[t] = mg;
+        const int fl = mg < ORDERMOE_MARGIN_FLAG;
+        a.out.flag[t] = (uint8_t)fl;
+        a.out.qhat_out[t] = loc_ok ? qhat : a.qhat_in[t];
+        a.out.loc_out[t] = loc_ok ? (uint8_t)first_m : a.loc_in[t];
+        if (loc_ok) {
+            for (int c = 0; c < 4; ++c) if (ncls[c]) atomicAdd(&s_cnt[c], ncls[c]);
+            if (nremote) atomicAdd(&s_cnt[6], nremote);
+            if (dstmask) atomicAdd(&s_cnt[5], __builtin_popcount(dstmask));
+        } else {
+            atomicAdd(&s_cnt[7], 1);
+        }
+        if (fl) atomicAdd(&s_cnt[4], 1);
+    }
+    __syncthreads();
+    if (tid < 8) a.blk_cnt[(int64_t)blockIdx.x * 8 + tid] = s_cnt[tid];
+    if (tid < M) a.blk_dst[(int64_t)blockIdx.x * M + tid] = s_cnt[8 + tid];
+}
+
+constexpr int SCAN_THREADS = 1024;
+
+// Exclusive scan over blocks of the per-destination counts; destination
+// segments are laid out in server order.  Also totals the counters.
+__global__ void __launch_bounds__(SCAN_THREADS)
+dispatch_scan_kernel(const int32_t* blk_dst, const int64_t* blk_cnt, int nblk, int M,
+                     int32_t* dst_base, int32_t* dst_count, int64_t* counters) {
+    __shared__ int64_t s_red[SCAN_THREADS / 64];
+    __shared__ int32_t s_scan[SCAN_THREADS / 64];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    // counters
+    for (int c = 0; c < 8; ++c) {
+        int64_t v = 0;
+        for (int b = tid; b < nblk; b += SCAN_THREADS) v += blk_cnt[(int64_t)b * 8 + c];
+        for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+        if (lane == 0) s_red[wave] = v;
+        __syncthreads();
+        if (tid == 0) {
+            int64_t s = 0;
+            for (int w = 0; w < SCAN_THREADS / 64; ++w) s += s_red[w];
+            counters[c] = s;
+        }
+        __syncthreads();
+    }
+    int32_t start = 0;  // first list position of the current destination
+    for (int m = 0; m < M; ++m) {
+        int32_t carry = start;
+        for (int b0 = 0; b0 < nblk; b0 += SCAN_THREADS) {
+            const int b = b0 + tid;
+            const int32_t v = b < nblk ? blk_dst[(int64_t)b * M + m] : 0;
+            // inclusive scan within the wave
+            int32_t inc = v;
+            for (int off = 1; off < 64; off <<= 1) {
+                int32_t o = __shfl_up(inc, off);
+                if (lane >= off) inc += o;
+            }
+            if (lane == 63) s_scan[wave] = inc;
+            __syncthreads();
+            int32_t wbase = 0, ctot = 0;
+            for (int w = 0; w < SCAN_THREADS / 64; ++w) {
+                if (w < wave) wbase += s_scan[w];
+                ctot += s_scan[w];
+            }
+            if (b < nblk) dst_base[(int64_t)b * M + m] = carry + wbase + inc - v;
+            carry += ctot;
+            __syncthreads();
+        }
+        if (tid == 0) dst_count[m] = carry - start;
+        start = carry;
+    }
+}
+
+__global__ void __launch_bounds__(RT_THREADS)
+dispatch_scatter_kernel(const uint8_t* exec_m, const uint8_t* loc_in, int64_t T, int k, int M,
+                        const int32_t* dst_base, int32_t* dispatch) {
+    __shared__ int8_t s_dst[RT_TB * ORDERMOE_MAX_TOPK];
+    const int tid = threadIdx.x;
+    const int64_t t0 = (int64_t)blockIdx.x * RT_TB;
+    const int n = RT_TB * k;
+    if (tid < n) {
+        const int64_t t = t0 + tid / k;
+        int dst = -1;
+        if (t < T) {
+            const int s = loc_in[t];
+            const int m = exec_m[t * k + tid % k];
+            if (s < M && m != s) dst = m;
+        }
+        s_dst[tid] = (int8_t)dst;
+    }
+    __syncthreads();
+    if (tid < n && s_dst[tid] >= 0) {
+        const int dst = s_dst[tid];
+        int rank = 0;
+        for (int i = 0; i < tid; ++i) rank += (s_dst[i] == dst);
+        const int32_t pos = dst_base[(int64_t)blockIdx.x * M + dst] + rank;
+        dispatch[pos] = (int32_t)((t0 + tid / k) * k + tid % k);
+    }
+}
+
+}  // namespace
+
+int route_tokens_per_block() { return RT_TB; }
+
+size_t route_smem_bytes(int E, int gmax, int M) {
+    const int Epad = (E + 15) & ~15;
+    return sizeof(float) * (size_t)RT_WAVES * RT_TB * Epad + (size_t)E * gmax * 8 + (size_t)E * 8 +
+           sizeof(int) * (size_t)(8 + M);
+}
+
+int launch_route_select(const RouteArgs& a, void* stream) {
+    hipStream_t st = (hipStream_t)stream;
+    if (a.nblk > 0) {
+        const size_t smem = route_smem_bytes(a.E, a.gmax, a.M);
+        static size_t lds_limit = 65536;
+        if (smem > lds_limit) {
+            hipError_t e = hipFuncSetAttribute((const void*)route_select_kernel,
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+            if (e != hipSuccess) return (int)e;
+            lds_limit = smem;
+        }
+        {
+        KernelTimer kt_("route_select", st);
+        hipLaunchKernelGGL(route_select_kernel, dim3(a.nblk), dim3(RT_THREADS), smem, st, a);
+        }
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return (int)e;
+    }
+    {
+        KernelTimer kt_("dispatch_scan", st);
+        hipLaunchKernelGGL(dispatch_scan_kernel, dim3(1), dim3(SCAN_THREADS), 0, st, a.blk_dst,
+                       a.blk_cnt, a.nblk, a.M, a.dst_base, a.out.dst_count, a.out.counters);
+        }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return (int)e;
+    if (a.nblk > 0) {
+        {
+        KernelTimer kt_("dispatch_scatter", st);
+        hipLaunchKernelGGL(dispatch_scatter_kernel, dim3(a.nblk), dim3(RT_THREADS), 0, st,
+                           a.out.exec_m, a.loc_in, a.T, a.k, a.M, a.dst_base, a.out.dispatch);
+        }
+        e = hipGetLastError();
+        if (e != hipSuccess) return (int)e;
+    }
+    return 0;
+}
+
+}  // namespace ordermoe

@@ -1,0 +1,191 @@
+"""Test harness: one MoE layer instance built for both the oracle and the HIP
+library from the same seeded inputs.
+
+The offline model (similarity, groups, deployment) is the oracle's; the
+library builds its own decision tables from it with ordermoe_build_tables, and
+the tests check those tables against the oracle's.  Everything device-side
+goes through the library's C ABI.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import Dict, List, Optional
+
+import numpy as np
+
+import workloads as wl
+from oracle import layer as olayer
+from oracle import placement, route, similarity, tables
+
+
+@dataclass
+class Case:
+    cfg: wl.LayerConfig
+    W_r: np.ndarray
+    X: np.ndarray
+    loc: np.ndarray
+    qhat: np.ndarray
+    model: Dict
+    sim32: np.ndarray
+    x_dep: np.ndarray
+    net: wl.Network
+    c: np.ndarray
+    dref: float
+    z_bits: float
+    S: np.ndarray
+    local: List[int]
+    _experts: Dict[int, tuple] = field(default_factory=dict)
+    _shared: Optional[List[tuple]] = None
+
+    def expert(self, j: int):
+        if j not in self._experts:
+            self._experts[j] = wl.expert(self.cfg, j)
+        return self._experts[j]
+
+    def shared(self) -> List[tuple]:
+        if self._shared is None:
+            self._shared = [wl.shared_expert(self.cfg, i) for i in range(self.cfg.n_shared)]
+        return self._shared
+
+
+def build_case(cfg: wl.LayerConfig, T: Optional[int] = None, qhat_scale: float = 0.0) -> Case:
+    W = wl.router(cfg)
+    model = similarity.build(wl.calibration(cfg), W, cfg.k, cfg.theta, cfg.alpha_f)
+    x_dep, _ = placement.place([model["group_of"]], [model["I"]], [np.ones(cfg.E)],
+                               np.array(cfg.capacity), np.full(cfg.M, 1.0 / cfg.M), cfg.lambda1)
+    x_dep = x_dep[0]
+    net = wl.network(cfg)
+    c = np.full(cfg.E, 6.0 * cfg.d * cfg.f)
+    dref = tables.d_ref(c, net.F)
+    z_bits = 8.0 * cfg.d * cfg.bytes_per_el
+    S = tables.static_cost(cfg.M, cfg.E, z_bits, net.B, net.tau, c, net.F, dref, cfg.omega_T)
+    T = cfg.T if T is None else T
+    local = [int(j) for j in np.nonzero(x_dep[cfg.m0])[0]]
+    return Case(cfg=cfg, W_r=W, X=wl.tokens(cfg, T), loc=wl.token_locations(cfg, T),
+                qhat=wl.accumulated_loss(cfg, T, qhat_scale), model=model,
+                sim32=model["sim"].astype(np.float32), x_dep=x_dep, net=net, c=c, dref=dref,
+                z_bits=z_bits, S=S, local=local)
+
+
+def oracle_decisions(case: Case, Qbar: Optional[float] = None):
+    cfg = case.cfg
+    Qbar = cfg.Qbar if Qbar is None else Qbar
+    idx, w, margin, _ = route.route(case.X, case.W_r, cfg.k, cfg.renorm)
+    sel = olayer.select(idx, case.x_dep, case.sim32, case.model["group_of"], cfg.theta, case.S,
+                        Qbar, cfg.omega_Q, case.loc, case.qhat, cfg.pin_local_exact, cfg.allow_sub)
+    sel.update(idx=idx, w=w, margin=margin)
+    return sel
+
+
+def oracle_output(case: Case, dec: Dict, tokens: np.ndarray) -> np.ndarray:
+    return olayer.server_output(case.X, dec["w"], dec["exec_k"], dec["exec_m"], case.loc,
+                                case.cfg.m0, case.expert, case.shared(), tokens)
+
+
+# ------------------------------------------------------------------ device side
+def library_tables(case: Case, gmax: int = 15):
+    from paper_2607_17154_amd import ordermoe as om
+    cfg = case.cfg
+    return om.ordermoe_build_tables(case.sim32, case.model["group_of"], cfg.theta, case.x_dep,
+                                    case.net.B, case.net.tau, case.net.F, case.z_bits, case.c,
+                                    case.dref, cfg.omega_T, None, gmax)
+
+
+def to_device(a: np.ndarray, dtype: str, device="cuda"):
+    """Upload a float32 host array holding values of the run dtype."""
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32))
+    t = t.to(torch.bfloat16) if dtype == "bf16" else t
+    return t.to(device)
+
+
+class DeviceLayer:
+    """Device buffers and ABI structs of one layer on server m0."""
+
+    def __init__(self, case: Case, tabs: Dict, Qbar: Optional[float] = None, gmax: int = 15,
+                 with_experts: bool = True):
+        import torch
+        from paper_2607_17154_amd import ordermoe as om
+        cfg = case.cfg
+        self.case, self.cfg = case, cfg
+        self.code = om.BF16 if cfg.dtype == "bf16" else om.F32
+        dev = "cuda"
+        self.w_router = to_device(case.W_r, cfg.dtype)
+        self.tabs_dev = {n: torch.from_numpy(np.ascontiguousarray(v)).to(dev)
+                         for n, v in tabs.items() if n != "srvmask"}
+        self.tabs_dev["srvmask"] = torch.from_numpy(tabs["srvmask"].view(np.int32)).to(dev)
+        self.Qbar = cfg.Qbar if Qbar is None else Qbar
+        self.layer = om.make_layer(self.code, cfg.d, cfg.E, cfg.k, cfg.M, gmax, self.w_router,
+                                   self.tabs_dev, self.Qbar, cfg.omega_Q, cfg.pin_local_exact,
+                                   cfg.allow_sub, cfg.renorm)
+        self.experts = None
+        if with_experts:
+            self._upload_experts()
+
+    def _upload_experts(self):
+        import torch
+        from paper_2607_17154_amd import ordermoe as om
+        cfg, case = self.cfg, self.case
+        tdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+        n = len(case.local)
+        g = torch.empty((max(n, 1), cfg.f, cfg.d), dtype=tdt, device="cuda")
+        u = torch.empty_like(g)
+        dn = torch.empty((max(n, 1), cfg.d, cfg.f), dtype=tdt, device="cuda")
+        for i, j in enumerate(case.local):
+            Wg, Wu, Wd = case.expert(j)
+            g[i] = to_device(Wg, cfg.dtype)
+            u[i] = to_device(Wu, cfg.dtype)
+            dn[i] = to_device(Wd, cfg.dtype)
+        self.w_gu = torch.empty((max(n, 1), 2 * cfg.f, cfg.d), dtype=tdt, device="cuda")
+        om.ordermoe_pack_gate_up(g, u, self.w_gu)
+        self.w_dn = dn
+        self.w_sh_gu = self.w_sh_dn = None
+        if cfg.n_shared:
+            sh = case.shared()
+            sg = torch.cat([to_device(s[0], cfg.dtype) for s in sh], 0).unsqueeze(0).contiguous()
+            su = torch.cat([to_device(s[1], cfg.dtype) for s in sh], 0).unsqueeze(0).contiguous()
+            self.w_sh_gu = torch.empty((1, 2 * cfg.n_shared * cfg.f, cfg.d), dtype=tdt, device="cuda")
+            om.ordermoe_pack_gate_up(sg, su, self.w_sh_gu)
+            self.w_sh_dn = torch.cat([to_device(s[2], cfg.dtype) for s in sh], 1).contiguous()
+        torch.cuda.synchronize()
+        del g, u
+        self.experts = om.make_experts(self.code, cfg.d, cfg.f, cfg.E, case.local, self.w_gu,
+                                       self.w_dn, cfg.n_shared, self.w_sh_gu, self.w_sh_dn)
+
+    def inputs(self, X=None, loc=None, qhat=None):
+        import torch
+        case = self.case
+        X = case.X if X is None else X
+        loc = case.loc if loc is None else loc
+        qhat = case.qhat if qhat is None else qhat
+        return (to_device(X, self.cfg.dtype), torch.from_numpy(np.ascontiguousarray(loc)).cuda(),
+                torch.from_numpy(np.ascontiguousarray(qhat, dtype=np.float32)).cuda())
+
+    def route(self, x, loc, qhat, T: int):
+        import torch
+        from paper_2607_17154_amd import ordermoe as om
+        out = om.alloc_route_out(T, self.cfg.k, self.cfg.M, "cuda")
+        ws = torch.empty(max(om.ordermoe_route_workspace_size(T, self.cfg.k, self.cfg.M), 1),
+                         dtype=torch.uint8, device="cuda")
+        om.ordermoe_route_select(self.layer, x, T, loc, qhat, out, ws)
+        return out
+
+    def forward(self, x, loc, out, T: int, server: Optional[int] = None):
+        import torch
+        from paper_2607_17154_amd import ordermoe as om
+        server = self.cfg.m0 if server is None else server
+        tdt = torch.bfloat16 if self.cfg.dtype == "bf16" else torch.float32
+        y = torch.empty((T, self.cfg.d), dtype=tdt, device="cuda")
+        ro = torch.empty(self.experts.n_local + 2, dtype=torch.int32, device="cuda")
+        ws = torch.empty(max(om.ordermoe_forward_workspace_size(self.experts, T, self.cfg.k), 1),
+                         dtype=torch.uint8, device="cuda")
+        om.ordermoe_local_moe_forward(self.experts, x, T, self.cfg.k, out["w"], out["exec_k"],
+                                      out["exec_m"], loc, server, y, ro, ws)
+        return y, ro
+
+
+def host(t) -> np.ndarray:
+    import torch
+    if t.dtype == torch.bfloat16:
+        t = t.float()
+    return t.cpu().numpy()

@@ -1,0 +1,263 @@
+"""GPU parity of the HIP library against the CPU oracle, through the C ABI.
+
+Bar (stated by the method's evaluation contract): expert indices, execution
+decisions, budgets, locations and dispatch lists bit-exact on every token
+whose router logit margin is at least 1e-4 on both sides (the others are
+flagged, counted and excluded); layer outputs within max relative error 2e-2
+(bf16) / 1e-4 (fp32) per token, tokens without local rows exactly zero."""
+import numpy as np
+import pytest
+
+import workloads as wl
+from oracle import layer as olayer
+
+from ._pipeline import DeviceLayer, build_case, host, library_tables, oracle_decisions, oracle_output
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():  # pragma: no cover
+    pytest.skip("no GPU", allow_module_level=True)
+
+TOL = {"bf16": 2e-2, "f32": 1e-4}
+
+# reduced shapes that span several tiles with ragged tails; full shapes below
+SMALL = {
+    "C1": wl.C1,
+    "C2s": wl.C2.with_(T=1000, T_cal=4096),
+    "C3s": wl.C3.with_(T=1500, T_cal=4096),
+    "C4s": wl.C4.with_(T=1700, T_cal=4096),
+}
+FULL = {"C2": wl.C2.with_(T_cal=4096), "C3": wl.C3.with_(T_cal=4096), "C4": wl.C4.with_(T_cal=4096)}
+
+_cache = {}
+
+
+def _case(name, cfg, **kw):
+    key = (name, tuple(sorted(kw.items())))
+    if key not in _cache:
+        case = build_case(cfg, **kw)
+        tabs = library_tables(case)
+        _cache[key] = (case, tabs)
+    return _cache[key]
+
+
+def _flags(dec, out):
+    return (dec["margin"] < 1e-4) | (host(out["margin"]) < 1e-4)
+
+
+def _check_decisions(case, dec, out):
+    cfg = case.cfg
+    T, k = dec["idx"].shape
+    fl = _flags(dec, out)
+    ok = ~fl
+    print("[%s] T=%d flagged=%d" % (cfg.name, T, int(fl.sum())), flush=True)
+    assert fl.sum() <= max(2, 0.01 * T)
+    g = {n: host(out[n]) for n in ("idx", "exec_k", "exec_m", "cls", "qhat_out", "loc_out", "flag")}
+    np.testing.assert_array_equal(g["idx"][ok], dec["idx"][ok])
+    np.testing.assert_array_equal(g["exec_k"][ok], dec["exec_k"][ok])
+    np.testing.assert_array_equal(g["exec_m"][ok], dec["exec_m"][ok])
+    np.testing.assert_array_equal(g["cls"][ok], dec["cls"][ok])
+    np.testing.assert_array_equal(g["qhat_out"][ok], dec["qhat_out"][ok])
+    np.testing.assert_array_equal(g["loc_out"][ok], dec["loc_out"][ok])
+    np.testing.assert_array_equal(g["flag"].astype(bool), host(out["margin"]) < 1e-4)
+    # gates: fp32 softmax of fp32 logits against fp64
+    np.testing.assert_allclose(host(out["w"])[ok], dec["w"][ok], rtol=2e-4, atol=2e-6)
+    # dispatch list: equal to the oracle's rule applied to the GPU's own decisions
+    # (every token), and to the oracle's list once flagged tokens are dropped
+    lst_gpu = host(out["dispatch"])
+    cnt_gpu = host(out["dst_count"])
+    counters = host(out["counters"])
+    n_remote = int(counters[6])
+    lst_self, cnt_self, tr_self = olayer.dispatch(g["exec_m"], case.loc, cfg.M)
+    np.testing.assert_array_equal(lst_gpu[:n_remote], lst_self)
+    np.testing.assert_array_equal(cnt_gpu, cnt_self)
+    assert int(counters[5]) == tr_self
+    lst_or, _, _ = olayer.dispatch(dec["exec_m"], case.loc, cfg.M)
+    keep = lambda L: L[ok[L // k]]
+    np.testing.assert_array_equal(keep(lst_gpu[:n_remote]), keep(lst_or))
+    np.testing.assert_array_equal(counters[:4], olayer.class_counts(g["cls"]))
+    assert int(counters[4]) == int(g["flag"].sum())
+    assert int(counters[7]) == 0
+    return ok
+
+
+def _check_output(case, dec, y_gpu, tokens, ok, tol):
+    want = oracle_output(case, dec, tokens)
+    got = host(y_gpu)[tokens]
+    worst = 0.0
+    for i, t in enumerate(tokens):
+        if not ok[t]:
+            continue
+        ref = np.max(np.abs(want[i]))
+        if ref == 0.0:
+            assert np.all(got[i] == 0.0), t
+            continue
+        err = np.max(np.abs(got[i] - want[i])) / ref
+        worst = max(worst, err)
+    print("[%s] output max rel err %.3g over %d tokens" % (case.cfg.name, worst, len(tokens)), flush=True)
+    assert worst <= tol
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_layer_parity_small(name):
+    case, tabs = _case(name, SMALL[name])
+    dl = DeviceLayer(case, tabs)
+    x, loc, qh = dl.inputs()
+    T = case.X.shape[0]
+    out = dl.route(x, loc, qh, T)
+    y, ro = dl.forward(x, loc, out, T)
+    torch.cuda.synchronize()
+    dec = oracle_decisions(case)
+    ok = _check_decisions(case, dec, out)
+    # row offsets: the GPU's own local rows, recounted from its decisions
+    rows = host(ro)
+    assert rows[0] == 0 and np.all(np.diff(rows) >= 0)
+    _check_output(case, dec, y, np.arange(T), ok, TOL[case.cfg.dtype])
+
+
+@pytest.mark.parametrize("name", list(FULL))
+def test_layer_parity_full_shape_sampled(name):
+    case, tabs = _case(name, FULL[name])
+    dl = DeviceLayer(case, tabs)
+    x, loc, qh = dl.inputs()
+    T = case.X.shape[0]
+    out = dl.route(x, loc, qh, T)
+    y, ro = dl.forward(x, loc, out, T)
+    torch.cuda.synchronize()
+    dec = oracle_decisions(case)
+    ok = _check_decisions(case, dec, out)
+    rng = np.random.default_rng(0)
+    sample = np.unique(np.concatenate([rng.choice(T, 40, replace=False), [0, T - 1]]))
+    _check_output(case, dec, y, sample, ok, TOL[case.cfg.dtype])
+
+
+@pytest.mark.parametrize("Qbar", wl.C4_QBAR_SWEEP)
+def test_quality_budget_sweep(Qbar):
+    cfg = wl.C4.with_(T=2048, T_cal=4096, Qbar=Qbar)
+    case, tabs = _case("C4q%g" % Qbar, cfg, qhat_scale=0.0)
+    dl = DeviceLayer(case, tabs, with_experts=False)
+    x, loc, qh = dl.inputs()
+    out = dl.route(x, loc, qh, case.X.shape[0])
+    torch.cuda.synchronize()
+    dec = oracle_decisions(case)
+    _check_decisions(case, dec, out)
+    assert np.all(host(out["qhat_out"]) <= np.float32(Qbar))       # Property 2
+    if Qbar == 0.0:
+        assert not np.any(host(out["cls"]) & 1)
+
+
+def test_partly_spent_budget_and_remote_sources():
+    cfg = wl.C3.with_(T=3000, T_cal=4096, Qbar=0.03)
+    case, tabs = _case("C3spent", cfg, qhat_scale=0.03)
+    dl = DeviceLayer(case, tabs, with_experts=False)
+    x, loc, qh = dl.inputs()
+    out = dl.route(x, loc, qh, case.X.shape[0])
+    torch.cuda.synchronize()
+    _check_decisions(case, oracle_decisions(case), out)
+
+
+def test_no_substitution_sum_over_servers_is_exact_moe():
+    # Qbar = 0: every slot runs its target; the outputs of all servers add up
+    # to the plain top-k MoE layer
+    cfg = wl.C3.with_(T=700, T_cal=4096, Qbar=0.0)
+    case, tabs = _case("C3exact", cfg)
+    dec = oracle_decisions(case)
+    assert np.array_equal(dec["exec_k"], dec["idx"])
+    total = None
+    for m in range(cfg.M):
+        local = [int(j) for j in np.nonzero(case.x_dep[m])[0]]
+        c_m = build_case(cfg.with_(m0=m), T=700)
+        dl = DeviceLayer(c_m, library_tables(c_m), with_experts=True)
+        x, loc, qh = dl.inputs()
+        out = dl.route(x, loc, qh, 700)
+        y, _ = dl.forward(x, loc, out, 700)
+        torch.cuda.synchronize()
+        assert c_m.local == local
+        total = host(y).astype(np.float64) if total is None else total + host(y)
+    want = sum(olayer.server_output(case.X, dec["w"], dec["exec_k"], dec["exec_m"], case.loc, m,
+                                    case.expert, case.shared(), np.arange(700)) for m in range(cfg.M))
+    fl = dec["margin"] < 1e-4
+    err = np.max(np.abs(total - want)[~fl], axis=1) / np.max(np.abs(want[~fl]), axis=1)
+    print("exact-MoE max rel err %.3g" % err.max(), flush=True)
+    assert err.max() <= 4e-2   # four bf16 roundings of partial outputs summed
+
+
+def test_all_local_means_no_remote():
+    cfg = wl.C2.with_(T=512, T_cal=4096)
+    case, _ = _case("C2local", cfg)
+    case.x_dep = case.x_dep.copy()
+    case.x_dep[cfg.m0, :] = 1
+    case.local = list(range(cfg.E))
+    tabs = library_tables(case)
+    dl = DeviceLayer(case, tabs, with_experts=False)
+    x, loc, qh = dl.inputs()
+    out = dl.route(x, loc, qh, 512)
+    torch.cuda.synchronize()
+    assert np.all(host(out["cls"]) == 0)
+    c = host(out["counters"])
+    assert c[2] == 0 and c[3] == 0 and c[5] == 0 and c[6] == 0
+    assert np.all(host(out["dst_count"]) == 0)
+
+
+@pytest.mark.parametrize("variant", ["pin0", "renorm0"])
+def test_selection_variants(variant):
+    kw = {"pin0": dict(pin_local_exact=0), "renorm0": dict(renorm=0)}[variant]
+    cfg = wl.C3.with_(T=1200, T_cal=4096, **kw)
+    case, tabs = _case("C3" + variant, cfg)
+    dl = DeviceLayer(case, tabs, with_experts=False)
+    x, loc, qh = dl.inputs()
+    out = dl.route(x, loc, qh, 1200)
+    torch.cuda.synchronize()
+    _check_decisions(case, oracle_decisions(case), out)
+
+
+def test_empty_and_single_token_batches():
+    case, tabs = _case("C1", wl.C1)
+    dl = DeviceLayer(case, tabs)
+    for T in (0, 1, 17):
+        x, loc, qh = dl.inputs(case.X[:T], case.loc[:T], case.qhat[:T])
+        if T == 0:
+            x = torch.empty((0, case.cfg.d), device="cuda")
+        out = dl.route(x, loc, qh, T)
+        y, ro = dl.forward(x, loc, out, T)
+        torch.cuda.synchronize()
+        c = host(out["counters"])
+        assert c[:4].sum() == T * case.cfg.k and c[7] == 0
+        if T == 0:
+            assert np.all(host(ro) == 0) and np.all(c == 0)
+        else:
+            dec = oracle_decisions(case)
+            sl = slice(0, T)
+            np.testing.assert_array_equal(host(out["exec_k"]), dec["exec_k"][sl])
+
+
+def test_invalid_locations_are_counted_not_routed():
+    case, tabs = _case("C1", wl.C1)
+    dl = DeviceLayer(case, tabs, with_experts=False)
+    loc = case.loc.copy()
+    loc[5] = 7
+    loc[9] = 255
+    x, loc_d, qh = dl.inputs(loc=loc)
+    out = dl.route(x, loc_d, qh, case.X.shape[0])
+    torch.cuda.synchronize()
+    c = host(out["counters"])
+    assert c[7] == 2
+    ek = host(out["exec_k"])
+    assert np.all(ek[[5, 9]] == -1) and np.all(host(out["cls"])[[5, 9]] == 255)
+    assert c[:4].sum() == (case.X.shape[0] - 2) * case.cfg.k
+
+
+def test_runs_are_bitwise_deterministic():
+    case, tabs = _case("C3s", SMALL["C3s"])
+    dl = DeviceLayer(case, tabs)
+    x, loc, qh = dl.inputs()
+    T = case.X.shape[0]
+    res = []
+    for _ in range(2):
+        out = dl.route(x, loc, qh, T)
+        y, _ = dl.forward(x, loc, out, T)
+        torch.cuda.synchronize()
+        res.append((host(out["exec_k"]), host(out["dispatch"]), host(y)))
+    for a, b in zip(res[0], res[1]):
+        np.testing.assert_array_equal(a, b)
