@@ -308,8 +308,8 @@ int ordermoe_local_moe_forward(const ordermoe_experts* W, const void* x, int64_t
 
 /* One-time weight packing for ordermoe_local_moe_forward (device).
  * w_gate, w_up: dev [n][f][d]; out: dev [n][2f][d] where, for every block b of
- * 16 FFN columns, rows [32b, 32b+16) hold gate rows [16b, 16b+16) and rows
- * [32b+16, 32b+32) hold the matching up rows.  Requires f % 16 == 0. */
+ * 32 FFN columns, rows [64b, 64b+32) hold gate rows [32b, 32b+32) and rows
+ * [64b+32, 64b+64) hold the matching up rows.  Requires f % 32 == 0. */
 int ordermoe_pack_gate_up(int32_t dtype, int32_t n, int32_t f, int32_t d, const void* w_gate,
                           const void* w_up, void* out, void* stream);
 

@@ -265,8 +265,8 @@ extern "C" int ordermoe_pack_gate_up(int32_t dtype, int32_t n, int32_t f, int32_
                                      const void* w_gate, const void* w_up, void* out,
                                      void* stream) {
     if (dtype != ORDERMOE_F32 && dtype != ORDERMOE_BF16) return fail(ORDERMOE_EDTYPE, "pack_gate_up: dtype");
-    if (n < 0 || f < 16 || f % 16 != 0 || d < 8 || d % 8 != 0)
-        return fail(ORDERMOE_EINVAL, "pack_gate_up: need n >= 0, f % 16 == 0, d % 8 == 0");
+    if (n < 0 || f < 32 || f % 32 != 0 || d < 8 || d % 8 != 0)
+        return fail(ORDERMOE_EINVAL, "pack_gate_up: need n >= 0, f % 32 == 0, d % 8 == 0");
     if (n > 0 && (!w_gate || !w_up || !out)) return fail(ORDERMOE_EINVAL, "pack_gate_up: null pointer");
     const int e = launch_pack_gate_up(dtype, n, f, d, w_gate, w_up, out, stream);
     if (e) return hip_fail(e, "pack_gate_up launch");

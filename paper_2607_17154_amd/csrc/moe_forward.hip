@@ -192,6 +192,7 @@ struct GemmArgs {
     const void* X;            // mode 0: token rows [T][ldx]
     const int32_t* row_tok;   // mode 0
     int ldx;
+    uint32_t x_bytes;         // mode 0: size of X in bytes
     const void* Ar;           // mode 1: routed activations [*][Kr]
     const void* As;           // mode 1: shared activations [*][Ks]
     void* Or;                 // mode 0: routed activations out; mode 1: row outputs [*][Nr]
@@ -226,141 +227,177 @@ __device__ inline bool decode_tile(const GemmArgs& p, int tile, TileLoc& L) {
 
 __device__ inline float silu_f(float g) { return g / (1.0f + __expf(-g)); }
 
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int BUF_DWORD3 = 0x00020000;   // raw buffer resource word 3 on gfx9-class GPUs
+
+__device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, BUF_DWORD3);
+}
+
+__device__ inline bf16x8 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, 0);
+    return __builtin_bit_cast(bf16x8, v);
+}
+
+// bf16 grouped GEMM C = A B^T per tile of BM x BN, K step 64, 4 waves (2 x 2),
+// each wave a (BM/2) x (BN/2) block of v_mfma_f32_32x32x16_bf16 tiles.
+// Operands are staged global -> registers -> LDS, double buffered, with rows
+// padded by 16 bytes so that 16-byte fragment reads of 8 consecutive rows hit
+// distinct banks.  Global reads are raw buffer loads: the K position travels in
+// the scalar offset, and rows past the end of a group read as zeros through
+// the buffer range check (their offset is set past the buffer).  Byte offsets
+// inside one operand fit in 31 bits (checked by the host).
 template <int BM, int BN, int MODE>
-__global__ void __launch_bounds__(256) ggemm_bf16(const GemmArgs p) {
-    constexpr int BK = 64, LDK = BK + 8;        // padded LDS rows: conflict-free 16-B reads
-    constexpr int WM = BM / 2, WN = BN / 2;     // 2 x 2 waves
-    constexpr int FM = WM / 16, FN = WN / 16;   // 16x16 MFMA blocks per wave
-    constexpr int AV = BM * BK / 8 / 256;       // 16-B vectors per thread per K tile
+__global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
+    constexpr int BK = 64, LDK = BK + 8;
+    constexpr int WM = BM / 2, WN = BN / 2;
+    constexpr int FM = WM / 32, FN = WN / 32;
+    constexpr int AV = BM * BK / 8 / 256;
     constexpr int BV = BN * BK / 8 / 256;
-    static_assert(FN % 2 == 0, "gate/up pairs need an even number of N blocks");
+    static_assert(FN % 2 == 0, "gate/up pairs need an even number of 32-column blocks");
     extern __shared__ __attribute__((aligned(16))) char lds_raw[];
     __bf16* sA = (__bf16*)lds_raw;                  // [2][BM][LDK]
     __bf16* sB = sA + 2 * BM * LDK;                 // [2][BN][LDK]
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
+    const int lrow = tid >> 3, lch = (tid & 7) * 8;  // this thread's load slot
     const int total = *p.ntiles;
     const int per_xcd = gridDim.x >> 3;
     const int vid = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+    constexpr uint32_t OOR = 0x80000000u;           // offset past every buffer: reads zero
 
     for (int tile = vid; tile < total; tile += gridDim.x) {
         TileLoc L;
         if (!decode_tile<BM, BN>(p, tile, L)) break;
         const bool shared = L.g >= p.n_routed;
+        const int K = L.K;
         const __bf16* Bw = shared ? (const __bf16*)p.Ws
-                                  : (const __bf16*)p.Wr + (int64_t)L.g * L.N * L.K;
-        // per-thread global row pointers of this tile
-        const __bf16* arow[AV];
-        bool aok[AV];
+                                  : (const __bf16*)p.Wr + (size_t)L.g * L.N * K;
+        const __amdgpu_buffer_rsrc_t rb_rs = make_rsrc(Bw, (uint32_t)((size_t)L.N * K * 2));
+        __amdgpu_buffer_rsrc_t ra_rs;
+        uint32_t aoff[AV];
+        if (MODE == 0) {
+            ra_rs = make_rsrc(p.X, p.x_bytes);
 #pragma unroll
-        for (int v = 0; v < AV; ++v) {
-            const int id = v * 256 + tid, r = id >> 3, ch = id & 7;
-            const int row = L.m0 + r;
-            aok[v] = row < L.R;
-            const int rr = aok[v] ? row : 0;
-            if (MODE == 0) {
-                const int tok = p.row_tok[L.rowbase + rr];
-                arow[v] = (const __bf16*)p.X + (int64_t)tok * p.ldx + ch * 8;
-            } else {
-                const __bf16* base = shared ? (const __bf16*)p.As
-                                            : (const __bf16*)p.Ar + (int64_t)L.rowbase * L.K;
-                arow[v] = base + (int64_t)rr * L.K + ch * 8;
+            for (int v = 0; v < AV; ++v) {
+                const int row = L.m0 + lrow + 32 * v;
+                aoff[v] = row < L.R ? ((uint32_t)p.row_tok[L.rowbase + row] * (uint32_t)p.ldx + lch) * 2u : OOR;
+            }
+        } else {
+            const __bf16* Ab = shared ? (const __bf16*)p.As : (const __bf16*)p.Ar + (size_t)L.rowbase * K;
+            ra_rs = make_rsrc(Ab, (uint32_t)((size_t)L.R * K * 2));
+#pragma unroll
+            for (int v = 0; v < AV; ++v) {
+                const int row = L.m0 + lrow + 32 * v;
+                aoff[v] = row < L.R ? ((uint32_t)row * (uint32_t)K + lch) * 2u : OOR;
             }
         }
-        const __bf16* brow[BV];
-#pragma unroll
-        for (int v = 0; v < BV; ++v) {
-            const int id = v * 256 + tid, r = id >> 3, ch = id & 7;
-            brow[v] = Bw + (int64_t)(L.n0 + r) * L.K + ch * 8;
-        }
-        f32x4 acc[FM][FN];
+        const uint32_t boff0 = ((uint32_t)(L.n0 + lrow) * (uint32_t)K + lch) * 2u;
+        const uint32_t bstride = 64u * (uint32_t)K;       // 32 rows, in bytes
+
+        f32x16 acc[FM][FN];
 #pragma unroll
         for (int i = 0; i < FM; ++i)
 #pragma unroll
-            for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
         bf16x8 ra[AV], rb[BV];
-        const bf16x8 zero8 = {};
         auto gload = [&](int k0) {
+            const uint32_t ks = (uint32_t)k0 * 2u;
 #pragma unroll
-            for (int v = 0; v < AV; ++v) ra[v] = aok[v] ? *(const bf16x8*)(arow[v] + k0) : zero8;
+            for (int v = 0; v < AV; ++v) ra[v] = buf_load16(ra_rs, aoff[v], ks);
 #pragma unroll
-            for (int v = 0; v < BV; ++v) rb[v] = *(const bf16x8*)(brow[v] + k0);
+            for (int v = 0; v < BV; ++v) rb[v] = buf_load16(rb_rs, boff0 + v * bstride, ks);
         };
         auto sstore = [&](int buf) {
-            __bf16* a = sA + buf * BM * LDK;
-            __bf16* b = sB + buf * BN * LDK;
+            __bf16* a = sA + buf * BM * LDK + lrow * LDK + lch;
+            __bf16* b = sB + buf * BN * LDK + lrow * LDK + lch;
 #pragma unroll
-            for (int v = 0; v < AV; ++v) {
-                const int id = v * 256 + tid;
-                *(bf16x8*)(a + (id >> 3) * LDK + (id & 7) * 8) = ra[v];
-            }
+            for (int v = 0; v < AV; ++v) *(bf16x8*)(a + v * 32 * LDK) = ra[v];
 #pragma unroll
-            for (int v = 0; v < BV; ++v) {
-                const int id = v * 256 + tid;
-                *(bf16x8*)(b + (id >> 3) * LDK + (id & 7) * 8) = rb[v];
-            }
+            for (int v = 0; v < BV; ++v) *(bf16x8*)(b + v * 32 * LDK) = rb[v];
         };
-        const int KT = L.K / BK;
+        const int KT = K / BK;
+        const int arow_off = (wm * WM + (lane & 31)) * LDK + (lane >> 5) * 8;
+        const int brow_off = (wn * WN + (lane & 31)) * LDK + (lane >> 5) * 8;
+        bf16x8 af[2][FM], bfm[2][FN];
+        auto fload = [&](int buf, int ks, int slot) {
+            const __bf16* a = sA + buf * BM * LDK + arow_off + ks * 16;
+            const __bf16* b = sB + buf * BN * LDK + brow_off + ks * 16;
+#pragma unroll
+            for (int i = 0; i < FM; ++i) af[slot][i] = *(const bf16x8*)(a + i * 32 * LDK);
+#pragma unroll
+            for (int j = 0; j < FN; ++j) bfm[slot][j] = *(const bf16x8*)(b + j * 32 * LDK);
+        };
         gload(0);
         sstore(0);
         __syncthreads();
+        fload(0, 0, 0);
         for (int kt = 0; kt < KT; ++kt) {
-            if (kt + 1 < KT) gload((kt + 1) * BK);
-            const __bf16* a = sA + (kt & 1) * BM * LDK + (wm * WM + (lane & 15)) * LDK + (lane >> 4) * 8;
-            const __bf16* b = sB + (kt & 1) * BN * LDK + (wn * WN + (lane & 15)) * LDK + (lane >> 4) * 8;
+            // branch-free body: the last iteration re-reads the last K tile
+            // and writes it to the idle buffer, which nobody reads afterwards.
+            // Scheduling fences keep the sub-steps in order: the fragment
+            // reads of sub-step ks+1 are in flight under the MFMAs of ks.
+            const int cur = kt & 1;
+            gload((kt + 1 < KT ? kt + 1 : kt) * BK);
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-            for (int ks = 0; ks < BK / 32; ++ks) {
-                bf16x8 af[FM], bfm[FN];
-#pragma unroll
-                for (int i = 0; i < FM; ++i) af[i] = *(const bf16x8*)(a + i * 16 * LDK + ks * 32);
-#pragma unroll
-                for (int j = 0; j < FN; ++j) bfm[j] = *(const bf16x8*)(b + j * 16 * LDK + ks * 32);
+            for (int ks = 0; ks < BK / 16; ++ks) {
+                const int slot = ks & 1;
+                if (ks + 1 < BK / 16) fload(cur, ks + 1, slot ^ 1);
+                __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                 for (int i = 0; i < FM; ++i)
 #pragma unroll
                     for (int j = 0; j < FN; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfm[j], acc[i][j], 0, 0, 0);
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[slot][i], bfm[slot][j], acc[i][j], 0, 0, 0);
+                __builtin_amdgcn_sched_barrier(0);
             }
-            if (kt + 1 < KT) sstore((kt + 1) & 1);
+            sstore(cur ^ 1);
             __syncthreads();
+            fload(cur ^ 1, 0, 0);
         }
 
-        // epilogue: lane holds rows (lane/16)*4 + e, column lane%16 of each block
-        const int rbase = L.m0 + wm * WM + (lane >> 4) * 4;
+        // epilogue: element e of a 32x32 block is row (e/4)*8 + (lane/32)*4 + e%4,
+        // column lane%32
+        const int rbase = L.m0 + wm * WM + (lane >> 5) * 4;
         if (MODE == 0) {
             __bf16* out = shared ? (__bf16*)p.Os : (__bf16*)p.Or;
             const int ldo = L.N / 2;
             const int orow0 = shared ? 0 : L.rowbase;
-            const int cbase = (L.n0 + wn * WN) / 2 + (lane & 15);
+            const int cbase = (L.n0 + wn * WN) / 2 + (lane & 31);
 #pragma unroll
             for (int i = 0; i < FM; ++i)
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int row = rbase + i * 16 + e;
+                for (int e = 0; e < 16; ++e) {
+                    const int row = rbase + i * 32 + (e >> 2) * 8 + (e & 3);
                     if (row < L.R) {
 #pragma unroll
                         for (int q = 0; q < FN / 2; ++q) {
                             const float gv = acc[i][2 * q][e], uv = acc[i][2 * q + 1][e];
-                            out[(int64_t)(orow0 + row) * ldo + cbase + q * 16] = (__bf16)(silu_f(gv) * uv);
+                            out[(size_t)(orow0 + row) * ldo + cbase + q * 32] = (__bf16)(silu_f(gv) * uv);
                         }
                     }
                 }
         } else {
             __bf16* out = (__bf16*)p.Or;
             const int ldo = L.N;
-            const int cbase = L.n0 + wn * WN + (lane & 15);
+            const int cbase = L.n0 + wn * WN + (lane & 31);
 #pragma unroll
             for (int i = 0; i < FM; ++i)
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int row = rbase + i * 16 + e;
+                for (int e = 0; e < 16; ++e) {
+                    const int row = rbase + i * 32 + (e >> 2) * 8 + (e & 3);
                     if (row < L.R) {
                         const float wr = p.row_w[L.rowbase + row];
 #pragma unroll
                         for (int j = 0; j < FN; ++j)
-                            out[(int64_t)(L.rowbase + row) * ldo + cbase + j * 16] = (__bf16)(acc[i][j][e] * wr);
+                            out[(size_t)(L.rowbase + row) * ldo + cbase + j * 32] = (__bf16)(acc[i][j][e] * wr);
                     }
                 }
         }
@@ -437,8 +474,8 @@ __global__ void __launch_bounds__(256) ggemm_f32(const GemmArgs p) {
                 const int r = idx / (BN / 2), c = idx % (BN / 2);   // activation column within tile
                 const int row = L.m0 + r;
                 if (row >= L.R) continue;
-                const int blk = c >> 4, cc = c & 15;
-                const float gv = sC[r][blk * 32 + cc], uv = sC[r][blk * 32 + 16 + cc];
+                const int blk = c >> 5, cc = c & 31;
+                const float gv = sC[r][blk * 64 + cc], uv = sC[r][blk * 64 + 32 + cc];
                 const int orow = (shared ? 0 : L.rowbase) + row;
                 out[(int64_t)orow * ldo + L.n0 / 2 + c] = silu_f(gv) * uv;
             }
@@ -563,6 +600,7 @@ int launch_local_forward(const ForwardArgs& f, void* stream) {
     GemmArgs g;
     g.offsets = f.row_offsets; g.G = G; g.n_routed = f.n_local;
     g.X = f.x; g.row_tok = f.row_tok; g.ldx = f.d; g.row_w = f.row_w;
+    g.x_bytes = (uint32_t)((size_t)f.T * f.d * (f.dtype == ORDERMOE_BF16 ? 2 : 4));
 
     // gate/up: [rows][d] x [2f][d]^T -> activations [rows][f]
     g.ntiles = f.tile_info + 0;

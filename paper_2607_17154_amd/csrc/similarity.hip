@@ -179,13 +179,13 @@ __global__ void __launch_bounds__(1024) sim_finalize_kernel(const SimArgs a, int
 
 __global__ void pack_gate_up_kernel(int esz, int64_t n, int f, int d, const char* g, const char* u,
                                     char* out) {
-    // one block per packed row; rows [32b, 32b+16) <- gate [16b, 16b+16), [32b+16, 32b+32) <- up
+    // one block per packed row; rows [64b, 64b+32) <- gate [32b, 32b+32), [64b+32, 64b+64) <- up
     const int64_t prow = blockIdx.x;                  // over n * 2f rows
     const int64_t ex = prow / (2 * f);
     const int pr = (int)(prow % (2 * f));
-    const int blk = pr / 32, within = pr % 32;
-    const int src_row = blk * 16 + (within & 15);
-    const char* src = (within < 16 ? g : u) + ((ex * f + src_row) * (int64_t)d) * esz;
+    const int blk = pr / 64, within = pr % 64;
+    const int src_row = blk * 32 + (within & 31);
+    const char* src = (within < 32 ? g : u) + ((ex * f + src_row) * (int64_t)d) * esz;
     char* dst = out + prow * (int64_t)d * esz;
     const int64_t nbytes = (int64_t)d * esz;
     for (int64_t i = threadIdx.x * 4; i < nbytes; i += blockDim.x * 4)
