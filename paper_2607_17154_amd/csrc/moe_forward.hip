@@ -307,18 +307,21 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
                 for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
         bf16x8 ra[AV], rb[BV];
-        auto gload = [&](int k0) {
-            const uint32_t ks = (uint32_t)k0 * 2u;
+        auto gloadA = [&](int k0) {
 #pragma unroll
-            for (int v = 0; v < AV; ++v) ra[v] = buf_load16(ra_rs, aoff[v], ks);
-#pragma unroll
-            for (int v = 0; v < BV; ++v) rb[v] = buf_load16(rb_rs, boff0 + v * bstride, ks);
+            for (int v = 0; v < AV; ++v) ra[v] = buf_load16(ra_rs, aoff[v], (uint32_t)k0 * 2u);
         };
-        auto sstore = [&](int buf) {
+        auto gloadB = [&](int k0) {
+#pragma unroll
+            for (int v = 0; v < BV; ++v) rb[v] = buf_load16(rb_rs, boff0 + v * bstride, (uint32_t)k0 * 2u);
+        };
+        auto sstoreA = [&](int buf) {
             __bf16* a = sA + buf * BM * LDK + lrow * LDK + lch;
-            __bf16* b = sB + buf * BN * LDK + lrow * LDK + lch;
 #pragma unroll
             for (int v = 0; v < AV; ++v) *(bf16x8*)(a + v * 32 * LDK) = ra[v];
+        };
+        auto sstoreB = [&](int buf) {
+            __bf16* b = sB + buf * BN * LDK + lrow * LDK + lch;
 #pragma unroll
             for (int v = 0; v < BV; ++v) *(bf16x8*)(b + v * 32 * LDK) = rb[v];
         };
@@ -334,31 +337,73 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
 #pragma unroll
             for (int j = 0; j < FN; ++j) bfm[slot][j] = *(const bf16x8*)(b + j * 32 * LDK);
         };
-        gload(0);
-        sstore(0);
+        auto mfmas = [&](int slot) {
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[slot][i], bfm[slot][j], acc[i][j], 0, 0, 0);
+        };
+        // Each K tile of 64 is four MFMA sub-steps of 16.  The memory traffic
+        // of the next K tile is spread over them so the MFMA pipe never waits
+        // behind a burst of memory instructions: sub-step 0 issues the B
+        // (weight) reads, 1 the A reads, 2 stores B to the idle LDS buffer, 3
+        // stores A, so each store waits only for reads issued two sub-steps
+        // earlier; every sub-step also reads the fragments of the next one.
+        // Scheduling groups interleave MFMAs with these instructions, fences
+        // keep the sub-steps in order.  The body is branch-free: after the last
+        // tile the last K tile is re-read into the idle buffer, never used.
+        static_assert(FM * FN == 16 && AV == 8 && BV == 8, "schedule written for 16 MFMAs and 8 loads per sub-step");
+        gloadA(0);
+        gloadB(0);
+        sstoreA(0);
+        sstoreB(0);
         __syncthreads();
         fload(0, 0, 0);
         for (int kt = 0; kt < KT; ++kt) {
-            // branch-free body: the last iteration re-reads the last K tile
-            // and writes it to the idle buffer, which nobody reads afterwards.
-            // Scheduling fences keep the sub-steps in order: the fragment
-            // reads of sub-step ks+1 are in flight under the MFMAs of ks.
             const int cur = kt & 1;
-            gload((kt + 1 < KT ? kt + 1 : kt) * BK);
-            __builtin_amdgcn_sched_barrier(0);
+            const int kn = (kt + 1 < KT ? kt + 1 : kt) * BK;
+            fload(cur, 1, 1);
+            gloadB(kn);
+            mfmas(0);
 #pragma unroll
-            for (int ks = 0; ks < BK / 16; ++ks) {
-                const int slot = ks & 1;
-                if (ks + 1 < BK / 16) fload(cur, ks + 1, slot ^ 1);
-                __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-                for (int i = 0; i < FM; ++i)
-#pragma unroll
-                    for (int j = 0; j < FN; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[slot][i], bfm[slot][j], acc[i][j], 0, 0, 0);
-                __builtin_amdgcn_sched_barrier(0);
+            for (int q = 0; q < 8; ++q) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // LDS read
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // global read
             }
-            sstore(cur ^ 1);
+            __builtin_amdgcn_sched_barrier(0);
+            fload(cur, 2, 0);
+            gloadA(kn);
+            mfmas(1);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            fload(cur, 3, 1);
+            sstoreB(cur ^ 1);
+            mfmas(0);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);   // LDS write
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            sstoreA(cur ^ 1);
+            mfmas(1);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+                __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+            }
+            __builtin_amdgcn_sched_barrier(0);
             __syncthreads();
             fload(cur ^ 1, 0, 0);
         }
