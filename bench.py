@@ -28,6 +28,45 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "gemm_gate_up_mixtral_traffic.md")
+GEMM_SOURCE = os.path.join(ROOT, "paper_2607_17154_amd", "csrc", "moe_forward.hip")
+
+
+def source_sha256(path: str) -> str:
+    import hashlib
+    with open(path, "rb") as fh:
+        return hashlib.sha256(fh.read()).hexdigest()
+
+
+def _measured_traffic():
+    """HBM bytes per launch of the gate/up GEMM from the committed rocprofv3
+    counter summary, if it was taken on the current kernel source."""
+    try:
+        lines = open(TRAFFIC_PROFILE).read().splitlines()
+    except OSError:
+        return None
+    vals = {}
+    for ln in lines:
+        if ln.startswith("- ") and ":" in ln:
+            k, v = ln[2:].split(":", 1)
+            vals[k.strip()] = v.strip().strip("`")
+    if vals.get("kernel source sha256") != source_sha256(GEMM_SOURCE):
+        return None
+    try:
+        return int(vals["HBM bytes per launch (scaled)"])
+    except (KeyError, ValueError):
+        return None
+
+
+def _calibrate_copy(torch, gib: int = 1):
+    """A plain device copy of known size, for scaling the HBM byte counters."""
+    n = gib * (1 << 30) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "launches": 3}))
 
 
 def _setup(cfg, torch, om):
@@ -153,6 +192,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a 1 GiB device copy (to scale rocprofv3 byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the layer runs one simulated server's experts on one "
@@ -161,6 +202,9 @@ def main():
         sys.exit(2)
 
     import torch
+    if args.calibrate_copy:
+        _calibrate_copy(torch)
+        return
 
     import workloads as wl
     from paper_2607_17154_amd import ordermoe as om
@@ -217,7 +261,8 @@ def main():
                    "flagged_tokens": int(counters[4]), "remote_transfers": int(counters[5])},
         "roofline": {"bound": "mfma", "kernel": "gemm_gate_up", "achieved": achieved,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
-                     "traffic": None, "flop_per_launch": gu_flops, "avg_launch_us": gu_avg_s * 1e6},
+                     "traffic": _measured_traffic(), "flop_per_launch": gu_flops,
+                     "avg_launch_us": gu_avg_s * 1e6},
         "kernels_avg_us": {k: v[0] / v[1] * 1e3 for k, v in sorted(kt.items())},
         "mfma_frac_ffn": (2.0 * R * cfg.d * 3 * cfg.f) / (ms_step / 1e3) / 1e12 / PEAK_BF16_TFLOPS,
     }
