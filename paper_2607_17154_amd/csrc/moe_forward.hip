@@ -241,6 +241,21 @@ __device__ inline bf16x8 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uin
     return __builtin_bit_cast(bf16x8, v);
 }
 
+// Scheduling pattern of one MFMA sub-step: NM MFMAs with NR LDS fragment
+// reads and NX other memory instructions (mask XMASK) spread between them,
+// reads after even-numbered MFMAs, the others after odd-numbered ones.
+template <int Q, int NM, int NR, int NX, int XMASK>
+__device__ inline void sched_interleave() {
+    if constexpr (Q < NM) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+        constexpr int r = ((Q + 1) * NR + NM - 1) / NM - (Q * NR + NM - 1) / NM;
+        if constexpr (r > 0) __builtin_amdgcn_sched_group_barrier(0x100, r, 0);   // LDS read
+        constexpr int x = (Q + 1) * NX / NM - Q * NX / NM;
+        if constexpr (x > 0) __builtin_amdgcn_sched_group_barrier(XMASK, x, 0);
+        sched_interleave<Q + 1, NM, NR, NX, XMASK>();
+    }
+}
+
 // bf16 grouped GEMM C = A B^T per tile of BM x BN, K step 64, 4 waves (2 x 2),
 // each wave a (BM/2) x (BN/2) block of v_mfma_f32_32x32x16_bf16 tiles.
 // Operands are staged global -> registers -> LDS, double buffered, with rows
@@ -353,7 +368,8 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
         // Scheduling groups interleave MFMAs with these instructions, fences
         // keep the sub-steps in order.  The body is branch-free: after the last
         // tile the last K tile is re-read into the idle buffer, never used.
-        static_assert(FM * FN == 16 && AV == 8 && BV == 8, "schedule written for 16 MFMAs and 8 loads per sub-step");
+        constexpr int NM = FM * FN, NR = FM + FN;
+        constexpr int VMEM_READ = 0x020, LDS_WRITE = 0x200;
         gloadA(0);
         gloadB(0);
         sstoreA(0);
@@ -366,43 +382,21 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
             fload(cur, 1, 1);
             gloadB(kn);
             mfmas(0);
-#pragma unroll
-            for (int q = 0; q < 8; ++q) {
-                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
-                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // LDS read
-                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-                __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // global read
-            }
+            sched_interleave<0, NM, NR, BV, VMEM_READ>();
             __builtin_amdgcn_sched_barrier(0);
             fload(cur, 2, 0);
             gloadA(kn);
             mfmas(1);
-#pragma unroll
-            for (int q = 0; q < 8; ++q) {
-                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-                __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-            }
+            sched_interleave<0, NM, NR, AV, VMEM_READ>();
             __builtin_amdgcn_sched_barrier(0);
             fload(cur, 3, 1);
             sstoreB(cur ^ 1);
             mfmas(0);
-#pragma unroll
-            for (int q = 0; q < 8; ++q) {
-                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-                __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);   // LDS write
-            }
+            sched_interleave<0, NM, NR, BV, LDS_WRITE>();
             __builtin_amdgcn_sched_barrier(0);
             sstoreA(cur ^ 1);
             mfmas(1);
-#pragma unroll
-            for (int q = 0; q < 8; ++q) {
-                __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-                __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
-            }
+            sched_interleave<0, NM, 0, AV, LDS_WRITE>();
             __builtin_amdgcn_sched_barrier(0);
             __syncthreads();
             fload(cur ^ 1, 0, 0);
@@ -572,7 +566,7 @@ __global__ void __launch_bounds__(256) combine_kernel(const CombineArgs c) {
 }
 
 
-constexpr int GU_BM = 256, GU_BN = 256, DN_BM = 256, DN_BN = 256;   // bf16 GEMM tiles
+constexpr int GU_BM = 256, GU_BN = 256, DN_BM = 192, DN_BN = 256;   // bf16 GEMM tiles
 constexpr int F32_BM = 64, F32_BN = 64;
 
 template <int BM, int BN>
