@@ -67,10 +67,11 @@ struct RouteArgs {
     int64_t* blk_cnt;      // [nblk][8] per-block counters
     int32_t* dst_base;     // [nblk][M] exclusive prefix (written by scan)
     int nblk;
+    int S_in_lds;          // set by the launcher: stage the cost table in LDS
 };
 int launch_route_select(const RouteArgs& a, void* stream);
 int route_tokens_per_block();
-size_t route_smem_bytes(int E, int gmax, int M);
+size_t route_smem_bytes(int E, int gmax, int M, bool S_in_lds);
 
 struct ForwardArgs {
     int dtype, d, f, E, n_local, n_shared, k;

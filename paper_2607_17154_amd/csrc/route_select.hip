@@ -28,8 +28,10 @@ namespace ordermoe {
 namespace {
 
 constexpr int RT_TB = 16;        // tokens per block
-constexpr int RT_THREADS = 256;  // 4 waves; 16 lanes per token in the token stage
+constexpr int RT_THREADS = 512;  // 8 waves share the router's K loop; waves 0-3 then
+                                 // run the token stage, 16 lanes per token
 constexpr int RT_WAVES = RT_THREADS / 64;
+constexpr int RT_SLOTS = 4;      // partial-sum slots of the two-round wave reduction
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -51,6 +53,58 @@ __device__ inline uint64_t shfl_xor64(uint64_t v, int mask) {
     return ((uint64_t)hi << 32) | lo;
 }
 
+// Router partial logits of this block's 16 tokens over the K steps of 32 that
+// belong to this wave (steps wave, wave + 8, ...): v_mfma_f32_16x16x32_bf16
+// with the tokens as rows and 16 experts per block as columns.  U steps are
+// loaded before they are multiplied so that each wave keeps U * (1 + NB)
+// 16-byte loads in flight.
+template <int NB, int U>
+__device__ inline void router_k_loop(const RouteArgs& a, int wave, int lane, int64_t t0, f32x4* acc) {
+    const __bf16* X = (const __bf16*)a.x;
+    const __bf16* W = (const __bf16*)a.w_router;
+    const int d = a.d, E = a.E;
+    const int r16 = lane & 15, kg = (lane >> 4) * 8;
+    const int64_t tok = t0 + r16;
+    const bool tok_ok = tok < a.T;
+    const __bf16* xrow = X + (tok_ok ? tok : 0) * (int64_t)d + kg;
+    const __bf16* wrow[NB];
+    bool wok[NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+        const int e = nb * 16 + r16;
+        wok[nb] = e < E;
+        wrow[nb] = W + (int64_t)(wok[nb] ? e : 0) * d + kg;
+    }
+    const bf16x8 zero8 = {};
+    const int nsteps = d / 32;
+    int s0 = wave;
+    for (; s0 + (U - 1) * RT_WAVES < nsteps; s0 += U * RT_WAVES) {
+        bf16x8 av[U], bv[U][NB];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int k = (s0 + u * RT_WAVES) * 32;
+            av[u] = tok_ok ? *(const bf16x8*)(xrow + k) : zero8;
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) bv[u][nb] = wok[nb] ? *(const bf16x8*)(wrow[nb] + k) : zero8;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+                acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[u], bv[u][nb], acc[nb], 0, 0, 0);
+    }
+    for (; s0 < nsteps; s0 += RT_WAVES) {
+        const int k = s0 * 32;
+        const bf16x8 x8 = tok_ok ? *(const bf16x8*)(xrow + k) : zero8;
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+            const bf16x8 w8 = wok[nb] ? *(const bf16x8*)(wrow[nb] + k) : zero8;
+            acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(x8, w8, acc[nb], 0, 0, 0);
+        }
+    }
+}
+
+template <int NBT>
 __global__ void __launch_bounds__(RT_THREADS)
 route_select_kernel(const RouteArgs a) {
     const int tid = threadIdx.x;
@@ -61,60 +115,70 @@ route_select_kernel(const RouteArgs a) {
     const int Epad = (E + 15) & ~15;
 
     extern __shared__ float smem[];
-    float* s_part = smem;                               // [RT_WAVES][RT_TB][Epad]
-    float* s_logit = smem;                              // reuses partition 0 after the sum
-    int32_t* s_t1k = (int32_t*)(smem + RT_WAVES * RT_TB * Epad);   // [E][gmax]
+    float* s_part = smem;                               // [RT_SLOTS][RT_TB][Epad]
+    float* s_logit = smem;                              // reuses slot 0 after the sum
+    int32_t* s_t1k = (int32_t*)(smem + RT_SLOTS * RT_TB * Epad);   // [E][gmax]
     float* s_t1q = (float*)(s_t1k + E * a.gmax);                   // [E][gmax]
     int32_t* s_t1n = (int32_t*)(s_t1q + E * a.gmax);               // [E]
     uint32_t* s_mask = (uint32_t*)(s_t1n + E);                     // [E]
     int* s_cnt = (int*)(s_mask + E);                               // [8 + M]
+    float* s_S = (float*)(s_cnt + 8 + M);                          // [M][M][E] if a.S_in_lds
+    const float* Stab = a.S_in_lds ? s_S : a.S;
 
     // stage the candidate tables (small) and clear the block counters
     for (int i = tid; i < E * a.gmax; i += RT_THREADS) { s_t1k[i] = a.t1_k[i]; s_t1q[i] = a.t1_q[i]; }
     for (int i = tid; i < E; i += RT_THREADS) { s_t1n[i] = a.t1_n[i]; s_mask[i] = a.srvmask[i]; }
     for (int i = tid; i < 8 + M; i += RT_THREADS) s_cnt[i] = 0;
+    if (a.S_in_lds)
+        for (int i = tid; i < M * M * E; i += RT_THREADS) s_S[i] = a.S[i];
+    // this thread's token location and budget, read before the router loop so
+    // that their latency is hidden behind it (lanes of waves 0-3 own tokens)
+    int loc_pre = 0;
+    float qhat_pre = 0.f;
+    {
+        const int64_t tp = t0 + (wave * 4 + (lane >> 4));
+        if (wave < RT_TB / 4 && tp < a.T) { loc_pre = a.loc_in[tp]; qhat_pre = a.qhat_in[tp]; }
+    }
 
     // ---------------- router logits ----------------
     if (a.dtype == ORDERMOE_BF16) {
-        const __bf16* X = (const __bf16*)a.x;
-        const __bf16* W = (const __bf16*)a.w_router;
         const int nblk = Epad / 16;
-        const int kq = d / RT_WAVES;                 // d % 64 == 0 -> kq % 16 == 0
-        const int kbeg = wave * kq, kend = kbeg + kq;
-        const int r16 = lane & 15, kg = (lane >> 4) * 8;
-        const int64_t tok = t0 + r16;
-        const bool tok_ok = tok < a.T;
-        const __bf16* xrow = X + (tok_ok ? tok : 0) * (int64_t)d;
-        f32x4 acc[16];
+        f32x4 acc[NBT];
 #pragma unroll
-        for (int i = 0; i < 16; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-        const bf16x8 zero8 = {};
-        for (int kk = kbeg; kk < kend; kk += 32) {
-            bf16x8 av = tok_ok ? *(const bf16x8*)(xrow + kk + kg) : zero8;
+        for (int i = 0; i < NBT; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+        // unroll depth: every wave keeps 16-32 loads of 16 bytes in flight
+        if constexpr (NBT == 1) router_k_loop<1, 16>(a, wave, lane, t0, acc);
+        else if constexpr (NBT == 2) router_k_loop<2, 8>(a, wave, lane, t0, acc);
+        else if constexpr (NBT == 4) router_k_loop<4, 4>(a, wave, lane, t0, acc);
+        else if constexpr (NBT == 8) router_k_loop<8, 2>(a, wave, lane, t0, acc);
+        else router_k_loop<16, 1>(a, wave, lane, t0, acc);
+        // acc[nb][i] = partial logit of token (lane/16)*4 + i, expert nb*16 + lane%16.
+        // Two-round reduction over the 8 waves in a fixed order: waves 4-7 hand
+        // their sums to waves 0-3, then the four slots are added.
+        const int r16 = lane & 15;
+        if (wave >= RT_SLOTS) {
 #pragma unroll
-            for (int nb = 0; nb < 16; ++nb) {
-                if (nb < nblk) {
-                    const int e = nb * 16 + r16;
-                    bf16x8 bv = e < E ? *(const bf16x8*)(W + (int64_t)e * d + kk + kg) : zero8;
-                    acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bv, acc[nb], 0, 0, 0);
-                }
-            }
+            for (int nb = 0; nb < NBT; ++nb)
+                if (nb < nblk)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        s_part[((wave - RT_SLOTS) * RT_TB + (lane >> 4) * 4 + i) * Epad + nb * 16 + r16] = acc[nb][i];
         }
-        // acc[nb][i] = partial logit of token (lane/16)*4 + i, expert nb*16 + lane%16
+        __syncthreads();
+        if (wave < RT_SLOTS) {
 #pragma unroll
-        for (int nb = 0; nb < 16; ++nb) {
-            if (nb < nblk) {
+            for (int nb = 0; nb < NBT; ++nb)
+                if (nb < nblk)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int tr = (lane >> 4) * 4 + i;
-                    s_part[(wave * RT_TB + tr) * Epad + nb * 16 + r16] = acc[nb][i];
-                }
-            }
+                    for (int i = 0; i < 4; ++i) {
+                        float* sp = &s_part[(wave * RT_TB + (lane >> 4) * 4 + i) * Epad + nb * 16 + r16];
+                        *sp = acc[nb][i] + *sp;
+                    }
         }
         __syncthreads();
         for (int i = tid; i < RT_TB * Epad; i += RT_THREADS) {
             float v = s_part[i];
-            for (int w = 1; w < RT_WAVES; ++w) v += s_part[w * RT_TB * Epad + i];
+            for (int w = 1; w < RT_SLOTS; ++w) v += s_part[w * RT_TB * Epad + i];
             s_logit[i] = v;
         }
     } else {
@@ -136,7 +200,8 @@ route_select_kernel(const RouteArgs a) {
     }
     __syncthreads();
 
-    // ---------------- per-token stage: 16 lanes per token ----------------
+    // ---------------- per-token stage: 16 lanes per token, waves 0-3 ----------------
+    if (wave < RT_TB / 4) {
     const int g = lane >> 4;                 // token within the wave
     const int j = lane & 15;                 // lane within the token group
     const int tr = wave * 4 + g;             // token within the block
@@ -190,9 +255,9 @@ route_select_kernel(const RouteArgs a) {
     }
 
     // server-expert selection, slots in rank order
-    const int s_loc = valid ? (int)a.loc_in[t] : 0;
+    const int s_loc = loc_pre;
     const bool loc_ok = s_loc < M;
-    float qhat = valid ? a.qhat_in[t] : 0.f;
+    float qhat = qhat_pre;
     const bool subs_on = a.allow_sub && a.Qbar > 0.f;
     const uint32_t mmask = M >= 32 ? 0xFFFFFFFFu : ((1u << M) - 1u);   // servers that exist
     int first_m = s_loc, ncls[4] = {0, 0, 0, 0}, nremote = 0;
@@ -220,7 +285,7 @@ route_select_kernel(const RouteArgs a) {
                 while (ms) {
                     const int m = __builtin_ctz(ms);
                     ms &= ms - 1;
-                    const float J = fmaf(a.cq, qe, a.S[((int64_t)s_loc * M + m) * E + ke]);
+                    const float J = fmaf(a.cq, qe, Stab[((int64_t)s_loc * M + m) * E + ke]);
                     const uint64_t cand = ((uint64_t)__float_as_uint(J) << 32) |
                                           ((uint32_t)j << 6) | ((uint32_t)(m != s_loc) << 5) |
                                           (uint32_t)m;
@@ -273,6 +338,7 @@ route_select_kernel(const RouteArgs a) {
         }
         if (fl) atomicAdd(&s_cnt[4], 1);
     }
+    }   // token stage
     __syncthreads();
     if (tid < 8) a.blk_cnt[(int64_t)blockIdx.x * 8 + tid] = s_cnt[tid];
     if (tid < M) a.blk_dst[(int64_t)blockIdx.x * M + tid] = s_cnt[8 + tid];
@@ -357,33 +423,51 @@ dispatch_scatter_kernel(const uint8_t* exec_m, const uint8_t* loc_in, int64_t T,
     }
 }
 
+template <int NBT>
+int launch_route_kernel(const RouteArgs& a, size_t smem, hipStream_t st) {
+    if (smem > 65536) {
+        hipError_t e = hipFuncSetAttribute((const void*)route_select_kernel<NBT>,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+        if (e != hipSuccess) return (int)e;
+    }
+    KernelTimer kt_("route_select", st);
+    hipLaunchKernelGGL(route_select_kernel<NBT>, dim3(a.nblk), dim3(RT_THREADS), smem, st, a);
+    return (int)hipGetLastError();
+}
+
 }  // namespace
 
 int route_tokens_per_block() { return RT_TB; }
 
-size_t route_smem_bytes(int E, int gmax, int M) {
+size_t route_smem_bytes(int E, int gmax, int M, bool S_in_lds) {
     const int Epad = (E + 15) & ~15;
-    return sizeof(float) * (size_t)RT_WAVES * RT_TB * Epad + (size_t)E * gmax * 8 + (size_t)E * 8 +
-           sizeof(int) * (size_t)(8 + M);
+    return sizeof(float) * (size_t)RT_SLOTS * RT_TB * Epad + (size_t)E * gmax * 8 + (size_t)E * 8 +
+           sizeof(int) * (size_t)(8 + M) + (S_in_lds ? sizeof(float) * (size_t)M * M * E : 0);
+}
+
+// the cost table is staged in LDS when it is small enough to leave room for
+// two blocks per CU
+static bool route_S_in_lds(int E, int gmax, int M) {
+    return route_smem_bytes(E, gmax, M, true) <= 64 * 1024;
 }
 
 int launch_route_select(const RouteArgs& a, void* stream) {
     hipStream_t st = (hipStream_t)stream;
     if (a.nblk > 0) {
-        const size_t smem = route_smem_bytes(a.E, a.gmax, a.M);
-        static size_t lds_limit = 65536;
-        if (smem > lds_limit) {
-            hipError_t e = hipFuncSetAttribute((const void*)route_select_kernel,
-                                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
-            if (e != hipSuccess) return (int)e;
-            lds_limit = smem;
+        RouteArgs b = a;
+        b.S_in_lds = route_S_in_lds(a.E, a.gmax, a.M) ? 1 : 0;
+        const size_t smem = route_smem_bytes(a.E, a.gmax, a.M, b.S_in_lds != 0);
+        const int nb = (a.E + 15) / 16;
+        const int nbt = nb <= 1 ? 1 : nb <= 2 ? 2 : nb <= 4 ? 4 : nb <= 8 ? 8 : 16;
+        int e = 0;
+        switch (nbt) {
+            case 1: e = launch_route_kernel<1>(b, smem, st); break;
+            case 2: e = launch_route_kernel<2>(b, smem, st); break;
+            case 4: e = launch_route_kernel<4>(b, smem, st); break;
+            case 8: e = launch_route_kernel<8>(b, smem, st); break;
+            default: e = launch_route_kernel<16>(b, smem, st); break;
         }
-        {
-        KernelTimer kt_("route_select", st);
-        hipLaunchKernelGGL(route_select_kernel, dim3(a.nblk), dim3(RT_THREADS), smem, st, a);
-        }
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return (int)e;
+        if (e) return e;
     }
     {
         KernelTimer kt_("dispatch_scan", st);
