@@ -185,6 +185,30 @@ def _cpu_baseline(cfg, st, target_s: float):
                       "server %d); %.1f s" % (n, cfg.T, cfg.m0, dt)}
 
 
+def _simbuild(torch, om, reps: int = 5):
+    """Similarity-model build of a 128-expert layer over 65536 calibration tokens of
+    hidden 4096 (eq 3-5): average device time of its two kernels, HBM fraction."""
+    import workloads as wl
+    cfg = wl.C5_BUILD
+    up = lambda a: torch.from_numpy(wl.bf16_bits(a).view(np.int16)).view(torch.bfloat16).to("cuda")
+    xc, w = up(wl.calibration(cfg)), up(wl.router(cfg))
+    ws = torch.empty(om.ordermoe_similarity_workspace_size(cfg.T_cal, cfg.d, cfg.E),
+                     dtype=torch.uint8, device="cuda")
+    om.ordermoe_build_similarity(xc, w, cfg.k, cfg.theta, cfg.alpha_f, ws)   # warm-up
+    om.ordermoe_timing_read(reset=True)
+    om.ordermoe_timing_enable(True)
+    for _ in range(reps):
+        res = om.ordermoe_build_similarity(xc, w, cfg.k, cfg.theta, cfg.alpha_f, ws)
+    om.ordermoe_timing_enable(False)
+    kt = om.ordermoe_timing_read(reset=True)
+    us = sum(v[0] / v[1] for k, v in kt.items() if k.startswith("sim_")) * 1e3
+    nbytes = cfg.T_cal * cfg.d * 2 + cfg.E * cfg.d * 2
+    return {"workload": cfg.name, "groups": len(res["centres"]), "device_us": us,
+            "kernels_avg_us": {k: v[0] / v[1] * 1e3 for k, v in kt.items()},
+            "hbm_bytes": nbytes, "achieved_GBs": nbytes / us / 1e3,
+            "hbm_frac": nbytes / us / 1e3 / PEAK_HBM_GBS}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -192,6 +216,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-simbuild", action="store_true",
+                    help="skip the similarity-build measurement (65536 x 4096 calibration tokens)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a 1 GiB device copy (to scale rocprofv3 byte counters)")
     args = ap.parse_args()
@@ -266,6 +292,9 @@ def main():
         "kernels_avg_us": {k: v[0] / v[1] * 1e3 for k, v in sorted(kt.items())},
         "mfma_frac_ffn": (2.0 * R * cfg.d * 3 * cfg.f) / (ms_step / 1e3) / 1e12 / PEAK_BF16_TFLOPS,
     }
+    if not args.no_simbuild:
+        print("bench: similarity build", file=sys.stderr, flush=True)
+        res["similarity_build"] = _simbuild(torch, om)
     if not args.no_cpu_baseline:
         print("bench: timing the CPU oracle", file=sys.stderr, flush=True)
         res["cpu_baseline"] = _cpu_baseline(cfg, st, args.cpu_seconds)

@@ -36,7 +36,7 @@ extern "C" const char* ordermoe_last_error(void) { return g_err.c_str(); }
 static int sim_parts(int64_t T_cal) {
     const int64_t tc = similarity_tokens_per_chunk(0);
     const int64_t chunks = (T_cal + tc - 1) / tc;
-    return (int)std::min<int64_t>(chunks, 512);
+    return (int)std::min<int64_t>(chunks, 256);   // one partial per CU at most
 }
 
 static size_t sim_ws(int64_t T_cal, Carver& c, SimArgs* a) {
@@ -44,7 +44,8 @@ static size_t sim_ws(int64_t T_cal, Carver& c, SimArgs* a) {
     const int emax = similarity_max_experts();
     float* g = c.take<float>((size_t)parts * emax * emax);
     int32_t* n = c.take<int32_t>((size_t)parts * emax);
-    if (a) { a->gram_part = g; a->count_part = n; a->nchunk = parts; }
+    double* gr = c.take<double>((size_t)emax * emax);
+    if (a) { a->gram_part = g; a->count_part = n; a->gram = gr; a->nchunk = parts; }
     return c.size();
 }
 

@@ -115,6 +115,7 @@ struct SimArgs {
     int64_t* counts;       // [E]
     float* gram_part;      // [nchunk][128][128] per-block partial Gram matrices
     int32_t* count_part;   // [nchunk][128] per-block activation counts
+    double* gram;          // [128][128] reduced Gram matrix
     int nchunk;            // blocks of the partial kernel (= number of partials)
 };
 int launch_similarity(const SimArgs& a, void* stream);

@@ -70,7 +70,28 @@ __global__ void __launch_bounds__(256) sim_partial_kernel(const SimArgs a) {
             for (int i = 0; i < 4; ++i)
 #pragma unroll
                 for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-            for (int kk = 0; kk < d; kk += 32) {
+            // U K-steps of loads are issued before they are multiplied, so each
+            // wave keeps 8 * U loads of 16 bytes in flight (d % 64 == 0)
+            constexpr int U = 4;
+            int kk = 0;
+            for (; kk + 32 * U <= d; kk += 32 * U) {
+                bf16x8 av[U][4], bv[U][4];
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        av[u][i] = wok[i] ? *(const bf16x8*)(wp[i] + kk + 32 * u) : zero8;
+                        bv[u][i] = xok[i] ? *(const bf16x8*)(xp[i] + kk + 32 * u) : zero8;
+                    }
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+#pragma unroll
+                        for (int j = 0; j < 4; ++j)
+                            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[u][i], bv[u][j], acc[i][j], 0, 0, 0);
+            }
+            for (; kk < d; kk += 32) {
                 bf16x8 av[4], bv[4];
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
@@ -110,19 +131,38 @@ __global__ void __launch_bounds__(256) sim_partial_kernel(const SimArgs a) {
         }
         __syncthreads();
 
-        // activation counts: top-k of each token's logits, ties to the lower index
-        if (tid < SIM_TC && t0 + tid < a.T_cal) {
-            uint64_t taken[SIM_EMAX / 64] = {0, 0};
-            for (int r = 0; r < a.k; ++r) {
-                int best = -1;
-                float bv = 0.f;
-                for (int e = 0; e < E; ++e) {
-                    if (taken[e >> 6] & (1ull << (e & 63))) continue;
-                    const float v = s_H[e][tid];
-                    if (best < 0 || v > bv) { best = e; bv = v; }
+        // activation counts: top-k of each token's logits, ties to the lower
+        // index; 16 lanes per token, each holding experts lane%16 + 16 i, a
+        // 64-bit (logit, -index) key max-reduced over the lanes per rank
+        {
+            const int g16 = lane >> 4, j16 = lane & 15;
+            for (int tb = wave * 4; tb < SIM_TC; tb += 16) {
+                const int tt = tb + g16;
+                const bool tok = t0 + tt < a.T_cal;
+                uint32_t removed = 0;
+                for (int r = 0; r < a.k; ++r) {
+                    uint64_t best = 0;
+                    for (int i = 0, e = j16; e < E; ++i, e += 16) {
+                        if (removed & (1u << i)) continue;
+                        const uint32_t u = __float_as_uint(s_H[e][tt]);
+                        const uint32_t o = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+                        const uint64_t key = ((uint64_t)o << 32) | (uint32_t)(0xFFFFu - (uint32_t)e);
+                        best = key > best ? key : best;
+                    }
+#pragma unroll
+                    for (int off = 8; off >= 1; off >>= 1) {
+                        uint32_t lo = (uint32_t)best, hi = (uint32_t)(best >> 32);
+                        lo = __shfl_xor(lo, off, 16);
+                        hi = __shfl_xor(hi, off, 16);
+                        const uint64_t o = ((uint64_t)hi << 32) | lo;
+                        best = o > best ? o : best;
+                    }
+                    const int e = (int)(0xFFFFu - (uint32_t)(best & 0xFFFFu));
+                    if ((e & 15) == j16) {
+                        removed |= 1u << (e >> 4);
+                        if (tok) atomicAdd(&s_cnt[e], 1);
+                    }
                 }
-                taken[best >> 6] |= 1ull << (best & 63);
-                atomicAdd(&s_cnt[best], 1);
             }
         }
         // Gram of this chunk; rows/columns beyond E hold zeros from the MFMA padding
@@ -147,34 +187,46 @@ __global__ void __launch_bounds__(256) sim_partial_kernel(const SimArgs a) {
     for (int i = tid; i < SIM_EMAX; i += 256) a.count_part[(int64_t)blockIdx.x * SIM_EMAX + i] = s_cnt[i];
 }
 
-__global__ void __launch_bounds__(1024) sim_finalize_kernel(const SimArgs a, int nparts) {
-    __shared__ double s_diag[SIM_EMAX];
-    const int E = a.E;
-    const int tid = threadIdx.x;
-    // diagonal first (norms of the rows of H)
-    for (int i = tid; i < E; i += 1024) {
-        double s = 0.0;
-        for (int b = 0; b < nparts; ++b) s += (double)a.gram_part[(int64_t)b * SIM_EMAX * SIM_EMAX + i * SIM_EMAX + i];
-        s_diag[i] = s;
+// Fixed-order fp64 sum of the per-block partial Gram matrices and counts;
+// one thread per (i, j) entry, consecutive threads on consecutive columns.
+__global__ void __launch_bounds__(256) sim_reduce_kernel(const SimArgs a, int nparts, double* gram) {
+    const int p = blockIdx.x * 256 + threadIdx.x;
+    if (p >= SIM_EMAX * SIM_EMAX) return;
+    const int i = p / SIM_EMAX, j = p % SIM_EMAX;
+    if (i >= a.E || j >= a.E) return;
+    // 8 interleaved partial sums (fixed order) keep 8 loads in flight
+    double s8[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    const float* src = a.gram_part + p;
+    int b = 0;
+    for (; b + 8 <= nparts; b += 8) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) s8[q] += (double)src[(int64_t)(b + q) * SIM_EMAX * SIM_EMAX];
+    }
+    for (int q = 0; b < nparts; ++b, ++q) s8[q] += (double)src[(int64_t)b * SIM_EMAX * SIM_EMAX];
+    double s = 0.0;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) s += s8[q];
+    gram[p] = s;
+    if (i == 0) {
         int64_t c = 0;
-        for (int b = 0; b < nparts; ++b) c += (int64_t)a.count_part[(int64_t)b * SIM_EMAX + i];
-        a.counts[i] = c;
+        for (int b = 0; b < nparts; ++b) c += (int64_t)a.count_part[(int64_t)b * SIM_EMAX + j];
+        a.counts[j] = c;
     }
-    __syncthreads();
-    for (int p = tid; p < E * E; p += 1024) {
-        const int i = p / E, j = p % E;
-        float out;
-        if (i == j) {
-            out = 1.0f;
-        } else {
-            double s = 0.0;
-            for (int b = 0; b < nparts; ++b)
-                s += (double)a.gram_part[(int64_t)b * SIM_EMAX * SIM_EMAX + i * SIM_EMAX + j];
-            const double den = sqrt(s_diag[i]) * sqrt(s_diag[j]);
-            out = den > 0.0 ? (float)(s / den) : 0.0f;
-        }
-        a.sim[p] = out;
+}
+
+// cosine of eq 4 from the reduced Gram matrix; a zero norm gives 0 off the
+// diagonal, every diagonal entry is 1
+__global__ void __launch_bounds__(256) sim_normalise_kernel(const SimArgs a, const double* gram) {
+    const int p = blockIdx.x * 256 + threadIdx.x;
+    const int E = a.E;
+    if (p >= E * E) return;
+    const int i = p / E, j = p % E;
+    float out = 1.0f;
+    if (i != j) {
+        const double den = sqrt(gram[i * SIM_EMAX + i]) * sqrt(gram[j * SIM_EMAX + j]);
+        out = den > 0.0 ? (float)(gram[i * SIM_EMAX + j] / den) : 0.0f;
     }
+    a.sim[p] = out;
 }
 
 __global__ void pack_gate_up_kernel(int esz, int64_t n, int f, int d, const char* g, const char* u,
@@ -206,9 +258,17 @@ int launch_similarity(const SimArgs& a, void* stream) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return (int)e;
     {
-        KernelTimer kt_("sim_finalize", st);
-        hipLaunchKernelGGL(sim_finalize_kernel, dim3(1), dim3(1024), 0, st, a, a.nchunk);
-        }
+        KernelTimer kt_("sim_reduce", st);
+        hipLaunchKernelGGL(sim_reduce_kernel, dim3(SIM_EMAX * SIM_EMAX / 256), dim3(256), 0, st, a,
+                           a.nchunk, a.gram);
+    }
+    e = hipGetLastError();
+    if (e != hipSuccess) return (int)e;
+    {
+        KernelTimer kt_("sim_normalise", st);
+        hipLaunchKernelGGL(sim_normalise_kernel, dim3((a.E * a.E + 255) / 256), dim3(256), 0, st, a,
+                           (const double*)a.gram);
+    }
     e = hipGetLastError();
     return (int)e;
 }
