@@ -104,7 +104,8 @@ struct ForwardArgs {
 };
 int launch_local_forward(const ForwardArgs& a, void* stream);
 int forward_tokens_per_block();
-void forward_tile_shape(int dtype, int* bm_gu, int* bn_gu, int* bm_dn, int* bn_dn);
+bool forward_uses_thin(int dtype, int64_t T);
+void forward_tile_shape(int dtype, int64_t T, int* bm_gu, int* bn_gu, int* bm_dn, int* bn_dn);
 
 struct SimArgs {
     int dtype, d, E, k;

@@ -443,6 +443,139 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
     }
 }
 
+// Thin grouped GEMM for small batches (decode): a few rows per expert, so the
+// time is the weight stream from HBM and the MFMA work is incidental.  A
+// workgroup computes 32 rows x 64 weight rows (a gate/up granule pair, or 64
+// output columns of the down projection) over the whole K.  Its 4 waves take
+// interleaved K steps of 64 (wave w: steps w, w+4, ...), so the workgroup
+// streams 512 contiguous bytes of each weight row per round.  Operands go from
+// global memory straight into MFMA registers in the v_mfma_f32_32x32x16_bf16
+// layout (lane: row lane%32, K elements 8*(lane/32) .. +7 of each 16), the
+// next step's reads issued before the current step's MFMAs.  The waves'
+// partial sums meet in LDS and are added in wave order, then the epilogue of
+// ggemm_bf16 runs on the sums.
+constexpr int TH_BM = 32, TH_BN = 64, TH_WAVES = 4;
+
+template <int MODE>
+__global__ void __launch_bounds__(256, 2) ggemm_thin(const GemmArgs p) {
+    __shared__ float red[TH_WAVES][2][16][64];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: K offsets go in SGPRs
+    const int c = lane & 31, h = lane >> 5;
+    const int total = *p.ntiles;
+    const int per_xcd = gridDim.x >> 3;
+    const int vid = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+    constexpr uint32_t OOR = 0x80000000u;
+
+    for (int tile = vid; tile < total; tile += gridDim.x) {
+        TileLoc L;
+        if (!decode_tile<TH_BM, TH_BN>(p, tile, L)) break;
+        const bool shared = L.g >= p.n_routed;
+        const int K = L.K;
+        const __bf16* Bw = shared ? (const __bf16*)p.Ws
+                                  : (const __bf16*)p.Wr + (size_t)L.g * L.N * K;
+        const __amdgpu_buffer_rsrc_t rb_rs = make_rsrc(Bw, (uint32_t)((size_t)L.N * K * 2));
+        const uint32_t boff0 = ((uint32_t)(L.n0 + c) * (uint32_t)K + 8u * h) * 2u;
+        const uint32_t boff1 = boff0 + 64u * (uint32_t)K;          // 32 rows further
+        const int row = L.m0 + c;
+        __amdgpu_buffer_rsrc_t ra_rs;
+        uint32_t aoff;
+        if (MODE == 0) {
+            ra_rs = make_rsrc(p.X, p.x_bytes);
+            aoff = row < L.R ? ((uint32_t)p.row_tok[L.rowbase + row] * (uint32_t)p.ldx + 8u * h) * 2u : OOR;
+        } else {
+            const __bf16* Ab = shared ? (const __bf16*)p.As : (const __bf16*)p.Ar + (size_t)L.rowbase * K;
+            ra_rs = make_rsrc(Ab, (uint32_t)((size_t)L.R * K * 2));
+            aoff = row < L.R ? ((uint32_t)row * (uint32_t)K + 8u * h) * 2u : OOR;
+        }
+        const int KS = K / 64;
+        const int nst = (KS - wave + TH_WAVES - 1) / TH_WAVES;   // steps of this wave
+
+        f32x16 acc0, acc1;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) { acc0[e] = 0.f; acc1[e] = 0.f; }
+        bf16x8 a[2][4], b0[2][4], b1[2][4];
+        auto load = [&](int buf, int it) {
+            const int st = wave + it * TH_WAVES;
+            // a step past the end reads zeros through the range check and is never used
+            const uint32_t ok = it < nst ? 0u : OOR;
+            const uint32_t k0 = (uint32_t)st * 128u;   // bytes
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const uint32_t so = k0 + 32u * i;
+                b0[buf][i] = buf_load16(rb_rs, boff0 | ok, so);
+                b1[buf][i] = buf_load16(rb_rs, boff1 | ok, so);
+                a[buf][i] = buf_load16(ra_rs, aoff | ok, so);
+            }
+        };
+        auto mma = [&](int buf) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[buf][i], b0[buf][i], acc0, 0, 0, 0);
+                acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[buf][i], b1[buf][i], acc1, 0, 0, 0);
+            }
+        };
+        // two register sets, one step of reads always in flight; fences keep
+        // the reads ahead of the MFMAs.  With an odd step count the last mma(1)
+        // multiplies zeros read past the end, which leaves the sums unchanged.
+        load(0, 0);
+        for (int it = 0; it < nst; it += 2) {
+            load(1, it + 1);
+            __builtin_amdgcn_sched_barrier(0);
+            mma(0);
+            __builtin_amdgcn_sched_barrier(0);
+            load(0, it + 2);
+            __builtin_amdgcn_sched_barrier(0);
+            mma(1);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            red[wave][0][e][lane] = acc0[e];
+            red[wave][1][e][lane] = acc1[e];
+        }
+        __syncthreads();
+        // element e of lane l in a 32x32 block: row (e/4)*8 + (l/32)*4 + e%4, column l%32
+        if (MODE == 0) {
+            __bf16* out = shared ? (__bf16*)p.Os : (__bf16*)p.Or;
+            const int ldo = L.N / 2;
+            const int orow0 = shared ? 0 : L.rowbase;
+            const int col = tid & 31, rg = tid >> 5;
+            const int ln = col + 32 * (rg >> 2);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int r = rg + 8 * i;            // row inside the tile
+                const int e = 4 * i + (rg & 3);
+                float gv = 0.f, uv = 0.f;
+#pragma unroll
+                for (int w = 0; w < TH_WAVES; ++w) { gv += red[w][0][e][ln]; uv += red[w][1][e][ln]; }
+                if (L.m0 + r < L.R)
+                    out[(size_t)(orow0 + L.m0 + r) * ldo + L.n0 / 2 + col] = (__bf16)(silu_f(gv) * uv);
+            }
+        } else {
+            __bf16* out = (__bf16*)p.Or;
+            const int ldo = L.N;
+            const int col = tid & 63, rg = tid >> 6;
+            const int j = col >> 5, cl = col & 31;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int r = rg + 4 * i;
+                const int e = 4 * (r >> 3) + (r & 3);
+                const int ln = cl + 32 * ((r >> 2) & 1);
+                float v = 0.f;
+#pragma unroll
+                for (int w = 0; w < TH_WAVES; ++w) v += red[w][j][e][ln];
+                if (L.m0 + r < L.R) {
+                    const float wr = p.row_w[L.rowbase + L.m0 + r];
+                    out[(size_t)(L.rowbase + L.m0 + r) * ldo + L.n0 + col] = (__bf16)(v * wr);
+                }
+            }
+        }
+        __syncthreads();
+    }
+}
+
 // fp32 storage: plain LDS-tiled FMA GEMM, 64 x 64 tiles, 4 x 4 outputs per thread
 template <int MODE>
 __global__ void __launch_bounds__(256) ggemm_f32(const GemmArgs p) {
@@ -568,6 +701,10 @@ __global__ void __launch_bounds__(256) combine_kernel(const CombineArgs c) {
 
 constexpr int GU_BM = 256, GU_BN = 256, DN_BM = 192, DN_BN = 256;   // bf16 GEMM tiles
 constexpr int F32_BM = 64, F32_BN = 64;
+// bf16 batches of at most THIN_MAX_T tokens (every expert then has at most that
+// many rows) take the thin GEMM, THIN_PER_CU resident workgroups per CU
+constexpr int64_t THIN_MAX_T = 128;
+constexpr int THIN_PER_CU = 3;
 
 template <int BM, int BN>
 constexpr size_t bf16_gemm_lds() { return (size_t)2 * (BM + BN) * (64 + 8) * 2; }
@@ -594,8 +731,11 @@ int persistent_grid(int64_t upper_tiles, int per_cu) {
 
 int forward_tokens_per_block() { return FT_TB; }
 
-void forward_tile_shape(int dtype, int* bm_gu, int* bn_gu, int* bm_dn, int* bn_dn) {
-    if (dtype == ORDERMOE_BF16) { *bm_gu = GU_BM; *bn_gu = GU_BN; *bm_dn = DN_BM; *bn_dn = DN_BN; }
+bool forward_uses_thin(int dtype, int64_t T) { return dtype == ORDERMOE_BF16 && T <= THIN_MAX_T; }
+
+void forward_tile_shape(int dtype, int64_t T, int* bm_gu, int* bn_gu, int* bm_dn, int* bn_dn) {
+    if (forward_uses_thin(dtype, T)) { *bm_gu = *bm_dn = TH_BM; *bn_gu = *bn_dn = TH_BN; }
+    else if (dtype == ORDERMOE_BF16) { *bm_gu = GU_BM; *bn_gu = GU_BN; *bm_dn = DN_BM; *bn_dn = DN_BN; }
     else { *bm_gu = F32_BM; *bn_gu = F32_BN; *bm_dn = F32_BM; *bn_dn = F32_BN; }
 }
 
@@ -603,8 +743,9 @@ int launch_local_forward(const ForwardArgs& f, void* stream) {
     hipStream_t st = (hipStream_t)stream;
     const int has_sh = f.n_shared > 0 ? 1 : 0;
     const int G = f.n_local + has_sh;
+    const bool thin = forward_uses_thin(f.dtype, f.T);
     int bm_gu, bn_gu, bm_dn, bn_dn;
-    forward_tile_shape(f.dtype, &bm_gu, &bn_gu, &bm_dn, &bn_dn);
+    forward_tile_shape(f.dtype, f.T, &bm_gu, &bn_gu, &bm_dn, &bn_dn);
 
     RowsArgs r;
     r.T = f.T; r.k = f.k; r.E = f.E; r.n_local = f.n_local; r.has_shared = has_sh; r.server = f.server;
@@ -650,7 +791,13 @@ int launch_local_forward(const ForwardArgs& f, void* stream) {
                     (has_sh ? ((rows_s + bm_gu - 1) / bm_gu + 1) * (2 * f.n_shared * f.f / bn_gu) : 0);
     int64_t ub_dn = ((rows_r + rows_s + bm_dn - 1) / bm_dn + G) * (f.d / bn_dn);
 
-    if (f.dtype == ORDERMOE_BF16) {
+    if (thin) {
+        {
+        KernelTimer kt_("gemm_gate_up", st);
+        ggemm_thin<0><<<dim3(persistent_grid(ub_gu, THIN_PER_CU)), dim3(256), 0, st>>>(g);
+        }
+        if ((e = hipGetLastError()) != hipSuccess) return (int)e;
+    } else if (f.dtype == ORDERMOE_BF16) {
         static int lds_ok = -1;
         if (lds_ok < 0) {
             lds_ok = set_lds(ggemm_bf16<GU_BM, GU_BN, 0>, bf16_gemm_lds<GU_BM, GU_BN>()) |
@@ -675,7 +822,12 @@ int launch_local_forward(const ForwardArgs& f, void* stream) {
     g.ntiles = f.tile_info + 1;
     g.Nr = f.d; g.Kr = f.f; g.Ns = f.d; g.Ks = f.n_shared * f.f;
     g.Wr = f.w_dn; g.Ws = f.w_sh_dn; g.Ar = f.act_r; g.As = f.act_s; g.Or = f.obuf; g.Os = nullptr;
-    if (f.dtype == ORDERMOE_BF16) {
+    if (thin) {
+        {
+        KernelTimer kt_("gemm_down", st);
+        ggemm_thin<1><<<dim3(persistent_grid(ub_dn, THIN_PER_CU)), dim3(256), 0, st>>>(g);
+        }
+    } else if (f.dtype == ORDERMOE_BF16) {
         {
         KernelTimer kt_("gemm_down", st);
         ggemm_bf16<DN_BM, DN_BN, 1>

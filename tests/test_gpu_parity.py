@@ -28,6 +28,12 @@ SMALL = {
     "C3s": wl.C3.with_(T=1500, T_cal=4096),
     "C4s": wl.C4.with_(T=1700, T_cal=4096),
 }
+# decode-sized batches (at most 128 tokens): the thin-GEMM path of the forward
+DECODE = {
+    "C2d": wl.C2.with_(T=64, T_cal=4096),
+    "C3d": wl.C3.with_(T=128, T_cal=4096),
+    "C4d": wl.C4.with_(T=97, T_cal=4096),
+}
 FULL = {"C2": wl.C2.with_(T_cal=4096), "C3": wl.C3.with_(T_cal=4096), "C4": wl.C4.with_(T_cal=4096)}
 
 _cache = {}
@@ -113,6 +119,20 @@ def test_layer_parity_small(name):
     # row offsets: the GPU's own local rows, recounted from its decisions
     rows = host(ro)
     assert rows[0] == 0 and np.all(np.diff(rows) >= 0)
+    _check_output(case, dec, y, np.arange(T), ok, TOL[case.cfg.dtype])
+
+
+@pytest.mark.parametrize("name", list(DECODE))
+def test_layer_parity_decode_batch(name):
+    case, tabs = _case(name, DECODE[name])
+    dl = DeviceLayer(case, tabs)
+    x, loc, qh = dl.inputs()
+    T = case.X.shape[0]
+    out = dl.route(x, loc, qh, T)
+    y, ro = dl.forward(x, loc, out, T)
+    torch.cuda.synchronize()
+    dec = oracle_decisions(case)
+    ok = _check_decisions(case, dec, out)
     _check_output(case, dec, y, np.arange(T), ok, TOL[case.cfg.dtype])
 
 
@@ -248,8 +268,9 @@ def test_invalid_locations_are_counted_not_routed():
     assert c[:4].sum() == (case.X.shape[0] - 2) * case.cfg.k
 
 
-def test_runs_are_bitwise_deterministic():
-    case, tabs = _case("C3s", SMALL["C3s"])
+@pytest.mark.parametrize("name", ["C3s", "C3d"])
+def test_runs_are_bitwise_deterministic(name):
+    case, tabs = _case(name, {**SMALL, **DECODE}[name])
     dl = DeviceLayer(case, tabs)
     x, loc, qh = dl.inputs()
     T = case.X.shape[0]
