@@ -209,6 +209,128 @@ def _simbuild(torch, om, reps: int = 5):
             "hbm_frac": nbytes / us / 1e3 / PEAK_HBM_GBS}
 
 
+def _decode_stream(torch, om, steps: int = 10, warmup: int = 2):
+    """Decode stream through a 32-layer stack of 128-expert top-8 layers (64
+    tokens, hidden 4096, FFN 1536, 8 servers, memory ratio 2.0, H = 3), server
+    0's share: per layer route/select with the location and accumulated loss
+    carried on the device from the previous layer, then the local expert FFN.
+    The offline model is built by the library (similarity on the device,
+    transitions, deployment, look-ahead and tables on the host).  Expert
+    weights of server 0 (32 per layer, 38.7 GB in all) are drawn on the device,
+    N(0, 0.02^2) in bf16, and stay resident.  Reports device time per layer and
+    the HBM fraction of the weights the layer has to stream."""
+    import workloads as wl
+    cfg = wl.C5_STREAM
+    dev = "cuda"
+    up = lambda a: torch.from_numpy(wl.bf16_bits(a).view(np.int16)).view(torch.bfloat16).to(dev)
+    N, E, M, T, k = cfg.N, cfg.E, cfg.M, cfg.T, cfg.k
+    W = wl.stream_routers(cfg)
+    theta = [om.ordermoe_theta_layer(l + 1, N, cfg.theta_min, cfg.theta_max) for l in range(N)]
+    ws = torch.empty(om.ordermoe_similarity_workspace_size(cfg.T_cal, cfg.d, E), dtype=torch.uint8,
+                     device=dev)
+    top1 = torch.empty((N, cfg.T_cal), dtype=torch.int32, device=dev)
+    w_router, models = [], []
+    for l, Xc in enumerate(wl.stream_calibration(cfg)):
+        w_router.append(up(W[l]))
+        models.append(om.ordermoe_build_similarity(up(Xc), w_router[l], k, theta[l], cfg.alpha_f, ws,
+                                                   top1=top1[l]))
+    del ws
+    P = om.ordermoe_estimate_transitions(top1.cpu().numpy(), E)
+    x_dep, _ = om.ordermoe_place([m["group_of"] for m in models], [m["importance"] for m in models],
+                                 [np.ones(E)] * N, np.array(cfg.capacity), np.full(M, 1.0 / M),
+                                 cfg.lambda1, 1)
+    net = wl.network(cfg)
+    c = np.full(E, 6.0 * cfg.d * cfg.f)
+    dref = float(np.mean(c)) / float(np.mean(net.F))
+    z_bits = 8.0 * cfg.d * cfg.bytes_per_el
+    phi = om.ordermoe_build_lookahead(cfg.H, P, np.stack(x_dep), np.stack([m["sim"] for m in models]),
+                                      np.stack([m["group_of"] for m in models]),
+                                      np.array(theta, np.float32), np.full(N, z_bits), np.tile(c, (N, 1)),
+                                      np.full(N, dref), net.B, net.tau, net.F, cfg.omega_T, cfg.omega_Q,
+                                      cfg.Qbar, cfg.pin_local_exact, cfg.allow_sub)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(cfg.seed)
+    layers = []
+    for l in range(N):
+        tabs = om.ordermoe_build_tables(models[l]["sim"], models[l]["group_of"], theta[l], x_dep[l],
+                                        net.B, net.tau, net.F, z_bits, c, dref, cfg.omega_T, phi[l])
+        tdev = {n: torch.from_numpy(np.ascontiguousarray(v)).to(dev) for n, v in tabs.items()
+                if n != "srvmask"}
+        tdev["srvmask"] = torch.from_numpy(tabs["srvmask"].view(np.int32)).to(dev)
+        L = om.make_layer(om.BF16, cfg.d, E, k, M, 15, w_router[l], tdev, cfg.Qbar, cfg.omega_Q,
+                          cfg.pin_local_exact, cfg.allow_sub, cfg.renorm)
+        local = [int(j) for j in np.nonzero(x_dep[l][cfg.m0])[0]]
+        n = len(local)
+        g = torch.randn((n, cfg.f, cfg.d), generator=gen, device=dev, dtype=torch.bfloat16) * 0.02
+        u = torch.randn((n, cfg.f, cfg.d), generator=gen, device=dev, dtype=torch.bfloat16) * 0.02
+        w_gu = torch.empty((n, 2 * cfg.f, cfg.d), dtype=torch.bfloat16, device=dev)
+        om.ordermoe_pack_gate_up(g, u, w_gu)
+        del g, u
+        w_dn = torch.randn((n, cfg.d, cfg.f), generator=gen, device=dev, dtype=torch.bfloat16) * 0.02
+        ex = om.make_experts(om.BF16, cfg.d, cfg.f, E, local, w_gu, w_dn)
+        out = om.alloc_route_out(T, k, M, dev)
+        layers.append(dict(L=L, keep=(tdev, w_gu, w_dn), ex=ex, out=out, os=om.route_out_struct(out),
+                           ro=torch.empty(n + 2, dtype=torch.int32, device=dev), n_local=n))
+    X = wl.stream_tokens(cfg)
+    xs = [up(X[l]) for l in range(N)]
+    ws_r = torch.empty(om.ordermoe_route_workspace_size(T, k, M), dtype=torch.uint8, device=dev)
+    ws_f = torch.empty(max(max(om.ordermoe_forward_workspace_size(Ld["ex"], T, k) for Ld in layers), 1),
+                       dtype=torch.uint8, device=dev)
+    y = torch.empty((T, cfg.d), dtype=torch.bfloat16, device=dev)
+    loc0 = torch.zeros(T, dtype=torch.uint8, device=dev)
+    q0 = torch.zeros(T, dtype=torch.float32, device=dev)
+    torch.cuda.synchronize()
+
+    def step():
+        loc, qh = loc0, q0
+        for l in range(N):
+            Ld = layers[l]
+            o = Ld["out"]
+            om.ordermoe_route_select(Ld["L"], xs[l], T, loc, qh, o, ws_r, out_struct=Ld["os"])
+            om.ordermoe_local_moe_forward(Ld["ex"], xs[l], T, k, o["w"], o["exec_k"], o["exec_m"], loc,
+                                          cfg.m0, y, Ld["ro"], ws_f)
+            loc, qh = o["loc_out"], o["qhat_out"]
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    # per-kernel averages from a separate pass (the events add a little time per launch)
+    om.ordermoe_timing_read(reset=True)
+    om.ordermoe_timing_enable(True)
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    om.ordermoe_timing_enable(False)
+    kt = om.ordermoe_timing_read(reset=True)
+    expert_bytes = 3 * cfg.f * cfg.d * 2
+    active, rows, cls = [], [], np.zeros(4, np.int64)
+    for Ld in layers:
+        ro = Ld["ro"].cpu().numpy()
+        active.append(int(np.sum(np.diff(ro[:Ld["n_local"] + 1]) > 0)))
+        rows.append(int(ro[-1]))
+        cls += Ld["out"]["counters"].cpu().numpy()[:4].astype(np.int64)
+    w_bytes = expert_bytes * float(np.sum(active))
+    other = N * (E * cfg.d * 2 + 2 * T * cfg.d * 2)        # routers, x in, y out
+    us_layer = ms / steps / N * 1e3
+    gemm_us = sum(kt[n][0] / kt[n][1] for n in ("gemm_gate_up", "gemm_down") if n in kt) * 1e3
+    return {"workload": cfg.name, "layers": N, "tokens": T, "server": cfg.m0,
+            "us_per_layer": us_layer, "ms_per_token_step": ms / steps,
+            "local_rows_per_layer": float(np.mean(rows)),
+            "active_local_experts_per_layer": float(np.mean(active)),
+            "classes_LE_LS_RE_RS": [int(v) for v in cls],
+            "weight_bytes_per_layer": w_bytes / N,
+            "hbm_frac_layer": (w_bytes + other) / (ms / steps / 1e3) / 1e9 / PEAK_HBM_GBS,
+            "hbm_frac_ffn_gemms": (w_bytes / N) / (gemm_us * 1e-6) / 1e9 / PEAK_HBM_GBS,
+            "kernels_avg_us": {n: v[0] / v[1] * 1e3 for n, v in sorted(kt.items())}}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -218,6 +340,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-simbuild", action="store_true",
                     help="skip the similarity-build measurement (65536 x 4096 calibration tokens)")
+    ap.add_argument("--no-stream", action="store_true",
+                    help="skip the 32-layer decode-stream measurement")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a 1 GiB device copy (to scale rocprofv3 byte counters)")
     args = ap.parse_args()
@@ -295,6 +419,11 @@ def main():
     if not args.no_simbuild:
         print("bench: similarity build", file=sys.stderr, flush=True)
         res["similarity_build"] = _simbuild(torch, om)
+    if not args.no_stream:
+        print("bench: decode stream", file=sys.stderr, flush=True)
+        del st["experts"], st["keep"]
+        torch.cuda.empty_cache()
+        res["decode_stream"] = _decode_stream(torch, om)
     if not args.no_cpu_baseline:
         print("bench: timing the CPU oracle", file=sys.stderr, flush=True)
         res["cpu_baseline"] = _cpu_baseline(cfg, st, args.cpu_seconds)

@@ -107,19 +107,23 @@ const char* ordermoe_last_error(void);
  *   alpha_f    weight of the frequency in the importance (eq 28), alpha_r = 1 - alpha_f
  *   sim_dev    dev  [E][E] float, out: Sim_l
  *   counts_dev dev  [E] int64, out: n_j
+ *   top1_dev   dev  [T_cal] int32, out (may be NULL): the top-1 expert of each
+ *              calibration token under the same rule -- the input of the
+ *              transition estimate of eq (41)
  *   sim_host, counts_host  host, out: copies of the two (may be NULL)
  *   group_of   host [E] int32, out: group index of each expert (groups are
  *              numbered in the order their dominant expert was chosen)
  *   centres    host [E] int32, out: dominant expert of each group, -1 padded
  *   num_groups host int32, out: K_l
  *   importance host [E] double, out: I_j (eq 28)
- * Requires d % 64 == 0, 1 <= E <= ORDERMOE_MAX_EXPERTS, T_cal >= 1.
+ * Requires d % 64 == 0, 1 <= E <= 128, T_cal >= 1.
  * Synchronises `stream` (the grouping runs on the host).
  */
 size_t ordermoe_similarity_workspace_size(int64_t T_cal, int32_t d, int32_t E);
 int ordermoe_build_similarity(const void* x_cal, int64_t T_cal, int32_t d, const void* w_router,
                               int32_t E, int32_t dtype, int32_t topk, float theta, double alpha_f,
-                              float* sim_dev, int64_t* counts_dev, float* sim_host,
+                              float* sim_dev, int64_t* counts_dev, int32_t* top1_dev,
+                              float* sim_host,
                               int64_t* counts_host, int32_t* group_of, int32_t* centres,
                               int32_t* num_groups, double* importance, void* ws, size_t ws_bytes,
                               void* stream);
@@ -203,6 +207,22 @@ int ordermoe_build_lookahead(int32_t N, int32_t E, int32_t M, int32_t H, const d
                              const double* d_ref, const double* B, const double* tau,
                              const double* F, double omega_T, double omega_Q, float Qbar,
                              int32_t pin_local_exact, int32_t allow_sub, double* phi_out);
+
+/* Transition probabilities between consecutive layers (eq 41), host only:
+ * P_l[k][k'] = the share of the calibration tokens with top-1 expert k at
+ * layer l whose top-1 expert at layer l+1 is k'; a row with no token is zero.
+ *   N layers (>= 1) of E experts, T_cal tokens followed through the stack;
+ *   top1 host [N][T_cal] int32 (from ordermoe_build_similarity's top1_dev of
+ *   each layer; an entry outside [0, E) is an EINVAL error);
+ *   P_out host [N-1][E][E] double (nothing is written when N = 1). */
+int ordermoe_estimate_transitions(int32_t N, int32_t E, int64_t T_cal, const int32_t* top1,
+                                  double* P_out);
+
+/* Similarity threshold of layer l (1-based) of an N-layer stack (eq 6):
+ * theta_l = theta_min + (theta_max - theta_min) (N - l) / (N - 1), in double,
+ * rounded to float.  N = 1, where eq 6 divides by zero, gives the midpoint.
+ * EINVAL unless 1 <= l <= N and theta_min <= theta_max. */
+int ordermoe_theta_layer(int32_t l, int32_t N, double theta_min, double theta_max, float* theta_out);
 
 /* ------------------------------------------------------------------------
  * Routing and server-expert selection of one layer (Section V, the per-layer

@@ -18,7 +18,10 @@ Redundant placement, over all layers (eq 32-35), greedy:
   * repeatedly deploy the candidate of largest positive benefit (ties: lower
     (l, m, j)), update y and b, until none is left.
 Reading of eq 32: the sum runs over the experts k of group g(j) in layer l.
-fp64 throughout.
+fp64 throughout.  The benefit of every candidate is evaluated elementwise with
+numpy (same operations and order per candidate as the formula above); the
+layers are padded to a common expert count with zero-importance entries,
+which never have a positive benefit.
 """
 from __future__ import annotations
 
@@ -51,10 +54,11 @@ def place(group_of: Sequence[np.ndarray], importance: Sequence[np.ndarray],
         waiting = []
         for j in order:
             best_m, best_score = -1, None
+            same_group = np.asarray(g) == g[j]
             for m in range(M):
                 if not (b[m] + p[l][j] <= C[m]):
                     continue
-                eta = sum(int(x[l][m, kk]) for kk in range(E) if g[kk] == g[j])
+                eta = int(np.sum(x[l][m, same_group]))
                 score = lambda1 * b[m] / C[m] + lambda2 * eta
                 if best_score is None or score < best_score:
                     best_m, best_score = m, score
@@ -69,25 +73,37 @@ def place(group_of: Sequence[np.ndarray], importance: Sequence[np.ndarray],
             b[best_m] += p[l][j]
 
     if redundancy:
+        Emax = max(len(gl) for gl in group_of)
+        G = np.zeros((N, Emax), dtype=np.int64)          # group ids (padding: own group)
+        I = np.zeros((N, Emax))                          # importance (padding: 0)
+        P = np.ones((N, Emax))                           # memory demand (padding: 1)
+        X = np.ones((N, M, Emax), dtype=np.uint8)        # deployment (padding: held)
+        for l in range(N):
+            E = len(group_of[l])
+            G[l, :E] = np.asarray(group_of[l])
+            G[l, E:] = G[l, :E].max(initial=-1) + 1 + np.arange(Emax - E)
+            I[l, :E] = importance[l]
+            P[l, :E] = p[l]
+            X[l, :, :E] = x[l]
+        pim = np.asarray(pi, dtype=np.float64)
+        same = G[:, :, None] == G[:, None, :]                          # [l, j, k]
+        # y[l, m, j] = 1 when server m holds some expert of j's group in layer l
+        y = np.zeros((N, M, Emax), dtype=np.int64)
+        for l in range(N):
+            for m in range(M):
+                for kk in np.nonzero(X[l, m])[0]:
+                    y[l, m, same[l, kk]] = 1
         while True:
-            best = None  # (benefit, l, m, j)
-            for l in range(N):
-                g = group_of[l]
-                E = len(g)
-                for m in range(M):
-                    covered = {int(g[kk]) for kk in range(E) if x[l][m, kk]}
-                    for j in range(E):
-                        if x[l][m, j] or not (b[m] + p[l][j] <= C[m]):
-                            continue
-                        y = 1 if int(g[j]) in covered else 0
-                        B = pi[m] * importance[l][j] * (1 - y) / p[l][j]
-                        if B <= 0:
-                            continue
-                        if best is None or B > best[0]:
-                            best = (B, l, m, j)
-            if best is None:
+            Bnf = pim[None, :, None] * I[:, None, :] * (1 - y) / P[:, None, :]
+            fits = (b[None, :, None] + P[:, None, :]) <= np.asarray(C)[None, :, None]
+            cand = (X == 0) & fits & (Bnf > 0)
+            if not cand.any():
                 break
-            _, l, m, j = best
+            Bm = np.where(cand, Bnf, -np.inf)
+            flat = int(np.argmax(Bm))           # first maximum: lowest (l, m, j)
+            l, m, j = np.unravel_index(flat, Bm.shape)
+            X[l, m, j] = 1
+            y[l, m, same[l, j]] = 1
             x[l][m, j] = 1
             b[m] += p[l][j]
     return x, b

@@ -110,13 +110,16 @@ def lookahead(H: int, P: Sequence[np.ndarray], x: Sequence[np.ndarray],
             val += omega_Q * q / Qbar
         return val
 
+    subs_memo = {}
+
     def candidates(l1, s, r1):
-        E1 = x[l1].shape[1]
         if pin_local_exact and x[l1][s, r1]:
             return [(s, r1)]
         ks = [r1]
         if allow_sub and Qbar > 0:
-            ks += [kk for kk, _ in substitutes(sim32[l1], group_of[l1], theta[l1], r1)]
+            if (l1, r1) not in subs_memo:
+                subs_memo[(l1, r1)] = [kk for kk, _ in substitutes(sim32[l1], group_of[l1], theta[l1], r1)]
+            ks += subs_memo[(l1, r1)]
         return [(m1, k1) for k1 in ks for m1 in range(M) if x[l1][m1, k1]]
 
     memo = {}
@@ -140,9 +143,10 @@ def lookahead(H: int, P: Sequence[np.ndarray], x: Sequence[np.ndarray],
                         if best is None or v < best:
                             best = v
                     V[m, r1] = 0.0 if best is None else best
-            for m in range(M):
-                for kk in range(E_l):
-                    out[m, kk] = sum(P[l][kk, r1] * V[m, r1] for r1 in range(E1))
+            # out[m, k] = sum over r1 of P[k, r1] V[m, r1], added in increasing r1
+            # (elementwise over (m, k), so every entry is the plain sequential sum)
+            for r1 in range(E1):
+                out += V[:, r1][:, None] * P[l][:, r1][None, :]
         memo[key] = out
         return out
 

@@ -59,7 +59,8 @@ extern "C" size_t ordermoe_similarity_workspace_size(int64_t T_cal, int32_t d, i
 extern "C" int ordermoe_build_similarity(const void* x_cal, int64_t T_cal, int32_t d,
                                          const void* w_router, int32_t E, int32_t dtype,
                                          int32_t topk, float theta, double alpha_f,
-                                         float* sim_dev, int64_t* counts_dev, float* sim_host,
+                                         float* sim_dev, int64_t* counts_dev, int32_t* top1_dev,
+                                         float* sim_host,
                                          int64_t* counts_host, int32_t* group_of,
                                          int32_t* centres, int32_t* num_groups,
                                          double* importance, void* ws, size_t ws_bytes,
@@ -79,7 +80,7 @@ extern "C" int ordermoe_build_similarity(const void* x_cal, int64_t T_cal, int32
 
     SimArgs a{};
     a.dtype = dtype; a.d = d; a.E = E; a.k = topk; a.x_cal = x_cal; a.T_cal = T_cal;
-    a.w_router = w_router; a.sim = sim_dev; a.counts = counts_dev;
+    a.w_router = w_router; a.sim = sim_dev; a.counts = counts_dev; a.top1 = top1_dev;
     Carver c(ws);
     sim_ws(T_cal, c, &a);
     int e = launch_similarity(a, stream);

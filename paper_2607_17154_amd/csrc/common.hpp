@@ -114,6 +114,7 @@ struct SimArgs {
     const void* w_router;
     float* sim;            // [E][E]
     int64_t* counts;       // [E]
+    int32_t* top1;         // [T_cal] top-1 expert of each token, or null
     float* gram_part;      // [nchunk][128][128] per-block partial Gram matrices
     int32_t* count_part;   // [nchunk][128] per-block activation counts
     double* gram;          // [128][128] reduced Gram matrix

@@ -299,3 +299,41 @@ extern "C" int ordermoe_build_lookahead(int32_t N, int32_t E, int32_t M, int32_t
     clear_error();
     return ORDERMOE_OK;
 }
+
+extern "C" int ordermoe_estimate_transitions(int32_t N, int32_t E, int64_t T_cal,
+                                             const int32_t* top1, double* P_out) {
+    if (N < 1 || E < 1 || E > ORDERMOE_MAX_EXPERTS || T_cal < 0)
+        return fail(ORDERMOE_EINVAL, "estimate_transitions: size out of range");
+    if (N == 1) { clear_error(); return ORDERMOE_OK; }
+    if (!top1 || !P_out) return fail(ORDERMOE_EINVAL, "estimate_transitions: null pointer");
+    for (int64_t i = 0; i < (int64_t)N * T_cal; ++i)
+        if (top1[i] < 0 || top1[i] >= E) return fail(ORDERMOE_EINVAL, "estimate_transitions: expert id out of range");
+    const size_t EE = (size_t)E * E;
+    std::vector<int64_t> n(EE);
+    for (int l = 0; l + 1 < N; ++l) {
+        std::fill(n.begin(), n.end(), 0);
+        const int32_t* a = top1 + (size_t)l * T_cal;
+        const int32_t* b = a + T_cal;
+        for (int64_t t = 0; t < T_cal; ++t) ++n[(size_t)a[t] * E + b[t]];
+        double* P = P_out + (size_t)l * EE;
+        for (int k = 0; k < E; ++k) {
+            int64_t tot = 0;
+            for (int k1 = 0; k1 < E; ++k1) tot += n[(size_t)k * E + k1];
+            for (int k1 = 0; k1 < E; ++k1)
+                P[(size_t)k * E + k1] = tot > 0 ? (double)n[(size_t)k * E + k1] / (double)tot : 0.0;
+        }
+    }
+    clear_error();
+    return ORDERMOE_OK;
+}
+
+extern "C" int ordermoe_theta_layer(int32_t l, int32_t N, double theta_min, double theta_max,
+                                    float* theta_out) {
+    if (N < 1 || l < 1 || l > N || !(theta_min <= theta_max) || !theta_out)
+        return fail(ORDERMOE_EINVAL, "theta_layer: need 1 <= l <= N and theta_min <= theta_max");
+    const double lo = theta_min, hi = theta_max;
+    *theta_out = N == 1 ? (float)(0.5 * (lo + hi))
+                        : (float)(lo + (hi - lo) * (double)(N - l) / (double)(N - 1));
+    clear_error();
+    return ORDERMOE_OK;
+}

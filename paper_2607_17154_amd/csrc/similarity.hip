@@ -158,6 +158,7 @@ __global__ void __launch_bounds__(256) sim_partial_kernel(const SimArgs a) {
                         best = o > best ? o : best;
                     }
                     const int e = (int)(0xFFFFu - (uint32_t)(best & 0xFFFFu));
+                    if (r == 0 && j16 == 0 && tok && a.top1) a.top1[t0 + tt] = e;
                     if ((e & 15) == j16) {
                         removed |= 1u << (e >> 4);
                         if (tok) atomicAdd(&s_cnt[e], 1);

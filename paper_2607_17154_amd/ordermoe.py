@@ -29,7 +29,8 @@ EXPORTS = ("ordermoe_last_error", "ordermoe_similarity_workspace_size", "ordermo
            "ordermoe_group_experts", "ordermoe_place", "ordermoe_build_tables",
            "ordermoe_build_lookahead", "ordermoe_route_workspace_size", "ordermoe_route_select",
            "ordermoe_forward_workspace_size", "ordermoe_local_moe_forward",
-           "ordermoe_pack_gate_up", "ordermoe_timing_enable", "ordermoe_timing_read")
+           "ordermoe_pack_gate_up", "ordermoe_timing_enable", "ordermoe_timing_read",
+           "ordermoe_estimate_transitions", "ordermoe_theta_layer")
 TIMING_NAME = 64
 
 
@@ -78,7 +79,11 @@ def lib() -> ctypes.CDLL:
     L.ordermoe_similarity_workspace_size.argtypes = [_I64, _I32, _I32]
     L.ordermoe_build_similarity.restype = ctypes.c_int
     L.ordermoe_build_similarity.argtypes = [_P, _I64, _I32, _P, _I32, _I32, _I32, _F32, _F64,
-                                            _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]
+                                            _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]
+    L.ordermoe_estimate_transitions.restype = ctypes.c_int
+    L.ordermoe_estimate_transitions.argtypes = [_I32, _I32, _I64, _P, _P]
+    L.ordermoe_theta_layer.restype = ctypes.c_int
+    L.ordermoe_theta_layer.argtypes = [_I32, _I32, _F64, _F64, _P]
     L.ordermoe_group_experts.restype = ctypes.c_int
     L.ordermoe_group_experts.argtypes = [_I32, _P, _P, _F32, _F64, _P, _P, _P, _P]
     L.ordermoe_place.restype = ctypes.c_int
@@ -159,14 +164,17 @@ def ordermoe_similarity_workspace_size(T_cal: int, d: int, E: int) -> int:
 
 
 def ordermoe_build_similarity(x_cal, w_router, topk: int, theta: float, alpha_f: float,
-                              workspace, stream=None) -> Dict[str, np.ndarray]:
-    """Sim and counts on the device, grouping on the host (eq 3-5, 24-28)."""
+                              workspace, stream=None, top1=None) -> Dict[str, np.ndarray]:
+    """Sim and counts on the device, grouping on the host (eq 3-5, 24-28).
+    top1: optional int32 device tensor [T_cal] that receives each calibration
+    token's top-1 expert."""
     import torch
     T_cal, d = x_cal.shape
     E = w_router.shape[0]
     code = BF16 if x_cal.dtype == torch.bfloat16 else F32
     sim_dev = torch.empty((E, E), dtype=torch.float32, device=x_cal.device)
     cnt_dev = torch.empty(E, dtype=torch.int64, device=x_cal.device)
+    top1_p = _dev(top1, torch.int32, T_cal)
     sim_h = np.empty((E, E), np.float32)
     cnt_h = np.empty(E, np.int64)
     g = np.empty(E, np.int32)
@@ -175,13 +183,31 @@ def ordermoe_build_similarity(x_cal, w_router, topk: int, theta: float, alpha_f:
     imp = np.empty(E, np.float64)
     _check(lib().ordermoe_build_similarity(
         _dev(x_cal, _torch_dtype(code)), T_cal, d, _dev(w_router, _torch_dtype(code), E * d), E, code,
-        topk, theta, alpha_f, _dev(sim_dev), _dev(cnt_dev), sim_h.ctypes.data_as(_P),
+        topk, theta, alpha_f, _dev(sim_dev), _dev(cnt_dev), top1_p, sim_h.ctypes.data_as(_P),
         cnt_h.ctypes.data_as(_P), g.ctypes.data_as(_P), c.ctypes.data_as(_P),
         ng.ctypes.data_as(_P), imp.ctypes.data_as(_P), _dev(workspace), workspace.numel(),
         _stream(stream)))
     K = int(ng[0])
     return dict(sim=sim_h, counts=cnt_h, group_of=g, centres=[int(v) for v in c[:K]],
                 importance=imp, sim_dev=sim_dev, counts_dev=cnt_dev)
+
+
+def ordermoe_estimate_transitions(top1: np.ndarray, E: int) -> np.ndarray:
+    """P [N-1][E][E] from the top-1 experts [N][T_cal] of the same calibration
+    tokens at consecutive layers (eq 41)."""
+    t = np.ascontiguousarray(top1, dtype=np.int32)
+    N, T_cal = t.shape
+    P = np.zeros((max(N - 1, 0), E, E), dtype=np.float64)
+    _check(lib().ordermoe_estimate_transitions(N, E, T_cal, t.ctypes.data_as(_P),
+                                               P.ctypes.data_as(_P)))
+    return P
+
+
+def ordermoe_theta_layer(l: int, N: int, theta_min: float, theta_max: float) -> float:
+    """theta_l of eq 6 (1-based l), as the float32 value the tables use."""
+    out = np.zeros(1, np.float32)
+    _check(lib().ordermoe_theta_layer(l, N, theta_min, theta_max, out.ctypes.data_as(_P)))
+    return float(out[0])
 
 
 def ordermoe_group_experts(sim: np.ndarray, counts: np.ndarray, theta: float, alpha_f: float):

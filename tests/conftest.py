@@ -8,3 +8,14 @@ if ROOT not in sys.path:
 
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU")
+
+
+import pytest  # noqa: E402
+
+
+@pytest.fixture(scope="session")
+def stream_case():
+    """The oracle's offline model of the 32-layer decode stack (built once)."""
+    import workloads as wl
+    from tests._pipeline import build_stream
+    return build_stream(wl.C5_STREAM)

@@ -1,0 +1,172 @@
+"""Decode stream through the 32-layer stack on the GPU, through the C ABI.
+
+Each layer's route/select reads the locations and accumulated losses the
+previous layer wrote on the device (Algorithm 2's loop over layers), with the
+layer's threshold (eq 6) and look-ahead tables (eq 41-42, H = 3).  The oracle
+runs the same chain from its own outputs.  A token whose router margin falls
+below 1e-4 on either side at some layer is flagged there; its decisions are
+compared up to that layer and it is left out afterwards (its later state may
+legitimately differ), and the number of such tokens is reported.  Property 2
+(the accumulated loss never exceeds the budget) is checked on every token at
+every layer.  The local expert FFN of server 0 is checked at the first and
+the last layer against the oracle's output."""
+import numpy as np
+import pytest
+
+import workloads as wl
+from oracle import layer as olayer
+
+from ._pipeline import host, stream_library_tables, stream_oracle_layer, to_device
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():  # pragma: no cover
+    pytest.skip("no GPU", allow_module_level=True)
+
+from paper_2607_17154_amd import ordermoe as om  # noqa: E402
+
+FORWARD_LAYERS = (0, 31)
+
+
+@pytest.fixture(scope="module")
+def chain(stream_case):
+    """Run the GPU chain once; keep every layer's outputs (host) and the device
+    inputs of the layers whose forward is checked."""
+    sc, cfg = stream_case, stream_case.cfg
+    theta32, phi, tabs = stream_library_tables(sc)
+    T = cfg.T
+    loc = torch.zeros(T, dtype=torch.uint8, device="cuda")
+    qh = torch.zeros(T, dtype=torch.float32, device="cuda")
+    ws = torch.empty(max(om.ordermoe_route_workspace_size(T, cfg.k, cfg.M), 1), dtype=torch.uint8,
+                     device="cuda")
+    gmax = 15
+    layers, keep = [], {}
+    for l in range(cfg.N):
+        wr = to_device(sc.W_r[l], cfg.dtype)
+        tdev = {n: torch.from_numpy(np.ascontiguousarray(v)).cuda() for n, v in tabs[l].items()
+                if n != "srvmask"}
+        tdev["srvmask"] = torch.from_numpy(tabs[l]["srvmask"].view(np.int32)).cuda()
+        L = om.make_layer(om.BF16, cfg.d, cfg.E, cfg.k, cfg.M, gmax, wr, tdev, cfg.Qbar, cfg.omega_Q,
+                          cfg.pin_local_exact, cfg.allow_sub, cfg.renorm)
+        x = to_device(sc.X[l], cfg.dtype)
+        out = om.alloc_route_out(T, cfg.k, cfg.M, "cuda")
+        om.ordermoe_route_select(L, x, T, loc, qh, out, ws)
+        torch.cuda.synchronize()
+        rec = {n: host(v) for n, v in out.items()}
+        rec["loc_in"] = host(loc)
+        layers.append(rec)
+        if l in FORWARD_LAYERS:
+            keep[l] = (x, loc.clone(), out)
+        loc, qh = out["loc_out"], out["qhat_out"]   # carried to the next layer on the device
+    return dict(layers=layers, keep=keep)
+
+
+@pytest.fixture(scope="module")
+def oracle_chain(stream_case, chain):
+    """The oracle's own chain: per layer its decisions, the locations it started
+    from, and the tokens not flagged (on either side) up to that layer."""
+    sc, cfg = stream_case, stream_case.cfg
+    loc = np.zeros(cfg.T, np.uint8)
+    qh = np.zeros(cfg.T, np.float32)
+    live = np.ones(cfg.T, bool)
+    res = []
+    for l in range(cfg.N):
+        dec = stream_oracle_layer(sc, l, loc, qh)
+        flag = (dec["margin"] < 1e-4) | (chain["layers"][l]["margin"] < 1e-4)
+        live = live & ~flag
+        res.append(dict(dec=dec, loc_in=loc, live=live, flag=flag))
+        loc, qh = dec["loc_out"], dec["qhat_out"]
+    return res
+
+
+def test_chain_decisions_match_the_oracle(stream_case, chain, oracle_chain):
+    sc, cfg = stream_case, stream_case.cfg
+    T, k = cfg.T, cfg.k
+    exhausted_layer = None
+    for l in range(cfg.N):
+        g = chain["layers"][l]
+        dec, loc, live, flag = (oracle_chain[l][n] for n in ("dec", "loc_in", "live", "flag"))
+        # the GPU's own inputs at this layer are its previous outputs
+        if l > 0:
+            np.testing.assert_array_equal(g["loc_in"], chain["layers"][l - 1]["loc_out"])
+        ok = live
+        for n in ("idx", "exec_k", "exec_m", "cls", "qhat_out", "loc_out"):
+            np.testing.assert_array_equal(g[n][ok], dec[n][ok], err_msg="layer %d %s" % (l, n))
+        # Property 2 on every token, flagged or not
+        assert np.all(g["qhat_out"] <= np.float32(cfg.Qbar)), l
+        # class counters and the dispatch list of the GPU's own decisions
+        c = g["counters"]
+        np.testing.assert_array_equal(c[:4], olayer.class_counts(g["cls"]))
+        lst, cnt, tr = olayer.dispatch(g["exec_m"], g["loc_in"], cfg.M)
+        n_remote = int(c[6])
+        np.testing.assert_array_equal(g["dispatch"][:n_remote], lst)
+        np.testing.assert_array_equal(g["dst_count"], cnt)
+        assert int(c[5]) == tr and int(c[7]) == 0
+        lst_o, _, _ = olayer.dispatch(dec["exec_m"], loc, cfg.M)
+        sel = lambda a: a[ok[a // k]]
+        np.testing.assert_array_equal(sel(g["dispatch"][:n_remote]), sel(lst_o))
+        subs = int(c[1] + c[3])
+        if exhausted_layer is None and l > 0 and subs < 0.02 * T * k:
+            exhausted_layer = l
+        print("layer %2d: LE/LS/RE/RS %s  flagged %d  compared %d  max Qhat %.4f" % (
+            l, list(c[:4]), int(flag.sum()), int(ok.sum()), float(g["qhat_out"].max())), flush=True)
+    live = oracle_chain[-1]["live"]
+    print("live tokens after %d layers: %d of %d; substitution stops at layer %s"
+          % (cfg.N, int(live.sum()), T, exhausted_layer), flush=True)
+    assert live.sum() >= T // 2
+    # the budget binds mid-stream: substitutions give way to exact execution
+    assert exhausted_layer is not None and 4 <= exhausted_layer < cfg.N - 4
+
+
+@pytest.mark.parametrize("layer", FORWARD_LAYERS)
+def test_local_forward_of_a_stream_layer(stream_case, chain, oracle_chain, layer):
+    sc, cfg = stream_case, stream_case.cfg
+    x, loc, out = chain["keep"][layer]
+    oc = oracle_chain[layer]
+    local = sc.local[layer]
+    cache = {}
+
+    def expert(j):
+        if j not in cache:
+            cache[j] = wl.stream_expert(cfg, layer, j)
+        return cache[j]
+
+    n = len(local)
+    wg = torch.empty((n, cfg.f, cfg.d), dtype=torch.bfloat16, device="cuda")
+    wu = torch.empty_like(wg)
+    wd = torch.empty((n, cfg.d, cfg.f), dtype=torch.bfloat16, device="cuda")
+    for i, j in enumerate(local):
+        a, b, c = expert(j)
+        wg[i], wu[i], wd[i] = to_device(a, "bf16"), to_device(b, "bf16"), to_device(c, "bf16")
+    wgu = torch.empty((n, 2 * cfg.f, cfg.d), dtype=torch.bfloat16, device="cuda")
+    om.ordermoe_pack_gate_up(wg, wu, wgu)
+    del wg, wu
+    ex = om.make_experts(om.BF16, cfg.d, cfg.f, cfg.E, local, wgu, wd)
+    T = cfg.T
+    y = torch.empty((T, cfg.d), dtype=torch.bfloat16, device="cuda")
+    ro = torch.empty(n + 2, dtype=torch.int32, device="cuda")
+    ws = torch.empty(max(om.ordermoe_forward_workspace_size(ex, T, cfg.k), 1), dtype=torch.uint8,
+                     device="cuda")
+    om.ordermoe_local_moe_forward(ex, x, T, cfg.k, out["w"], out["exec_k"], out["exec_m"], loc,
+                                  cfg.m0, y, ro, ws)
+    torch.cuda.synchronize()
+    rows = host(ro)
+    print("layer %d: %d local rows over %d experts" % (layer, int(rows[-1]), int(np.sum(np.diff(rows[:-1]) > 0))),
+          flush=True)
+    # the oracle's output from its own decisions, on the tokens whose decisions
+    # agree (not flagged up to this layer)
+    dec = oc["dec"]
+    tokens = np.nonzero(oc["live"])[0]
+    want = olayer.server_output(sc.X[layer], dec["w"], dec["exec_k"], dec["exec_m"], oc["loc_in"],
+                                cfg.m0, expert, [], tokens)
+    got = host(y)[tokens]
+    worst = 0.0
+    for t in range(len(tokens)):
+        ref = np.max(np.abs(want[t]))
+        if ref == 0.0:
+            assert np.all(got[t] == 0.0), t
+            continue
+        worst = max(worst, float(np.max(np.abs(got[t] - want[t])) / ref))
+    print("layer %d output max rel err %.3g over %d tokens" % (layer, worst, len(tokens)), flush=True)
+    assert worst <= 2e-2

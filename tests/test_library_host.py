@@ -185,7 +185,7 @@ def test_device_entry_points_validate_before_launch():
     rc = om.lib().ordermoe_local_moe_forward(ctypes.byref(ex), None, 0, 2, None, None, None, None,
                                              0, None, None, None, 0, None)
     assert rc == om.EINVAL and "f must be" in om.last_error()
-    rc = om.lib().ordermoe_build_similarity(None, 10, 64, None, 300, om.BF16, 2, 0.7, 0.5, *([None] * 8),
+    rc = om.lib().ordermoe_build_similarity(None, 10, 64, None, 300, om.BF16, 2, 0.7, 0.5, *([None] * 9),
                                             None, 0, None)
     assert rc == om.EINVAL
     assert om.lib().ordermoe_pack_gate_up(om.BF16, 1, 10, 64, None, None, None, None) == om.EINVAL

@@ -152,6 +152,69 @@ class BuildConfig:
 C5_BUILD = BuildConfig()
 
 
+@dataclass(frozen=True)
+class StreamConfig:
+    """A decode stream through an N-layer stack of 128-expert top-8 MoE layers
+    (Section V: tokens carry their location and accumulated loss from layer to
+    layer; Section VI-A: H = 3, theta_l from 0.9 down to 0.5, memory ratio 2.0).
+
+    The token states entering consecutive layers, and the router cluster
+    centres of consecutive layers, are first-order autoregressive chains with
+    correlation rho_x and rho_c, standing in for a trained model's residual
+    stream: a token's top-1 expert then tends to stay in the same cluster from
+    one layer to the next, which is what the transition estimate (eq 41) and
+    the look-ahead (eq 42) feed on.  The same chains give the calibration
+    tokens of every layer."""
+
+    name: str = "decode_N32_T64_d4096_E128_f1536_top8"
+    dtype: str = "bf16"
+    seed: int = 4
+    N: int = 32            # layers
+    T: int = 64            # tokens of the decode batch
+    d: int = 4096
+    E: int = 128
+    f: int = 1536
+    k: int = 8
+    n_shared: int = 0
+    clusters: int = 32
+    cluster_size: int = 4
+    sigma: float = 0.15
+    centre_std: float = 4096 ** -0.5
+    M: int = 8
+    m0: int = 0
+    memory_ratio: float = 2.0   # total server memory / one copy of every expert
+    loc_mode: str = "zero"      # every token starts on server 0 at the first layer
+    Qbar: float = 1.0
+    H: int = 3
+    theta_min: float = 0.5
+    theta_max: float = 0.9
+    T_cal: int = 2048
+    rho_x: float = 0.8
+    rho_c: float = 0.8
+    omega_T: float = 0.5
+    omega_Q: float = 0.5
+    alpha_f: float = 0.5
+    lambda1: float = 0.5
+    renorm: int = 1
+    pin_local_exact: int = 1
+    allow_sub: int = 1
+
+    @property
+    def bytes_per_el(self) -> int:
+        return 2
+
+    @property
+    def capacity(self) -> Tuple[float, ...]:
+        """C_m in expert units: memory_ratio copies of the N*E experts over M servers."""
+        return _cap(self.M, self.memory_ratio * self.N * self.E / self.M)
+
+    def with_(self, **kw) -> "StreamConfig":
+        return replace(self, **kw)
+
+
+C5_STREAM = StreamConfig()
+
+
 # ---------------------------------------------------------------- generators
 def router(cfg) -> np.ndarray:
     """W_r [E, d]: row j = centre[j // cluster_size] + sigma * centre_std * N(0, 1)."""
@@ -191,6 +254,57 @@ def shared_expert(cfg: LayerConfig, i: int):
     g = _rng(cfg.seed, _S_SHARED, 3 * i + 0).standard_normal((cfg.f, cfg.d), dtype=np.float32) * s
     u = _rng(cfg.seed, _S_SHARED, 3 * i + 1).standard_normal((cfg.f, cfg.d), dtype=np.float32) * s
     dn = _rng(cfg.seed, _S_SHARED, 3 * i + 2).standard_normal((cfg.d, cfg.f), dtype=np.float32) * s
+    return _store(g, cfg.dtype), _store(u, cfg.dtype), _store(dn, cfg.dtype)
+
+
+def _ar_chain(rng: np.random.Generator, steps: int, shape, rho: float):
+    """Yield z_0, ..., z_{steps-1}: z_0 ~ N(0,1), z_l = rho z_{l-1} + sqrt(1-rho^2) N(0,1)."""
+    a, b = np.float32(rho), np.float32(np.sqrt(1.0 - rho * rho))
+    z = rng.standard_normal(shape, dtype=np.float32)
+    yield z
+    for _ in range(1, steps):
+        z = a * z + b * rng.standard_normal(shape, dtype=np.float32)
+        yield z
+
+
+def stream_routers(cfg: StreamConfig):
+    """W_r of every layer [N][E][d]: row j = centre_l[j // cluster_size] +
+    sigma * N(0,1), times centre_std; the centres follow an AR(1) chain over the
+    layers."""
+    cent = _ar_chain(_rng(cfg.seed, _S_CENTRES), cfg.N, (cfg.clusters, cfg.d), cfg.rho_c)
+    noise = _rng(cfg.seed, _S_NOISE)
+    cl = np.arange(cfg.E) // cfg.cluster_size
+    out = np.empty((cfg.N, cfg.E, cfg.d), dtype=np.float32)
+    for l, c in enumerate(cent):
+        n = noise.standard_normal((cfg.E, cfg.d), dtype=np.float32)
+        out[l] = _store(cfg.centre_std * (c[cl] + np.float32(cfg.sigma) * n), cfg.dtype)
+    return out
+
+
+def stream_tokens(cfg: StreamConfig, T: Optional[int] = None) -> np.ndarray:
+    """X_l [N][T][d]: the states of the decode batch entering each layer
+    (an AR(1) chain per token), rounded to the storage type."""
+    T = cfg.T if T is None else T
+    out = np.empty((cfg.N, T, cfg.d), dtype=np.float32)
+    for l, z in enumerate(_ar_chain(_rng(cfg.seed, _S_X), cfg.N, (T, cfg.d), cfg.rho_x)):
+        out[l] = _store(z, cfg.dtype)
+    return out
+
+
+def stream_calibration(cfg: StreamConfig, T_cal: Optional[int] = None):
+    """Yield X_cal_l [T_cal][d] for l = 0..N-1: calibration tokens followed
+    through the stack (the same AR(1) recipe as the decode batch)."""
+    T_cal = cfg.T_cal if T_cal is None else T_cal
+    for z in _ar_chain(_rng(cfg.seed, _S_XCAL), cfg.N, (T_cal, cfg.d), cfg.rho_x):
+        yield _store(z, cfg.dtype)
+
+
+def stream_expert(cfg: StreamConfig, l: int, j: int):
+    """Weights of expert j of layer l (0-based), torch Linear layout, N(0, 0.02^2)."""
+    s = np.float32(0.02)
+    g = _rng(cfg.seed, _S_WG, l, j).standard_normal((cfg.f, cfg.d), dtype=np.float32) * s
+    u = _rng(cfg.seed, _S_WU, l, j).standard_normal((cfg.f, cfg.d), dtype=np.float32) * s
+    dn = _rng(cfg.seed, _S_WD, l, j).standard_normal((cfg.d, cfg.f), dtype=np.float32) * s
     return _store(g, cfg.dtype), _store(u, cfg.dtype), _store(dn, cfg.dtype)
 
 
