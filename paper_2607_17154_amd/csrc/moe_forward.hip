@@ -198,6 +198,7 @@ struct GemmArgs {
     void* Or;                 // mode 0: routed activations out; mode 1: row outputs [*][Nr]
     void* Os;                 // mode 0: shared activations out; mode 1: unused
     const float* row_w;       // mode 1
+    int head_grid;            // PART 1 and 2: grid of the whole-round launch
 };
 
 struct TileLoc {
@@ -264,7 +265,12 @@ __device__ inline void sched_interleave() {
 // the scalar offset, and rows past the end of a group read as zeros through
 // the buffer range check (their offset is set past the buffer).  Byte offsets
 // inside one operand fit in 31 bits (checked by the host).
-template <int BM, int BN, int MODE>
+//
+// PART selects the tiles: 0 all tiles; 1 the whole rounds of tiles, the first
+// head_grid * floor(tiles / head_grid); 2 the remaining tiles of a BM x 2BN
+// tiling, each cut into two BM x BN halves along N, so that the last, partly
+// filled round of big tiles runs as a round of half tiles on all CUs.
+template <int BM, int BN, int MODE, int PART>
 __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
     constexpr int BK = 64, LDK = BK + 8;
     constexpr int WM = BM / 2, WN = BN / 2;
@@ -283,10 +289,17 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
     const int per_xcd = gridDim.x >> 3;
     const int vid = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
     constexpr uint32_t OOR = 0x80000000u;           // offset past every buffer: reads zero
+    const int head = PART == 0 ? total : (total / p.head_grid) * p.head_grid;
+    const int ntile = PART == 2 ? 2 * (total - head) : head;
 
-    for (int tile = vid; tile < total; tile += gridDim.x) {
+    for (int tile = vid; tile < ntile; tile += gridDim.x) {
         TileLoc L;
-        if (!decode_tile<BM, BN>(p, tile, L)) break;
+        if (PART == 2) {
+            if (!decode_tile<BM, 2 * BN>(p, head + (tile >> 1), L)) break;
+            L.n0 += (tile & 1) * BN;
+        } else if (!decode_tile<BM, BN>(p, tile, L)) {
+            break;
+        }
         const bool shared = L.g >= p.n_routed;
         const int K = L.K;
         const __bf16* Bw = shared ? (const __bf16*)p.Ws
@@ -777,7 +790,7 @@ int launch_local_forward(const ForwardArgs& f, void* stream) {
         }
     if ((e = hipGetLastError()) != hipSuccess) return (int)e;
 
-    GemmArgs g;
+    GemmArgs g{};
     g.offsets = f.row_offsets; g.G = G; g.n_routed = f.n_local;
     g.X = f.x; g.row_tok = f.row_tok; g.ldx = f.d; g.row_w = f.row_w;
     g.x_bytes = (uint32_t)((size_t)f.T * f.d * (f.dtype == ORDERMOE_BF16 ? 2 : 4));
@@ -800,14 +813,24 @@ int launch_local_forward(const ForwardArgs& f, void* stream) {
     } else if (f.dtype == ORDERMOE_BF16) {
         static int lds_ok = -1;
         if (lds_ok < 0) {
-            lds_ok = set_lds(ggemm_bf16<GU_BM, GU_BN, 0>, bf16_gemm_lds<GU_BM, GU_BN>()) |
-                     set_lds(ggemm_bf16<DN_BM, DN_BN, 1>, bf16_gemm_lds<DN_BM, DN_BN>());
+            lds_ok = set_lds(ggemm_bf16<GU_BM, GU_BN, 0, 1>, bf16_gemm_lds<GU_BM, GU_BN>()) |
+                     set_lds(ggemm_bf16<GU_BM, GU_BN / 2, 0, 2>, bf16_gemm_lds<GU_BM, GU_BN / 2>()) |
+                     set_lds(ggemm_bf16<DN_BM, DN_BN, 1, 0>, bf16_gemm_lds<DN_BM, DN_BN>());
         }
         if (lds_ok) return lds_ok;
+        // whole rounds of 256 x 256 tiles, then the rest as 256 x 128 halves
+        const int grid_gu = persistent_grid(ub_gu, 1);
+        g.head_grid = grid_gu;
         {
         KernelTimer kt_("gemm_gate_up", st);
-        ggemm_bf16<GU_BM, GU_BN, 0>
-            <<<dim3(persistent_grid(ub_gu, 1)), dim3(256), bf16_gemm_lds<GU_BM, GU_BN>(), st>>>(g);
+        ggemm_bf16<GU_BM, GU_BN, 0, 1>
+            <<<dim3(grid_gu), dim3(256), bf16_gemm_lds<GU_BM, GU_BN>(), st>>>(g);
+        }
+        if ((e = hipGetLastError()) != hipSuccess) return (int)e;
+        {
+        KernelTimer kt_("gemm_gate_up_tail", st);
+        ggemm_bf16<GU_BM, GU_BN / 2, 0, 2>
+            <<<dim3(persistent_grid(2 * (int64_t)grid_gu, 1)), dim3(256), bf16_gemm_lds<GU_BM, GU_BN / 2>(), st>>>(g);
         }
         if ((e = hipGetLastError()) != hipSuccess) return (int)e;
     } else {
@@ -830,7 +853,7 @@ int launch_local_forward(const ForwardArgs& f, void* stream) {
     } else if (f.dtype == ORDERMOE_BF16) {
         {
         KernelTimer kt_("gemm_down", st);
-        ggemm_bf16<DN_BM, DN_BN, 1>
+        ggemm_bf16<DN_BM, DN_BN, 1, 0>
             <<<dim3(persistent_grid(ub_dn, 1)), dim3(256), bf16_gemm_lds<DN_BM, DN_BN>(), st>>>(g);
         }
     } else {
