@@ -1,16 +1,21 @@
-// Expert similarity model on gfx950 (eq 3-5): for chunks of calibration
-// tokens, the routing-logit tile H = W_r X_chunk^T is formed on chip and used
+// Expert similarity model on gfx950 (eq 3-5): for tiles of calibration
+// tokens, the routing-logit tile H = X_tile W_r^T is formed on chip and used
 // twice before it is dropped -- for the activation counts (top-k per token) and
-// for the Gram matrix H H^T -- so H never reaches HBM.
+// for the Gram matrix H^T H -- so H never reaches HBM.
 //
-//   sim_partial_kernel   persistent over chunks of SIM_TC tokens:
-//                          bf16: H tile by v_mfma_f32_16x16x32_bf16 (2 x 2 waves,
-//                                each 64 experts x 64 tokens), fp32 accumulate;
-//                          fp32: fp64 dot products rounded to fp32;
-//                        H tile -> LDS; per-token top-k -> block histogram;
-//                        Gram += H H^T with an 8 x 8 register tile per thread;
-//                        per-block partial Gram and counts to the workspace
-//   sim_finalize_kernel  fixed-order fp64 sum of the partials, cosine (eq 4)
+//   sim_tile_kernel      bf16, persistent over tiles of 256 tokens x 128
+//                        experts: X and W_r staged global -> registers -> LDS
+//                        (double buffered) into v_mfma_f32_32x32x16_bf16, the
+//                        calibration tokens streamed from HBM once; the fp32 H
+//                        tile then parked in the same LDS for the per-token
+//                        top-k counts (and top-1) and Gram += H^T H with an
+//                        8 x 8 register tile per thread; per-workgroup partial
+//                        Gram and counts to the workspace
+//   sim_partial_kernel   fp32 storage: chunks of 128 tokens, fp64 dot products
+//                        rounded to fp32, same partial outputs
+//   sim_reduce_kernel    fixed-order fp64 sum of the partials: 16 slices of
+//                        parts per entry, then the slices in order
+//   sim_normalise_kernel cosine (eq 4)
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -27,6 +32,234 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 constexpr int SIM_TC = 128;        // tokens per chunk
 constexpr int SIM_EMAX = 128;      // experts supported by the fused kernel
 constexpr int SIM_LDH = SIM_TC + 4;
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int ST_BM = 256;                 // tokens per tile
+constexpr int ST_BK = 64, ST_LDK = ST_BK + 8;
+constexpr int ST_LDH = SIM_EMAX + 4;       // row stride of the parked H tile (floats)
+constexpr size_t ST_LDS_KLOOP = (size_t)2 * (ST_BM + SIM_EMAX) * ST_LDK * 2;
+constexpr size_t ST_LDS_H = (size_t)ST_BM * ST_LDH * 4;
+constexpr size_t ST_LDS = ST_LDS_KLOOP > ST_LDS_H ? ST_LDS_KLOOP : ST_LDS_H;
+
+__device__ inline bf16x8 st_load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, 0);
+    return __builtin_bit_cast(bf16x8, v);
+}
+
+// Scheduling pattern of one MFMA sub-step (as in the grouped GEMM): NM MFMAs
+// with NR LDS fragment reads and NX other memory instructions between them.
+template <int Q, int NM, int NR, int NX, int XMASK>
+__device__ inline void st_interleave() {
+    if constexpr (Q < NM) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        constexpr int r = ((Q + 1) * NR + NM - 1) / NM - (Q * NR + NM - 1) / NM;
+        if constexpr (r > 0) __builtin_amdgcn_sched_group_barrier(0x100, r, 0);
+        constexpr int x = (Q + 1) * NX / NM - Q * NX / NM;
+        if constexpr (x > 0) __builtin_amdgcn_sched_group_barrier(XMASK, x, 0);
+        st_interleave<Q + 1, NM, NR, NX, XMASK>();
+    }
+}
+
+__global__ void __launch_bounds__(256, 1) sim_tile_kernel(const SimArgs a) {
+    constexpr int BM = ST_BM, BN = SIM_EMAX, BK = ST_BK, LDK = ST_LDK;
+    constexpr int WM = BM / 2, WN = BN / 2, FM = WM / 32, FN = WN / 32;   // 4 x 2 blocks per wave
+    constexpr int AV = BM * BK / 8 / 256, BV = BN * BK / 8 / 256;        // 8 and 4 loads per thread
+    extern __shared__ __attribute__((aligned(16))) char lds_raw[];
+    __shared__ int s_cnt[SIM_EMAX];
+    __bf16* sA = (__bf16*)lds_raw;                 // [2][BM][LDK]
+    __bf16* sB = sA + 2 * BM * LDK;                // [2][BN][LDK]
+    float* sH = (float*)lds_raw;                   // [BM][ST_LDH], after the K loop
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int lrow = tid >> 3, lch = (tid & 7) * 8;
+    const int E = a.E, d = a.d;
+    const int ntiles = (int)((a.T_cal + BM - 1) / BM);
+    for (int i = tid; i < SIM_EMAX; i += 256) s_cnt[i] = 0;
+    const __amdgpu_buffer_rsrc_t rb_rs =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(a.w_router), (short)0, E * d * 2, 0x00020000);
+    const uint32_t boff0 = ((uint32_t)lrow * (uint32_t)d + lch) * 2u;
+    const uint32_t bstride = 64u * (uint32_t)d;     // 32 rows, in bytes
+
+    // Gram register tile: rows ti + 16 u, columns tj + 16 v (u, v < 8)
+    const int ti = tid >> 4, tj = tid & 15;
+    float gacc[8][8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+#pragma unroll
+        for (int v = 0; v < 8; ++v) gacc[u][v] = 0.f;
+
+    // consecutive tiles on one XCD when the grid spans the 8 XCDs evenly
+    const int vid = (gridDim.x & 7) == 0 ? (blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3)
+                                         : (int)blockIdx.x;
+    for (int tile = vid; tile < ntiles; tile += gridDim.x) {
+        const int64_t t0 = (int64_t)tile * BM;
+        const int nt = (int)((a.T_cal - t0) < BM ? (a.T_cal - t0) : BM);
+        // this tile's tokens only: rows past the end read zeros through the range check
+        const __amdgpu_buffer_rsrc_t ra_rs = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<__bf16*>((const __bf16*)a.x_cal + t0 * d), (short)0, nt * d * 2, 0x00020000);
+        f32x16 acc[FM][FN];
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+        bf16x8 ra[AV], rb[BV];
+        auto gloadA = [&](int k0) {
+#pragma unroll
+            for (int v = 0; v < AV; ++v)
+                ra[v] = st_load16(ra_rs, ((uint32_t)(lrow + 32 * v) * (uint32_t)d + lch) * 2u, (uint32_t)k0 * 2u);
+        };
+        auto gloadB = [&](int k0) {
+#pragma unroll
+            for (int v = 0; v < BV; ++v) rb[v] = st_load16(rb_rs, boff0 + v * bstride, (uint32_t)k0 * 2u);
+        };
+        auto sstoreA = [&](int buf) {
+            __bf16* p = sA + buf * BM * LDK + lrow * LDK + lch;
+#pragma unroll
+            for (int v = 0; v < AV; ++v) *(bf16x8*)(p + v * 32 * LDK) = ra[v];
+        };
+        auto sstoreB = [&](int buf) {
+            __bf16* p = sB + buf * BN * LDK + lrow * LDK + lch;
+#pragma unroll
+            for (int v = 0; v < BV; ++v) *(bf16x8*)(p + v * 32 * LDK) = rb[v];
+        };
+        const int arow_off = (wm * WM + (lane & 31)) * LDK + (lane >> 5) * 8;
+        const int brow_off = (wn * WN + (lane & 31)) * LDK + (lane >> 5) * 8;
+        bf16x8 af[2][FM], bfm[2][FN];
+        auto fload = [&](int buf, int ks, int slot) {
+            const __bf16* pa = sA + buf * BM * LDK + arow_off + ks * 16;
+            const __bf16* pb = sB + buf * BN * LDK + brow_off + ks * 16;
+#pragma unroll
+            for (int i = 0; i < FM; ++i) af[slot][i] = *(const bf16x8*)(pa + i * 32 * LDK);
+#pragma unroll
+            for (int j = 0; j < FN; ++j) bfm[slot][j] = *(const bf16x8*)(pb + j * 32 * LDK);
+        };
+        auto mfmas = [&](int slot) {
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[slot][i], bfm[slot][j], acc[i][j], 0, 0, 0);
+        };
+        // K tiles of 64 as four MFMA sub-steps; the next tile's reads and LDS
+        // stores spread over them (B reads, A reads, B stores, A stores)
+        {
+            constexpr int NM = FM * FN, NR = FM + FN;
+            constexpr int VMEM_READ = 0x020, LDS_WRITE = 0x200;
+            const int KT = d / BK;
+            gloadA(0);
+            gloadB(0);
+            sstoreA(0);
+            sstoreB(0);
+            __syncthreads();
+            fload(0, 0, 0);
+            for (int kt = 0; kt < KT; ++kt) {
+                const int cb = kt & 1;
+                const int kn = (kt + 1 < KT ? kt + 1 : kt) * BK;
+                fload(cb, 1, 1);
+                gloadB(kn);
+                mfmas(0);
+                st_interleave<0, NM, NR, BV, VMEM_READ>();
+                __builtin_amdgcn_sched_barrier(0);
+                fload(cb, 2, 0);
+                gloadA(kn);
+                mfmas(1);
+                st_interleave<0, NM, NR, AV, VMEM_READ>();
+                __builtin_amdgcn_sched_barrier(0);
+                fload(cb, 3, 1);
+                sstoreB(cb ^ 1);
+                mfmas(0);
+                st_interleave<0, NM, NR, BV, LDS_WRITE>();
+                __builtin_amdgcn_sched_barrier(0);
+                sstoreA(cb ^ 1);
+                mfmas(1);
+                st_interleave<0, NM, 0, AV, LDS_WRITE>();
+                __builtin_amdgcn_sched_barrier(0);
+                __syncthreads();
+                fload(cb ^ 1, 0, 0);
+            }
+        }
+        __syncthreads();   // every wave is done with the operand buffers
+        // park H: element e of a 32x32 block is token (e/4)*8 + (lane/32)*4 + e%4,
+        // expert lane%32
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) {
+                    const int tr = wm * WM + i * 32 + (e >> 2) * 8 + (lane >> 5) * 4 + (e & 3);
+                    const int ex = wn * WN + j * 32 + (lane & 31);
+                    sH[tr * ST_LDH + ex] = acc[i][j][e];
+                }
+        __syncthreads();
+
+        // activation counts: top-k of each token's logits, ties to the lower
+        // index; 16 lanes per token, lane j holding experts j + 16 i, a 64-bit
+        // (logit, -index) key max-reduced over the lanes per rank
+        {
+            const int g16 = tid >> 4, j16 = tid & 15;
+            for (int tb = 0; tb < nt; tb += 16) {
+                const int tt = tb + g16;
+                const bool tok = tt < nt;
+                uint32_t ordv[SIM_EMAX / 16];
+#pragma unroll
+                for (int i = 0; i < SIM_EMAX / 16; ++i) {
+                    const int e = j16 + 16 * i;
+                    const uint32_t u = __float_as_uint(sH[(tok ? tt : 0) * ST_LDH + e]);
+                    ordv[i] = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+                }
+                uint32_t removed = 0;
+                for (int r = 0; r < a.k; ++r) {
+                    uint64_t best = 0;
+#pragma unroll
+                    for (int i = 0; i < SIM_EMAX / 16; ++i) {
+                        const int e = j16 + 16 * i;
+                        if (e >= E || (removed & (1u << i))) continue;
+                        const uint64_t key = ((uint64_t)ordv[i] << 32) | (uint32_t)(0xFFFFu - (uint32_t)e);
+                        best = key > best ? key : best;
+                    }
+#pragma unroll
+                    for (int off = 8; off >= 1; off >>= 1) {
+                        uint32_t lo = (uint32_t)best, hi = (uint32_t)(best >> 32);
+                        lo = __shfl_xor(lo, off, 16);
+                        hi = __shfl_xor(hi, off, 16);
+                        const uint64_t o = ((uint64_t)hi << 32) | lo;
+                        best = o > best ? o : best;
+                    }
+                    const int e = (int)(0xFFFFu - (uint32_t)(best & 0xFFFFu));
+                    if (r == 0 && j16 == 0 && tok && a.top1) a.top1[t0 + tt] = e;
+                    if ((e & 15) == j16) {
+                        removed |= 1u << (e >> 4);
+                        if (tok) atomicAdd(&s_cnt[e], 1);
+                    }
+                }
+            }
+        }
+        // Gram += H^T H over this tile's tokens (padding experts are zero columns)
+        for (int t = 0; t < nt; ++t) {
+            float hu[8], hv[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) { hu[u] = sH[t * ST_LDH + ti + 16 * u]; hv[u] = sH[t * ST_LDH + tj + 16 * u]; }
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+#pragma unroll
+                for (int v = 0; v < 8; ++v) gacc[u][v] = fmaf(hu[u], hv[v], gacc[u][v]);
+        }
+        __syncthreads();   // before the next tile's operands overwrite H
+    }
+    float* gp = a.gram_part + (int64_t)blockIdx.x * SIM_EMAX * SIM_EMAX;
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+#pragma unroll
+        for (int v = 0; v < 8; ++v) gp[(ti + 16 * u) * SIM_EMAX + tj + 16 * v] = gacc[u][v];
+    __syncthreads();
+    for (int i = tid; i < SIM_EMAX; i += 256) a.count_part[(int64_t)blockIdx.x * SIM_EMAX + i] = s_cnt[i];
+}
 
 __global__ void __launch_bounds__(256) sim_partial_kernel(const SimArgs a) {
     __shared__ float s_H[SIM_EMAX][SIM_LDH];
@@ -188,30 +421,34 @@ __global__ void __launch_bounds__(256) sim_partial_kernel(const SimArgs a) {
     for (int i = tid; i < SIM_EMAX; i += 256) a.count_part[(int64_t)blockIdx.x * SIM_EMAX + i] = s_cnt[i];
 }
 
-// Fixed-order fp64 sum of the per-block partial Gram matrices and counts;
-// one thread per (i, j) entry, consecutive threads on consecutive columns.
-__global__ void __launch_bounds__(256) sim_reduce_kernel(const SimArgs a, int nparts, double* gram) {
-    const int p = blockIdx.x * 256 + threadIdx.x;
-    if (p >= SIM_EMAX * SIM_EMAX) return;
-    const int i = p / SIM_EMAX, j = p % SIM_EMAX;
-    if (i >= a.E || j >= a.E) return;
-    // 8 interleaved partial sums (fixed order) keep 8 loads in flight
-    double s8[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+// Fixed-order fp64 sum of the per-block partial Gram matrices and counts.
+// A block of 1024 threads takes 64 consecutive entries; thread (s, c) adds the
+// parts s, s + 16, ... of entry c (independent loads, coalesced over c), then
+// the 16 slices are added in slice order.
+constexpr int RED_SLICES = 16, RED_COLS = 64;
+
+__global__ void __launch_bounds__(RED_SLICES * RED_COLS) sim_reduce_kernel(const SimArgs a, int nparts,
+                                                                           double* gram) {
+    __shared__ double s_g[RED_SLICES][RED_COLS];
+    __shared__ int64_t s_c[RED_SLICES][RED_COLS];
+    const int c = threadIdx.x % RED_COLS, sl = threadIdx.x / RED_COLS;
+    const int p = blockIdx.x * RED_COLS + c;            // entry of the 128 x 128 Gram
+    double g = 0.0;
+    int64_t n = 0;
     const float* src = a.gram_part + p;
-    int b = 0;
-    for (; b + 8 <= nparts; b += 8) {
-#pragma unroll
-        for (int q = 0; q < 8; ++q) s8[q] += (double)src[(int64_t)(b + q) * SIM_EMAX * SIM_EMAX];
-    }
-    for (int q = 0; b < nparts; ++b, ++q) s8[q] += (double)src[(int64_t)b * SIM_EMAX * SIM_EMAX];
-    double s = 0.0;
-#pragma unroll
-    for (int q = 0; q < 8; ++q) s += s8[q];
-    gram[p] = s;
-    if (i == 0) {
-        int64_t c = 0;
-        for (int b = 0; b < nparts; ++b) c += (int64_t)a.count_part[(int64_t)b * SIM_EMAX + j];
-        a.counts[j] = c;
+#pragma unroll 4
+    for (int b = sl; b < nparts; b += RED_SLICES) g += (double)src[(int64_t)b * SIM_EMAX * SIM_EMAX];
+    if (p < SIM_EMAX)
+        for (int b = sl; b < nparts; b += RED_SLICES) n += a.count_part[(int64_t)b * SIM_EMAX + p];
+    s_g[sl][c] = g;
+    s_c[sl][c] = n;
+    __syncthreads();
+    if (sl == 0) {
+        double t = 0.0;
+        int64_t m = 0;
+        for (int q = 0; q < RED_SLICES; ++q) { t += s_g[q][c]; m += s_c[q][c]; }
+        gram[p] = t;
+        if (p < a.E) a.counts[p] = m;
     }
 }
 
@@ -252,16 +489,29 @@ int similarity_max_experts() { return SIM_EMAX; }
 
 int launch_similarity(const SimArgs& a, void* stream) {
     hipStream_t st = (hipStream_t)stream;
-    {
+    int nparts = a.nchunk;
+    hipError_t e;
+    if (a.dtype == ORDERMOE_BF16) {
+        static int lds_ok = -1;
+        if (lds_ok < 0)
+            lds_ok = (int)hipFuncSetAttribute((const void*)sim_tile_kernel,
+                                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)ST_LDS);
+        if (lds_ok) return lds_ok;
+        // one workgroup per tile up to the partial slots the workspace holds
+        const int64_t ntiles = (a.T_cal + ST_BM - 1) / ST_BM;
+        nparts = (int)(ntiles < a.nchunk ? ntiles : a.nchunk);
+        KernelTimer kt_("sim_partial", st);
+        sim_tile_kernel<<<dim3(nparts), dim3(256), ST_LDS, st>>>(a);
+    } else {
         KernelTimer kt_("sim_partial", st);
         hipLaunchKernelGGL(sim_partial_kernel, dim3(a.nchunk), dim3(256), 0, st, a);
-        }
-    hipError_t e = hipGetLastError();
+    }
+    e = hipGetLastError();
     if (e != hipSuccess) return (int)e;
     {
         KernelTimer kt_("sim_reduce", st);
-        hipLaunchKernelGGL(sim_reduce_kernel, dim3(SIM_EMAX * SIM_EMAX / 256), dim3(256), 0, st, a,
-                           a.nchunk, a.gram);
+        hipLaunchKernelGGL(sim_reduce_kernel, dim3(SIM_EMAX * SIM_EMAX / RED_COLS), dim3(RED_SLICES * RED_COLS),
+                           0, st, a, nparts, a.gram);
     }
     e = hipGetLastError();
     if (e != hipSuccess) return (int)e;
