@@ -4,13 +4,13 @@
 // for the Gram matrix H^T H -- so H never reaches HBM.
 //
 //   sim_tile_kernel      bf16, persistent over tiles of 256 tokens x 128
-//                        experts: X and W_r staged global -> registers -> LDS
-//                        (double buffered) into v_mfma_f32_32x32x16_bf16, the
-//                        calibration tokens streamed from HBM once; the fp32 H
-//                        tile then parked in the same LDS for the per-token
-//                        top-k counts (and top-1) and Gram += H^T H with an
-//                        8 x 8 register tile per thread; per-workgroup partial
-//                        Gram and counts to the workspace
+//                        experts by v_mfma_f32_32x32x16_bf16: the calibration
+//                        tokens streamed from HBM once, straight into operand
+//                        registers several K steps ahead, W_r through LDS; the
+//                        fp32 H tile then parked in LDS for the per-token top-k
+//                        counts (and top-1) and Gram += H^T H with an 8 x 8
+//                        register tile per thread; per-workgroup partial Gram
+//                        and counts to the workspace
 //   sim_partial_kernel   fp32 storage: chunks of 128 tokens, fp64 dot products
 //                        rounded to fp32, same partial outputs
 //   sim_reduce_kernel    fixed-order fp64 sum of the partials: 16 slices of
@@ -36,10 +36,13 @@ constexpr int SIM_LDH = SIM_TC + 4;
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int ST_BM = 256;                 // tokens per tile
+constexpr int ST_BM = 256;                 // tokens per tile (32 per wave)
+constexpr int ST_WAVES = 8;
+constexpr int ST_THREADS = ST_WAVES * 64;
 constexpr int ST_BK = 64, ST_LDK = ST_BK + 8;
+constexpr int ST_STAGES = 4;               // K steps of reads in flight per wave
 constexpr int ST_LDH = SIM_EMAX + 4;       // row stride of the parked H tile (floats)
-constexpr size_t ST_LDS_KLOOP = (size_t)2 * (ST_BM + SIM_EMAX) * ST_LDK * 2;
+constexpr size_t ST_LDS_KLOOP = (size_t)2 * SIM_EMAX * ST_LDK * 2;
 constexpr size_t ST_LDS_H = (size_t)ST_BM * ST_LDH * 4;
 constexpr size_t ST_LDS = ST_LDS_KLOOP > ST_LDS_H ? ST_LDS_KLOOP : ST_LDS_H;
 
@@ -48,218 +51,198 @@ __device__ inline bf16x8 st_load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint
     return __builtin_bit_cast(bf16x8, v);
 }
 
-// Scheduling pattern of one MFMA sub-step (as in the grouped GEMM): NM MFMAs
-// with NR LDS fragment reads and NX other memory instructions between them.
-template <int Q, int NM, int NR, int NX, int XMASK>
-__device__ inline void st_interleave() {
-    if constexpr (Q < NM) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        constexpr int r = ((Q + 1) * NR + NM - 1) / NM - (Q * NR + NM - 1) / NM;
-        if constexpr (r > 0) __builtin_amdgcn_sched_group_barrier(0x100, r, 0);
-        constexpr int x = (Q + 1) * NX / NM - Q * NX / NM;
-        if constexpr (x > 0) __builtin_amdgcn_sched_group_barrier(XMASK, x, 0);
-        st_interleave<Q + 1, NM, NR, NX, XMASK>();
-    }
-}
-
-__global__ void __launch_bounds__(256, 1) sim_tile_kernel(const SimArgs a) {
-    constexpr int BM = ST_BM, BN = SIM_EMAX, BK = ST_BK, LDK = ST_LDK;
-    constexpr int WM = BM / 2, WN = BN / 2, FM = WM / 32, FN = WN / 32;   // 4 x 2 blocks per wave
-    constexpr int AV = BM * BK / 8 / 256, BV = BN * BK / 8 / 256;        // 8 and 4 loads per thread
+// One workgroup per tile of 256 calibration tokens; wave w owns tokens
+// 32w .. 32w+31 against all 128 experts (4 blocks of 32x32).  The tokens are
+// streamed from HBM once, straight into MFMA operand registers (lane: token
+// lane%32, K elements 8*(lane/32) .. +7 of each 16); the router rows W_r (L2
+// resident) go through a double-buffered LDS tile shared by the waves.  The
+// reads of a K step are issued ST_STAGES steps ahead.  After the K loop the
+// fp32 H tile is parked in LDS for the top-k counts and the Gram update; the
+// Gram partial of a workgroup lives in its workspace slot.
+__global__ void __launch_bounds__(ST_THREADS, 1) sim_tile_kernel(const SimArgs a) {
+    constexpr int BN = SIM_EMAX, BK = ST_BK, LDK = ST_LDK, S = ST_STAGES;
+    constexpr int FN = BN / 32;                         // per wave: 32 tokens x 128 experts
+    constexpr int BV = BN * BK / 8 / ST_THREADS;        // W loads per thread per K step
     extern __shared__ __attribute__((aligned(16))) char lds_raw[];
     __shared__ int s_cnt[SIM_EMAX];
-    __bf16* sA = (__bf16*)lds_raw;                 // [2][BM][LDK]
-    __bf16* sB = sA + 2 * BM * LDK;                // [2][BN][LDK]
-    float* sH = (float*)lds_raw;                   // [BM][ST_LDH], after the K loop
+    __bf16* sB = (__bf16*)lds_raw;                      // [2][BN][LDK]
+    float* sH = (float*)lds_raw;                        // [ST_BM][ST_LDH], after the K loop
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
-    const int lrow = tid >> 3, lch = (tid & 7) * 8;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int lrow = tid >> 3, lch = (tid & 7) * 8;     // W load slot: rows lrow + 64 v
     const int E = a.E, d = a.d;
-    const int ntiles = (int)((a.T_cal + BM - 1) / BM);
-    for (int i = tid; i < SIM_EMAX; i += 256) s_cnt[i] = 0;
+    const int KT = d / BK;
+    const int ntiles = (int)((a.T_cal + ST_BM - 1) / ST_BM);
+    for (int i = tid; i < SIM_EMAX; i += ST_THREADS) s_cnt[i] = 0;
     const __amdgpu_buffer_rsrc_t rb_rs =
         __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(a.w_router), (short)0, E * d * 2, 0x00020000);
     const uint32_t boff0 = ((uint32_t)lrow * (uint32_t)d + lch) * 2u;
-    const uint32_t bstride = 64u * (uint32_t)d;     // 32 rows, in bytes
+    const uint32_t bstride = 128u * (uint32_t)d;        // 64 rows, in bytes
+    const int brow_off = (lane & 31) * LDK + (lane >> 5) * 8;
+    constexpr uint32_t OOR = 0x80000000u;
+    const int ti = tid >> 4, tj = tid & 15;             // Gram tile: rows 4 ti .. +3, columns 8 tj .. +7
+    float* gp = a.gram_part + (int64_t)blockIdx.x * SIM_EMAX * SIM_EMAX;
+    bool first_tile = true;
 
-    // Gram register tile: rows ti + 16 u, columns tj + 16 v (u, v < 8)
-    const int ti = tid >> 4, tj = tid & 15;
-    float gacc[8][8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u)
-#pragma unroll
-        for (int v = 0; v < 8; ++v) gacc[u][v] = 0.f;
-
-    // consecutive tiles on one XCD when the grid spans the 8 XCDs evenly
     const int vid = (gridDim.x & 7) == 0 ? (blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3)
                                          : (int)blockIdx.x;
     for (int tile = vid; tile < ntiles; tile += gridDim.x) {
-        const int64_t t0 = (int64_t)tile * BM;
-        const int nt = (int)((a.T_cal - t0) < BM ? (a.T_cal - t0) : BM);
+        const int64_t t0 = (int64_t)tile * ST_BM;
+        const int nt = (int)((a.T_cal - t0) < ST_BM ? (a.T_cal - t0) : ST_BM);
         // this tile's tokens only: rows past the end read zeros through the range check
         const __amdgpu_buffer_rsrc_t ra_rs = __builtin_amdgcn_make_buffer_rsrc(
             const_cast<__bf16*>((const __bf16*)a.x_cal + t0 * d), (short)0, nt * d * 2, 0x00020000);
-        f32x16 acc[FM][FN];
+        const uint32_t aoff = ((uint32_t)(wave * 32 + (lane & 31)) * (uint32_t)d + 8u * (lane >> 5)) * 2u;
+
+        f32x16 acc[FN];
 #pragma unroll
-        for (int i = 0; i < FM; ++i)
+        for (int j = 0; j < FN; ++j)
 #pragma unroll
-            for (int j = 0; j < FN; ++j)
+            for (int e = 0; e < 16; ++e) acc[j][e] = 0.f;
+        bf16x8 ax[S][4];                                // token operands of S K steps
+        bf16x8 rb[S][BV], bfr[FN];                      // W rows of S K steps
+        auto loadA = [&](int st, int step) {
+            const uint32_t ok = step < KT ? 0u : OOR;    // past the end: zeros, never used
+            const uint32_t k0 = (uint32_t)step * BK * 2u;
 #pragma unroll
-                for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
-        bf16x8 ra[AV], rb[BV];
-        auto gloadA = [&](int k0) {
-#pragma unroll
-            for (int v = 0; v < AV; ++v)
-                ra[v] = st_load16(ra_rs, ((uint32_t)(lrow + 32 * v) * (uint32_t)d + lch) * 2u, (uint32_t)k0 * 2u);
+            for (int ks = 0; ks < 4; ++ks) ax[st][ks] = st_load16(ra_rs, aoff | ok, k0 + 32u * ks);
         };
-        auto gloadB = [&](int k0) {
+        auto loadB = [&](int st, int step) {
+            const uint32_t ok = step < KT ? 0u : OOR;
 #pragma unroll
-            for (int v = 0; v < BV; ++v) rb[v] = st_load16(rb_rs, boff0 + v * bstride, (uint32_t)k0 * 2u);
+            for (int v = 0; v < BV; ++v)
+                rb[st][v] = st_load16(rb_rs, (boff0 + v * bstride) | ok, (uint32_t)step * BK * 2u);
         };
-        auto sstoreA = [&](int buf) {
-            __bf16* p = sA + buf * BM * LDK + lrow * LDK + lch;
-#pragma unroll
-            for (int v = 0; v < AV; ++v) *(bf16x8*)(p + v * 32 * LDK) = ra[v];
-        };
-        auto sstoreB = [&](int buf) {
+        auto storeB = [&](int st, int buf) {
             __bf16* p = sB + buf * BN * LDK + lrow * LDK + lch;
 #pragma unroll
-            for (int v = 0; v < BV; ++v) *(bf16x8*)(p + v * 32 * LDK) = rb[v];
+            for (int v = 0; v < BV; ++v) *(bf16x8*)(p + v * 64 * LDK) = rb[st][v];
         };
-        const int arow_off = (wm * WM + (lane & 31)) * LDK + (lane >> 5) * 8;
-        const int brow_off = (wn * WN + (lane & 31)) * LDK + (lane >> 5) * 8;
-        bf16x8 af[2][FM], bfm[2][FN];
-        auto fload = [&](int buf, int ks, int slot) {
-            const __bf16* pa = sA + buf * BM * LDK + arow_off + ks * 16;
-            const __bf16* pb = sB + buf * BN * LDK + brow_off + ks * 16;
+        auto mma = [&](int st, int buf) {
+            const __bf16* pb = sB + buf * BN * LDK + brow_off;
 #pragma unroll
-            for (int i = 0; i < FM; ++i) af[slot][i] = *(const bf16x8*)(pa + i * 32 * LDK);
+            for (int ks = 0; ks < 4; ++ks) {
 #pragma unroll
-            for (int j = 0; j < FN; ++j) bfm[slot][j] = *(const bf16x8*)(pb + j * 32 * LDK);
-        };
-        auto mfmas = [&](int slot) {
-#pragma unroll
-            for (int i = 0; i < FM; ++i)
+                for (int j = 0; j < FN; ++j) bfr[j] = *(const bf16x8*)(pb + j * 32 * LDK + ks * 16);
 #pragma unroll
                 for (int j = 0; j < FN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[slot][i], bfm[slot][j], acc[i][j], 0, 0, 0);
+                    acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ax[st][ks], bfr[j], acc[j], 0, 0, 0);
+            }
         };
-        // K tiles of 64 as four MFMA sub-steps; the next tile's reads and LDS
-        // stores spread over them (B reads, A reads, B stores, A stores)
-        {
-            constexpr int NM = FM * FN, NR = FM + FN;
-            constexpr int VMEM_READ = 0x020, LDS_WRITE = 0x200;
-            const int KT = d / BK;
-            gloadA(0);
-            gloadB(0);
-            sstoreA(0);
-            sstoreB(0);
-            __syncthreads();
-            fload(0, 0, 0);
-            for (int kt = 0; kt < KT; ++kt) {
-                const int cb = kt & 1;
-                const int kn = (kt + 1 < KT ? kt + 1 : kt) * BK;
-                fload(cb, 1, 1);
-                gloadB(kn);
-                mfmas(0);
-                st_interleave<0, NM, NR, BV, VMEM_READ>();
+        // The reads of one K step (tokens, then W rows) form a batch issued S
+        // steps before the step is multiplied.  The memory counter retires reads
+        // in issue order, so waiting for the W rows of step kt + 1 (to put them
+        // in LDS) never waits for the S - 1 younger batches still in flight.
+        // prologue: batches 0 .. S-1, W of step 0 in LDS
+#pragma unroll
+        for (int st = 0; st < S; ++st) { loadA(st, st); loadB(st, st); }
+        storeB(0, 0);
+        __syncthreads();
+        // steady state, unrolled by S so that every register stage has a fixed name:
+        // step kt multiplies stage kt % S and LDS buffer kt & 1, refills the stage
+        // with batch kt + S, and moves W of step kt + 1 to the other buffer
+        // (KT is a multiple of S: d % 256 == 0 for this kernel)
+        for (int kt0 = 0; kt0 < KT; kt0 += S) {
+#pragma unroll
+            for (int u = 0; u < S; ++u) {
+                const int kt = kt0 + u;
+                mma(u, kt & 1);
                 __builtin_amdgcn_sched_barrier(0);
-                fload(cb, 2, 0);
-                gloadA(kn);
-                mfmas(1);
-                st_interleave<0, NM, NR, AV, VMEM_READ>();
+                loadA(u, kt + S);
+                loadB(u, kt + S);
                 __builtin_amdgcn_sched_barrier(0);
-                fload(cb, 3, 1);
-                sstoreB(cb ^ 1);
-                mfmas(0);
-                st_interleave<0, NM, NR, BV, LDS_WRITE>();
-                __builtin_amdgcn_sched_barrier(0);
-                sstoreA(cb ^ 1);
-                mfmas(1);
-                st_interleave<0, NM, 0, AV, LDS_WRITE>();
-                __builtin_amdgcn_sched_barrier(0);
+                storeB((u + 1) % S, (kt + 1) & 1);
                 __syncthreads();
-                fload(cb ^ 1, 0, 0);
             }
         }
-        __syncthreads();   // every wave is done with the operand buffers
+        __syncthreads();   // every wave is done with the W buffers
         // park H: element e of a 32x32 block is token (e/4)*8 + (lane/32)*4 + e%4,
         // expert lane%32
 #pragma unroll
-        for (int i = 0; i < FM; ++i)
+        for (int j = 0; j < FN; ++j)
 #pragma unroll
-            for (int j = 0; j < FN; ++j)
-#pragma unroll
-                for (int e = 0; e < 16; ++e) {
-                    const int tr = wm * WM + i * 32 + (e >> 2) * 8 + (lane >> 5) * 4 + (e & 3);
-                    const int ex = wn * WN + j * 32 + (lane & 31);
-                    sH[tr * ST_LDH + ex] = acc[i][j][e];
-                }
+            for (int e = 0; e < 16; ++e) {
+                const int tr = wave * 32 + (e >> 2) * 8 + (lane >> 5) * 4 + (e & 3);
+                sH[tr * ST_LDH + j * 32 + (lane & 31)] = acc[j][e];
+            }
         __syncthreads();
 
         // activation counts: top-k of each token's logits, ties to the lower
-        // index; 16 lanes per token, lane j holding experts j + 16 i, a 64-bit
-        // (logit, -index) key max-reduced over the lanes per rank
-        {
-            const int g16 = tid >> 4, j16 = tid & 15;
-            for (int tb = 0; tb < nt; tb += 16) {
-                const int tt = tb + g16;
-                const bool tok = tt < nt;
-                uint32_t ordv[SIM_EMAX / 16];
+        // index.  One thread per token scans the logits in expert order and keeps
+        // a sorted top-k list in registers, branch-free: a logit's place is the
+        // number of kept logits >= it (so equal logits keep their index order),
+        // the entries from that place on move down one, and a place of k or more
+        // leaves the list unchanged.
+        for (int tt = tid; tt < nt; tt += ST_THREADS) {
+            constexpr int MK = ORDERMOE_MAX_TOPK;
+            const int k = a.k;
+            float tv[MK];
+            int te[MK];
 #pragma unroll
-                for (int i = 0; i < SIM_EMAX / 16; ++i) {
-                    const int e = j16 + 16 * i;
-                    const uint32_t u = __float_as_uint(sH[(tok ? tt : 0) * ST_LDH + e]);
-                    ordv[i] = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-                }
-                uint32_t removed = 0;
-                for (int r = 0; r < a.k; ++r) {
-                    uint64_t best = 0;
+            for (int r = 0; r < MK; ++r) { tv[r] = -__builtin_inff(); te[r] = -1; }
+            const float* row = sH + tt * ST_LDH;
+            for (int e4 = 0; e4 < E; e4 += 4) {
+                const f32x4 v4 = *(const f32x4*)(row + e4);
 #pragma unroll
-                    for (int i = 0; i < SIM_EMAX / 16; ++i) {
-                        const int e = j16 + 16 * i;
-                        if (e >= E || (removed & (1u << i))) continue;
-                        const uint64_t key = ((uint64_t)ordv[i] << 32) | (uint32_t)(0xFFFFu - (uint32_t)e);
-                        best = key > best ? key : best;
-                    }
+                for (int q = 0; q < 4; ++q) {
+                    const int e = e4 + q;
+                    const float v = v4[q];
+                    int pos = 0;
 #pragma unroll
-                    for (int off = 8; off >= 1; off >>= 1) {
-                        uint32_t lo = (uint32_t)best, hi = (uint32_t)(best >> 32);
-                        lo = __shfl_xor(lo, off, 16);
-                        hi = __shfl_xor(hi, off, 16);
-                        const uint64_t o = ((uint64_t)hi << 32) | lo;
-                        best = o > best ? o : best;
-                    }
-                    const int e = (int)(0xFFFFu - (uint32_t)(best & 0xFFFFu));
-                    if (r == 0 && j16 == 0 && tok && a.top1) a.top1[t0 + tt] = e;
-                    if ((e & 15) == j16) {
-                        removed |= 1u << (e >> 4);
-                        if (tok) atomicAdd(&s_cnt[e], 1);
+                    for (int r = 0; r < MK; ++r) pos += (r < k && te[r] >= 0 && tv[r] >= v) ? 1 : 0;
+                    if (e >= E) pos = MK;             // padding column: no change
+#pragma unroll
+                    for (int r = MK - 1; r >= 0; --r) {
+                        const float below_v = r > 0 ? tv[r - 1] : v;
+                        const int below_e = r > 0 ? te[r - 1] : e;
+                        tv[r] = r < pos ? tv[r] : (r == pos ? v : below_v);
+                        te[r] = r < pos ? te[r] : (r == pos ? e : below_e);
                     }
                 }
             }
+            if (a.top1) a.top1[t0 + tt] = te[0];
+#pragma unroll
+            for (int r = 0; r < MK; ++r)
+                if (r < k && te[r] >= 0) atomicAdd(&s_cnt[te[r]], 1);
         }
-        // Gram += H^T H over this tile's tokens (padding experts are zero columns)
-        for (int t = 0; t < nt; ++t) {
-            float hu[8], hv[8];
+        // Gram += H^T H over this tile's tokens (padding experts are zero
+        // columns), accumulated in the workgroup's workspace slot
+        {
+            float gacc[4][8];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) { hu[u] = sH[t * ST_LDH + ti + 16 * u]; hv[u] = sH[t * ST_LDH + tj + 16 * u]; }
+            for (int u = 0; u < 4; ++u)
 #pragma unroll
-            for (int u = 0; u < 8; ++u)
+                for (int v = 0; v < 8; ++v)
+                    gacc[u][v] = first_tile ? 0.f : gp[(4 * ti + u) * SIM_EMAX + 8 * tj + v];
+#pragma unroll 4
+            for (int t = 0; t < nt; ++t) {
+                const float* hr = sH + t * ST_LDH;
+                const f32x4 hu = *(const f32x4*)(hr + 4 * ti);
+                const f32x4 hv0 = *(const f32x4*)(hr + 8 * tj);
+                const f32x4 hv1 = *(const f32x4*)(hr + 8 * tj + 4);
 #pragma unroll
-                for (int v = 0; v < 8; ++v) gacc[u][v] = fmaf(hu[u], hv[v], gacc[u][v]);
+                for (int u = 0; u < 4; ++u)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) {
+                        gacc[u][v] = fmaf(hu[u], hv0[v], gacc[u][v]);
+                        gacc[u][v + 4] = fmaf(hu[u], hv1[v], gacc[u][v + 4]);
+                    }
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+#pragma unroll
+                for (int v = 0; v < 8; ++v) gp[(4 * ti + u) * SIM_EMAX + 8 * tj + v] = gacc[u][v];
         }
-        __syncthreads();   // before the next tile's operands overwrite H
+        first_tile = false;
+        __syncthreads();   // before the next tile's W overwrites H
     }
-    float* gp = a.gram_part + (int64_t)blockIdx.x * SIM_EMAX * SIM_EMAX;
-#pragma unroll
-    for (int u = 0; u < 8; ++u)
-#pragma unroll
-        for (int v = 0; v < 8; ++v) gp[(ti + 16 * u) * SIM_EMAX + tj + 16 * v] = gacc[u][v];
+    if (first_tile)        // no tile for this workgroup: an empty partial
+        for (int p = tid; p < SIM_EMAX * SIM_EMAX; p += ST_THREADS) gp[p] = 0.f;
     __syncthreads();
-    for (int i = tid; i < SIM_EMAX; i += 256) a.count_part[(int64_t)blockIdx.x * SIM_EMAX + i] = s_cnt[i];
+    for (int i = tid; i < SIM_EMAX; i += ST_THREADS) a.count_part[(int64_t)blockIdx.x * SIM_EMAX + i] = s_cnt[i];
 }
+
 
 __global__ void __launch_bounds__(256) sim_partial_kernel(const SimArgs a) {
     __shared__ float s_H[SIM_EMAX][SIM_LDH];
@@ -491,7 +474,7 @@ int launch_similarity(const SimArgs& a, void* stream) {
     hipStream_t st = (hipStream_t)stream;
     int nparts = a.nchunk;
     hipError_t e;
-    if (a.dtype == ORDERMOE_BF16) {
+    if (a.dtype == ORDERMOE_BF16 && a.d % (ST_BK * ST_STAGES) == 0) {
         static int lds_ok = -1;
         if (lds_ok < 0)
             lds_ok = (int)hipFuncSetAttribute((const void*)sim_tile_kernel,
@@ -501,7 +484,7 @@ int launch_similarity(const SimArgs& a, void* stream) {
         const int64_t ntiles = (a.T_cal + ST_BM - 1) / ST_BM;
         nparts = (int)(ntiles < a.nchunk ? ntiles : a.nchunk);
         KernelTimer kt_("sim_partial", st);
-        sim_tile_kernel<<<dim3(nparts), dim3(256), ST_LDS, st>>>(a);
+        sim_tile_kernel<<<dim3(nparts), dim3(ST_THREADS), ST_LDS, st>>>(a);
     } else {
         KernelTimer kt_("sim_partial", st);
         hipLaunchKernelGGL(sim_partial_kernel, dim3(a.nchunk), dim3(256), 0, st, a);
