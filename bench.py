@@ -217,8 +217,9 @@ def _decode_stream(torch, om, steps: int = 10, warmup: int = 2):
     The offline model is built by the library (similarity on the device,
     transitions, deployment, look-ahead and tables on the host).  Expert
     weights of server 0 (32 per layer, 38.7 GB in all) are drawn on the device,
-    N(0, 0.02^2) in bf16, and stay resident.  Reports device time per layer and
-    the HBM fraction of the weights the layer has to stream."""
+    N(0, 0.02^2) in bf16, and stay resident.  The 32-layer step is timed as a
+    HIP graph replay (also with eager launches); reports time per layer and the
+    HBM fraction of the weights the layer has to stream."""
     import workloads as wl
     cfg = wl.C5_STREAM
     dev = "cuda"
@@ -301,6 +302,25 @@ def _decode_stream(torch, om, steps: int = 10, warmup: int = 2):
     e1.record()
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1)
+    # the same step captured once in a HIP graph and replayed (no launch gaps)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    graph.replay()
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(steps):
+        graph.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    ms_graph = e0.elapsed_time(e1)
+    del graph
     # per-kernel averages from a separate pass (the events add a little time per launch)
     om.ordermoe_timing_read(reset=True)
     om.ordermoe_timing_enable(True)
@@ -318,16 +338,18 @@ def _decode_stream(torch, om, steps: int = 10, warmup: int = 2):
         cls += Ld["out"]["counters"].cpu().numpy()[:4].astype(np.int64)
     w_bytes = expert_bytes * float(np.sum(active))
     other = N * (E * cfg.d * 2 + 2 * T * cfg.d * 2)        # routers, x in, y out
-    us_layer = ms / steps / N * 1e3
+    us_layer = ms_graph / steps / N * 1e3
+    us_layer_eager = ms / steps / N * 1e3
     gemm_us = sum(kt[n][0] / kt[n][1] for n in ("gemm_gate_up", "gemm_gate_up_tail", "gemm_down")
                   if n in kt) * 1e3
     return {"workload": cfg.name, "layers": N, "tokens": T, "server": cfg.m0,
-            "us_per_layer": us_layer, "ms_per_token_step": ms / steps,
+            "us_per_layer": us_layer, "us_per_layer_eager_launches": us_layer_eager,
+            "ms_per_token_step": ms_graph / steps,
             "local_rows_per_layer": float(np.mean(rows)),
             "active_local_experts_per_layer": float(np.mean(active)),
             "classes_LE_LS_RE_RS": [int(v) for v in cls],
             "weight_bytes_per_layer": w_bytes / N,
-            "hbm_frac_layer": (w_bytes + other) / (ms / steps / 1e3) / 1e9 / PEAK_HBM_GBS,
+            "hbm_frac_layer": (w_bytes + other) / (ms_graph / steps / 1e3) / 1e9 / PEAK_HBM_GBS,
             "hbm_frac_ffn_gemms": (w_bytes / N) / (gemm_us * 1e-6) / 1e9 / PEAK_HBM_GBS,
             "kernels_avg_us": {n: v[0] / v[1] * 1e3 for n, v in sorted(kt.items())}}
 

@@ -108,7 +108,9 @@ static size_t route_ws(int64_t T, int32_t k, int32_t M, Carver& c, RouteArgs* a)
     int32_t* bd = c.take<int32_t>((size_t)std::max(nblk, 1) * M);
     int64_t* bc = c.take<int64_t>((size_t)std::max(nblk, 1) * 8);
     int32_t* db = c.take<int32_t>((size_t)std::max(nblk, 1) * M);
-    if (a) { a->blk_dst = bd; a->blk_cnt = bc; a->dst_base = db; a->nblk = nblk; }
+    // small batches split the router over K slices: room for their partial logits
+    float* lp = c.take<float>(route_split_buffer_floats(T));
+    if (a) { a->blk_dst = bd; a->blk_cnt = bc; a->dst_base = db; a->logit_part = lp; a->nblk = nblk; }
     return c.size();
 }
 

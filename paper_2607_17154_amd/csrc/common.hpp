@@ -65,12 +65,15 @@ struct RouteArgs {
     // workspace
     int32_t* blk_dst;      // [nblk][M] remote slots per destination per block
     int64_t* blk_cnt;      // [nblk][8] per-block counters
-    int32_t* dst_base;     // [nblk][M] exclusive prefix (written by scan)
+    int32_t* dst_base;     // [nblk][M] first position of each block inside the destination segment
+    float* logit_part;     // [ksplit][T][Epad] router partial logits of small batches
     int nblk;
     int S_in_lds;          // set by the launcher: stage the cost table in LDS
+    int ksplit;            // set by the launcher: K slices of the split router (0: fused)
 };
 int launch_route_select(const RouteArgs& a, void* stream);
 int route_tokens_per_block();
+size_t route_split_buffer_floats(int64_t T);
 size_t route_smem_bytes(int E, int gmax, int M, bool S_in_lds);
 
 struct ForwardArgs {
@@ -91,7 +94,7 @@ struct ForwardArgs {
     int32_t* row_offsets;
     // workspace
     int32_t* blk_rows;     // [nblk][G] rows per group per block (G = n_local + has_shared)
-    int32_t* blk_base;     // [nblk][G] first row of each group's block segment
+    int32_t* blk_base;     // [nblk][G] first row of each block inside its group
     int32_t* row_tok;      // [rmax] token of each row
     float* row_w;          // [rmax] merged gate weight of each row
     int32_t* tok_rows;     // [T][k + 1] rows of each token, -1 padded

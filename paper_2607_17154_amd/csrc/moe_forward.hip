@@ -44,7 +44,7 @@ struct RowsArgs {
     const uint8_t* loc_in;
     int32_t lidx[ORDERMOE_MAX_EXPERTS];   // expert -> local slot (kernel argument)
     int32_t* blk_rows;        // [nblk][G]
-    int32_t* blk_base;        // [nblk][G]
+    int32_t* blk_base;        // [nblk][G] first row of each block inside its group
     int32_t* row_offsets;     // [n_local + 2]
     int32_t* row_tok;
     float* row_w;
@@ -57,22 +57,52 @@ struct RowsArgs {
 };
 
 // rows of one token: group ids (local slot, or n_local for the shared group)
-// and merged gate weights, in slot order of first occurrence
+// and merged gate weights, in slot order of first occurrence.  The token's
+// slots are read up front (independent loads); the arrays are indexed only by
+// unrolled constants so that they stay in registers.
 __device__ inline int token_rows(const RowsArgs& a, const int32_t* s_lidx, int64_t t, int* grp,
                                  float* wsum) {
-    int n = 0;
-    for (int s = 0; s < a.k; ++s) {
-        const int64_t o = t * a.k + s;
-        if (a.exec_m[o] != a.server) continue;
-        const int e = a.exec_k[o];
-        const int ls = (e >= 0 && e < a.E) ? s_lidx[e] : -1;
-        if (ls < 0) continue;
-        int i = 0;
-        while (i < n && grp[i] != ls) ++i;
-        if (i == n) { grp[n] = ls; wsum[n] = a.w[o]; ++n; }
-        else wsum[i] = wsum[i] + a.w[o];
+    int m[ORDERMOE_MAX_TOPK], ek[ORDERMOE_MAX_TOPK];
+    float wv[ORDERMOE_MAX_TOPK];
+#pragma unroll
+    for (int s = 0; s < ORDERMOE_MAX_TOPK; ++s) {
+        m[s] = -1;
+        ek[s] = -1;
+        wv[s] = 0.f;
+        if (s < a.k) {
+            const int64_t o = t * a.k + s;
+            m[s] = a.exec_m[o];
+            ek[s] = a.exec_k[o];
+            wv[s] = a.w[o];
+        }
     }
-    if (a.has_shared && a.loc_in[t] == a.server) { grp[n] = a.n_local; wsum[n] = 1.0f; ++n; }
+    const int loc = a.has_shared ? (int)a.loc_in[t] : -1;
+#pragma unroll
+    for (int q = 0; q < MAXR; ++q) { grp[q] = -1; wsum[q] = 0.f; }
+    int n = 0;
+#pragma unroll
+    for (int s = 0; s < ORDERMOE_MAX_TOPK; ++s) {
+        const int e = ek[s];
+        const int ls = (m[s] == a.server && e >= 0 && e < a.E) ? s_lidx[e] : -1;
+        if (ls >= 0) {
+            bool found = false;
+#pragma unroll
+            for (int q = 0; q < MAXR; ++q)
+                if (grp[q] == ls) { wsum[q] = wsum[q] + wv[s]; found = true; }
+            if (!found) {
+#pragma unroll
+                for (int q = 0; q < MAXR; ++q)
+                    if (q == n) { grp[q] = ls; wsum[q] = wv[s]; }
+                ++n;
+            }
+        }
+    }
+    if (loc == a.server) {
+#pragma unroll
+        for (int q = 0; q < MAXR; ++q)
+            if (q == n) { grp[q] = a.n_local; wsum[q] = 1.0f; }
+        ++n;
+    }
     return n;
 }
 
@@ -88,96 +118,127 @@ __global__ void __launch_bounds__(FT_TB) rows_count_kernel(const RowsArgs a) {
         int grp[MAXR];
         float ws[MAXR];
         const int n = token_rows(a, s_lidx, t, grp, ws);
-        for (int i = 0; i < n; ++i) atomicAdd(&s_h[grp[i]], 1);
+#pragma unroll
+        for (int q = 0; q < MAXR; ++q)
+            if (q < n) atomicAdd(&s_h[grp[q]], 1);
     }
     __syncthreads();
     for (int i = threadIdx.x; i < G; i += FT_TB) a.blk_rows[(int64_t)blockIdx.x * G + i] = s_h[i];
 }
 
 constexpr int SCAN_THREADS = 1024;
+constexpr int SCAN_WAVES = SCAN_THREADS / 64;
 
+// One block.  Wave w scans groups w, w + 16, ... over the token blocks on its
+// own (64 blocks per step, a wave-level inclusive scan plus a carry), so the
+// groups proceed in parallel without block-wide barriers; then wave 0 lays
+// out the group offsets and the tile counts of the two GEMMs.
 __global__ void __launch_bounds__(SCAN_THREADS) rows_scan_kernel(const RowsArgs a) {
-    __shared__ int32_t s_scan[SCAN_THREADS / 64];
     __shared__ int32_t s_tot[MAXG];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int G = a.n_local + a.has_shared;
-    int32_t start = 0;
-    for (int g = 0; g < G; ++g) {
-        int32_t carry = start;
-        for (int b0 = 0; b0 < a.nblk; b0 += SCAN_THREADS) {
-            const int b = b0 + tid;
+    for (int g = wave; g < G; g += SCAN_WAVES) {
+        int32_t carry = 0;
+        for (int b0 = 0; b0 < a.nblk; b0 += 64) {
+            const int b = b0 + lane;
             const int32_t v = b < a.nblk ? a.blk_rows[(int64_t)b * G + g] : 0;
             int32_t inc = v;
             for (int off = 1; off < 64; off <<= 1) {
-                int32_t o = __shfl_up(inc, off);
+                const int32_t o = __shfl_up(inc, off);
                 if (lane >= off) inc += o;
             }
-            if (lane == 63) s_scan[wave] = inc;
-            __syncthreads();
-            int32_t wbase = 0, ctot = 0;
-            for (int w = 0; w < SCAN_THREADS / 64; ++w) {
-                if (w < wave) wbase += s_scan[w];
-                ctot += s_scan[w];
-            }
-            if (b < a.nblk) a.blk_base[(int64_t)b * G + g] = carry + wbase + inc - v;
-            carry += ctot;
-            __syncthreads();
+            if (b < a.nblk) a.blk_base[(int64_t)b * G + g] = carry + inc - v;   // within-group offset
+            carry += __shfl(inc, 63);
         }
-        if (tid == 0) s_tot[g] = carry - start;
-        start = carry;
+        if (lane == 0) s_tot[g] = carry;
     }
     __syncthreads();
-    if (tid == 0) {
-        int32_t off = 0;
+    // group offsets (exclusive scan of the totals) and tile counts, wave 0
+    if (wave == 0) {
+        int32_t base = 0;
         int64_t tiles_gu = 0, tiles_dn = 0;
-        for (int g = 0; g <= a.n_local; ++g) {
-            a.row_offsets[g] = off;
-            const int32_t R = (g < G) ? s_tot[g] : 0;
-            const bool sh = g == a.n_local;
-            if (g < G) {
-                tiles_gu += (int64_t)((R + a.bm_gu - 1) / a.bm_gu) * ((sh ? a.n_gu_s : a.n_gu_r) / a.bn_gu);
-                tiles_dn += (int64_t)((R + a.bm_dn - 1) / a.bm_dn) * (a.n_dn / a.bn_dn);
+        for (int g0 = 0; g0 <= a.n_local; g0 += 64) {
+            const int g = g0 + lane;
+            const int32_t R = g < G ? s_tot[g] : 0;
+            int32_t inc = R;
+            for (int off = 1; off < 64; off <<= 1) {
+                const int32_t o = __shfl_up(inc, off);
+                if (lane >= off) inc += o;
             }
-            off += R;
+            if (g <= a.n_local) a.row_offsets[g] = base + inc - R;
+            int64_t tg = 0, td = 0;
+            if (g < G) {
+                const bool sh = g == a.n_local;
+                tg = (int64_t)((R + a.bm_gu - 1) / a.bm_gu) * ((sh ? a.n_gu_s : a.n_gu_r) / a.bn_gu);
+                td = (int64_t)((R + a.bm_dn - 1) / a.bm_dn) * (a.n_dn / a.bn_dn);
+            }
+            for (int off = 32; off >= 1; off >>= 1) {
+                tg += __shfl_xor(tg, off);
+                td += __shfl_xor(td, off);
+            }
+            tiles_gu += tg;
+            tiles_dn += td;
+            base += __shfl(inc, 63);
         }
-        a.row_offsets[a.n_local + 1] = off;
-        a.tile_info[0] = (int32_t)tiles_gu;
-        a.tile_info[1] = (int32_t)tiles_dn;
-        a.tile_info[2] = off;
-        a.tile_info[3] = 0;
+        if (lane == 0) {
+            a.row_offsets[a.n_local + 1] = base;
+            a.tile_info[0] = (int32_t)tiles_gu;
+            a.tile_info[1] = (int32_t)tiles_dn;
+            a.tile_info[2] = base;
+            a.tile_info[3] = 0;
+        }
     }
 }
 
 __global__ void __launch_bounds__(FT_TB) rows_scatter_kernel(const RowsArgs a) {
     __shared__ int32_t s_lidx[ORDERMOE_MAX_EXPERTS];
     __shared__ int32_t s_wcnt[FT_TB / 64][MAXG];
+    __shared__ int32_t s_first[MAXG];        // first row of this block in each group
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int G = a.n_local + a.has_shared;
     for (int i = tid; i < a.E; i += FT_TB) s_lidx[i] = a.lidx[i];
+    for (int g = tid; g < G; g += FT_TB) s_first[g] = a.row_offsets[g] + a.blk_base[(int64_t)blockIdx.x * G + g];
     __syncthreads();
     const int64_t t = (int64_t)blockIdx.x * FT_TB + tid;
     int grp[MAXR], rank[MAXR];
     float ws[MAXR];
-    const int n = t < a.T ? token_rows(a, s_lidx, t, grp, ws) : 0;
+    int n = 0;
+    if (t < a.T) {
+        n = token_rows(a, s_lidx, t, grp, ws);
+    } else {
+#pragma unroll
+        for (int q = 0; q < MAXR; ++q) { grp[q] = -1; ws[q] = 0.f; }
+    }
+#pragma unroll
+    for (int q = 0; q < MAXR; ++q) rank[q] = 0;
     for (int g = 0; g < G; ++g) {
         int has = -1;
-        for (int i = 0; i < n; ++i) if (grp[i] == g) has = i;
+#pragma unroll
+        for (int q = 0; q < MAXR; ++q)
+            if (q < n && grp[q] == g) has = q;
         const uint64_t bal = __ballot(has >= 0);
         if (lane == 0) s_wcnt[wave][g] = __popcll(bal);
-        if (has >= 0) rank[has] = __popcll(bal & ((1ull << lane) - 1ull));
+        const int r = __popcll(bal & ((1ull << lane) - 1ull));
+#pragma unroll
+        for (int q = 0; q < MAXR; ++q)
+            if (q == has) rank[q] = r;
     }
     __syncthreads();
     if (t < a.T) {
         const int stride = a.k + 1;
-        for (int i = 0; i < n; ++i) {
-            const int g = grp[i];
-            int32_t pos = a.blk_base[(int64_t)blockIdx.x * G + g] + rank[i];
-            for (int w = 0; w < wave; ++w) pos += s_wcnt[w][g];
-            a.row_tok[pos] = (int32_t)t;
-            a.row_w[pos] = ws[i];
-            a.tok_rows[t * stride + i] = pos;
+#pragma unroll
+        for (int q = 0; q < MAXR; ++q) {
+            if (q < n) {
+                const int g = grp[q];
+                int32_t pos = s_first[g] + rank[q];
+                for (int w = 0; w < wave; ++w) pos += s_wcnt[w][g];
+                a.row_tok[pos] = (int32_t)t;
+                a.row_w[pos] = ws[q];
+                a.tok_rows[t * stride + q] = pos;
+            } else if (q < stride) {
+                a.tok_rows[t * stride + q] = -1;
+            }
         }
-        for (int i = n; i < stride; ++i) a.tok_rows[t * stride + i] = -1;
     }
 }
 

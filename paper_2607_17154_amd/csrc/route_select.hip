@@ -14,7 +14,8 @@
 //     gives (m*, k*); the budget is updated as eq (44);
 //   * per-block counters and per-destination remote-slot counts.
 // Kernel 2 (dispatch_scan_kernel), one block: exclusive scans of the
-//   per-block destination counts, totals of the counters.
+//   per-block destination counts (one wave per destination), totals of the
+//   counters.
 // Kernel 3 (dispatch_scatter_kernel), one block per RT_TB tokens: stable
 //   placement of the block's remote slots into the (destination, token, slot)
 //   ordered dispatch list.
@@ -104,6 +105,65 @@ __device__ inline void router_k_loop(const RouteArgs& a, int wave, int lane, int
     }
 }
 
+// global -> LDS copy of n 32-bit words by the block, 8 reads in flight per thread
+__device__ inline void stage_copy(int32_t* dst, const int32_t* src, int n, int tid) {
+    for (int i0 = 0; i0 < n; i0 += 8 * RT_THREADS) {
+        int32_t v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int i = i0 + u * RT_THREADS + tid;
+            v[u] = i < n ? src[i] : 0;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int i = i0 + u * RT_THREADS + tid;
+            if (i < n) dst[i] = v[u];
+        }
+    }
+}
+
+// Small batches (at most RT_SPLIT_MAX_T tokens): the router GEMM alone on many
+// waves.  Wave (token block, expert block, K slice) forms the 16 x 16 partial
+// logits of its K slice with v_mfma_f32_16x16x32_bf16, its loads issued 16
+// steps at a time; route_select_kernel adds the slices in slice order.
+constexpr int64_t RT_SPLIT_MAX_T = 1024;
+constexpr int RT_SPLIT_MAX_K = 16;
+
+__global__ void __launch_bounds__(64) router_split_kernel(const RouteArgs a) {
+    const __bf16* X = (const __bf16*)a.x;
+    const __bf16* W = (const __bf16*)a.w_router;
+    const int lane = threadIdx.x;
+    const int r16 = lane & 15, kg = (lane >> 4) * 8;
+    const int d = a.d, E = a.E;
+    const int Epad = (E + 15) & ~15;
+    const int64_t tok = (int64_t)blockIdx.x * 16 + r16;
+    const int e = blockIdx.y * 16 + r16;
+    const bool tok_ok = tok < a.T, e_ok = e < E;
+    const int kc = d / a.ksplit;                          // a multiple of 32
+    const __bf16* xrow = X + (tok_ok ? tok : 0) * (int64_t)d + blockIdx.z * kc + kg;
+    const __bf16* wrow = W + (int64_t)(e_ok ? e : 0) * d + blockIdx.z * kc + kg;
+    const bf16x8 zero8 = {};
+    const int nsteps = kc / 32;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int s0 = 0; s0 < nsteps; s0 += 16) {
+        bf16x8 xv[16], wv[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+            const bool in = s0 + u < nsteps;
+            xv[u] = tok_ok && in ? *(const bf16x8*)(xrow + (s0 + u) * 32) : zero8;
+            wv[u] = e_ok && in ? *(const bf16x8*)(wrow + (s0 + u) * 32) : zero8;
+        }
+#pragma unroll
+        for (int u = 0; u < 16; ++u) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xv[u], wv[u], acc, 0, 0, 0);
+    }
+    // acc[i]: token (lane/16)*4 + i of the block, expert lane%16 of the block
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int64_t t = (int64_t)blockIdx.x * 16 + (lane >> 4) * 4 + i;
+        if (t < a.T) a.logit_part[((int64_t)blockIdx.z * a.T + t) * Epad + blockIdx.y * 16 + r16] = acc[i];
+    }
+}
+
 template <int NBT>
 __global__ void __launch_bounds__(RT_THREADS)
 route_select_kernel(const RouteArgs a) {
@@ -125,12 +185,14 @@ route_select_kernel(const RouteArgs a) {
     float* s_S = (float*)(s_cnt + 8 + M);                          // [M][M][E] if a.S_in_lds
     const float* Stab = a.S_in_lds ? s_S : a.S;
 
-    // stage the candidate tables (small) and clear the block counters
-    for (int i = tid; i < E * a.gmax; i += RT_THREADS) { s_t1k[i] = a.t1_k[i]; s_t1q[i] = a.t1_q[i]; }
-    for (int i = tid; i < E; i += RT_THREADS) { s_t1n[i] = a.t1_n[i]; s_mask[i] = a.srvmask[i]; }
+    // stage the candidate tables (small) and clear the block counters; the
+    // copies issue several reads per thread before their LDS stores
+    stage_copy(s_t1k, a.t1_k, E * a.gmax, tid);
+    stage_copy((int32_t*)s_t1q, (const int32_t*)a.t1_q, E * a.gmax, tid);
+    stage_copy(s_t1n, a.t1_n, E, tid);
+    stage_copy((int32_t*)s_mask, (const int32_t*)a.srvmask, E, tid);
     for (int i = tid; i < 8 + M; i += RT_THREADS) s_cnt[i] = 0;
-    if (a.S_in_lds)
-        for (int i = tid; i < M * M * E; i += RT_THREADS) s_S[i] = a.S[i];
+    if (a.S_in_lds) stage_copy((int32_t*)s_S, (const int32_t*)a.S, M * M * E, tid);
     // this thread's token location and budget, read before the router loop so
     // that their latency is hidden behind it (lanes of waves 0-3 own tokens)
     int loc_pre = 0;
@@ -141,7 +203,22 @@ route_select_kernel(const RouteArgs a) {
     }
 
     // ---------------- router logits ----------------
-    if (a.dtype == ORDERMOE_BF16) {
+    if (a.ksplit > 0) {
+        // split router: add the K slices in slice order (the reads of all
+        // slices of an element are issued before the additions)
+        for (int i = tid; i < RT_TB * Epad; i += RT_THREADS) {
+            const int64_t tok = t0 + i / Epad;
+            float pv[RT_SPLIT_MAX_K];
+#pragma unroll
+            for (int z = 0; z < RT_SPLIT_MAX_K; ++z)
+                pv[z] = (z < a.ksplit && tok < a.T) ? a.logit_part[((int64_t)z * a.T + tok) * Epad + i % Epad] : 0.f;
+            float v = 0.f;
+#pragma unroll
+            for (int z = 0; z < RT_SPLIT_MAX_K; ++z)
+                if (z < a.ksplit) v += pv[z];
+            s_logit[i] = v;
+        }
+    } else if (a.dtype == ORDERMOE_BF16) {
         const int nblk = Epad / 16;
         f32x4 acc[NBT];
 #pragma unroll
@@ -345,60 +422,44 @@ route_select_kernel(const RouteArgs a) {
 }
 
 constexpr int SCAN_THREADS = 1024;
+constexpr int SCAN_WAVES = SCAN_THREADS / 64;
 
-// Exclusive scan over blocks of the per-destination counts; destination
-// segments are laid out in server order.  Also totals the counters.
+// One block, every wave on its own (no block-wide barriers): waves 0-7 total
+// the eight counters over the token blocks; wave w (and w + 16) scans the
+// per-block counts of destination w over the blocks, giving each block's
+// first position inside that destination's segment and the destination's
+// total.  The segments follow in server order (dispatch_scatter_kernel adds
+// the segment start).
 __global__ void __launch_bounds__(SCAN_THREADS)
 dispatch_scan_kernel(const int32_t* blk_dst, const int64_t* blk_cnt, int nblk, int M,
                      int32_t* dst_base, int32_t* dst_count, int64_t* counters) {
-    __shared__ int64_t s_red[SCAN_THREADS / 64];
-    __shared__ int32_t s_scan[SCAN_THREADS / 64];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    // counters
-    for (int c = 0; c < 8; ++c) {
+    if (wave < 8) {
         int64_t v = 0;
-        for (int b = tid; b < nblk; b += SCAN_THREADS) v += blk_cnt[(int64_t)b * 8 + c];
+        for (int b = lane; b < nblk; b += 64) v += blk_cnt[(int64_t)b * 8 + wave];
         for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
-        if (lane == 0) s_red[wave] = v;
-        __syncthreads();
-        if (tid == 0) {
-            int64_t s = 0;
-            for (int w = 0; w < SCAN_THREADS / 64; ++w) s += s_red[w];
-            counters[c] = s;
-        }
-        __syncthreads();
+        if (lane == 0) counters[wave] = v;
     }
-    int32_t start = 0;  // first list position of the current destination
-    for (int m = 0; m < M; ++m) {
-        int32_t carry = start;
-        for (int b0 = 0; b0 < nblk; b0 += SCAN_THREADS) {
-            const int b = b0 + tid;
+    for (int m = wave; m < M; m += SCAN_WAVES) {
+        int32_t carry = 0;
+        for (int b0 = 0; b0 < nblk; b0 += 64) {
+            const int b = b0 + lane;
             const int32_t v = b < nblk ? blk_dst[(int64_t)b * M + m] : 0;
-            // inclusive scan within the wave
             int32_t inc = v;
             for (int off = 1; off < 64; off <<= 1) {
-                int32_t o = __shfl_up(inc, off);
+                const int32_t o = __shfl_up(inc, off);
                 if (lane >= off) inc += o;
             }
-            if (lane == 63) s_scan[wave] = inc;
-            __syncthreads();
-            int32_t wbase = 0, ctot = 0;
-            for (int w = 0; w < SCAN_THREADS / 64; ++w) {
-                if (w < wave) wbase += s_scan[w];
-                ctot += s_scan[w];
-            }
-            if (b < nblk) dst_base[(int64_t)b * M + m] = carry + wbase + inc - v;
-            carry += ctot;
-            __syncthreads();
+            if (b < nblk) dst_base[(int64_t)b * M + m] = carry + inc - v;
+            carry += __shfl(inc, 63);
         }
-        if (tid == 0) dst_count[m] = carry - start;
-        start = carry;
+        if (lane == 0) dst_count[m] = carry;
     }
 }
 
 __global__ void __launch_bounds__(RT_THREADS)
 dispatch_scatter_kernel(const uint8_t* exec_m, const uint8_t* loc_in, int64_t T, int k, int M,
-                        const int32_t* dst_base, int32_t* dispatch) {
+                        const int32_t* dst_base, const int32_t* dst_count, int32_t* dispatch) {
     __shared__ int8_t s_dst[RT_TB * ORDERMOE_MAX_TOPK];
     const int tid = threadIdx.x;
     const int64_t t0 = (int64_t)blockIdx.x * RT_TB;
@@ -418,7 +479,9 @@ dispatch_scatter_kernel(const uint8_t* exec_m, const uint8_t* loc_in, int64_t T,
         const int dst = s_dst[tid];
         int rank = 0;
         for (int i = 0; i < tid; ++i) rank += (s_dst[i] == dst);
-        const int32_t pos = dst_base[(int64_t)blockIdx.x * M + dst] + rank;
+        int32_t start = 0;                        // the destination's segment
+        for (int m = 0; m < dst; ++m) start += dst_count[m];
+        const int32_t pos = start + dst_base[(int64_t)blockIdx.x * M + dst] + rank;
         dispatch[pos] = (int32_t)((t0 + tid / k) * k + tid % k);
     }
 }
@@ -445,18 +508,39 @@ size_t route_smem_bytes(int E, int gmax, int M, bool S_in_lds) {
            sizeof(int) * (size_t)(8 + M) + (S_in_lds ? sizeof(float) * (size_t)M * M * E : 0);
 }
 
+// partial logits of the split router: at most 256 blocks of RT_TB tokens times
+// the K slices (the launcher keeps slices * blocks <= 256), every expert count
+size_t route_split_buffer_floats(int64_t T) {
+    const int64_t rows = T * RT_SPLIT_MAX_K < 256 * RT_TB ? T * RT_SPLIT_MAX_K : 256 * RT_TB;
+    return (size_t)(rows > 0 ? rows : 1) * ORDERMOE_MAX_EXPERTS;
+}
+
 // the cost table is staged in LDS when it is small enough to leave room for
-// two blocks per CU
-static bool route_S_in_lds(int E, int gmax, int M) {
-    return route_smem_bytes(E, gmax, M, true) <= 64 * 1024;
+// two blocks per CU, or, for batches of at most one block per CU, when it fits
+static bool route_S_in_lds(int E, int gmax, int M, int nblk) {
+    const size_t b = route_smem_bytes(E, gmax, M, true);
+    return b <= 64 * 1024 || (nblk <= 256 && b <= 150 * 1024);
 }
 
 int launch_route_select(const RouteArgs& a, void* stream) {
     hipStream_t st = (hipStream_t)stream;
     if (a.nblk > 0) {
         RouteArgs b = a;
-        b.S_in_lds = route_S_in_lds(a.E, a.gmax, a.M) ? 1 : 0;
+        b.S_in_lds = route_S_in_lds(a.E, a.gmax, a.M, a.nblk) ? 1 : 0;
         const size_t smem = route_smem_bytes(a.E, a.gmax, a.M, b.S_in_lds != 0);
+        b.ksplit = 0;
+        if (a.dtype == ORDERMOE_BF16 && a.T <= RT_SPLIT_MAX_T && a.logit_part) {
+            // enough waves to cover the CUs, K slices a multiple of 32
+            const int nbe = (a.E + 15) / 16;
+            int ks = 256 / (a.nblk * nbe);
+            ks = ks < 1 ? 1 : (ks > RT_SPLIT_MAX_K ? RT_SPLIT_MAX_K : ks);
+            while (ks > 1 && a.d % (32 * ks) != 0) --ks;
+            b.ksplit = ks;
+            KernelTimer kt_("router_split", st);
+            router_split_kernel<<<dim3((unsigned)a.nblk, (unsigned)nbe, (unsigned)ks), dim3(64), 0, st>>>(b);
+            hipError_t e = hipGetLastError();
+            if (e != hipSuccess) return (int)e;
+        }
         const int nb = (a.E + 15) / 16;
         const int nbt = nb <= 1 ? 1 : nb <= 2 ? 2 : nb <= 4 ? 4 : nb <= 8 ? 8 : 16;
         int e = 0;
@@ -480,7 +564,8 @@ int launch_route_select(const RouteArgs& a, void* stream) {
         {
         KernelTimer kt_("dispatch_scatter", st);
         hipLaunchKernelGGL(dispatch_scatter_kernel, dim3(a.nblk), dim3(RT_THREADS), 0, st,
-                           a.out.exec_m, a.loc_in, a.T, a.k, a.M, a.dst_base, a.out.dispatch);
+                           a.out.exec_m, a.loc_in, a.T, a.k, a.M, a.dst_base, a.out.dst_count,
+                           a.out.dispatch);
         }
         e = hipGetLastError();
         if (e != hipSuccess) return (int)e;

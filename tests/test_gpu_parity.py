@@ -284,3 +284,51 @@ def test_runs_are_bitwise_deterministic(name):
                     host(out["counters"])))
     for a, b in zip(res[0], res[1]):
         np.testing.assert_array_equal(a, b)
+
+
+def test_graph_replay_matches_eager():
+    """route/select and the local forward captured in a HIP graph: every
+    replay, with eager work and synchronisation between them, equals the eager
+    result bit for bit (decode-sized and prefill-sized batches)."""
+    for name in ("C3d", "C2s"):
+        case, tabs = _case(name, {**SMALL, **DECODE}[name])
+        dl = DeviceLayer(case, tabs)
+        x, loc, qh = dl.inputs()
+        T = case.X.shape[0]
+        cfg = case.cfg
+        from paper_2607_17154_amd import ordermoe as om
+        out = om.alloc_route_out(T, cfg.k, cfg.M, "cuda")
+        ws_r = torch.empty(max(om.ordermoe_route_workspace_size(T, cfg.k, cfg.M), 1), dtype=torch.uint8,
+                           device="cuda")
+        y = torch.empty((T, cfg.d), dtype=torch.bfloat16, device="cuda")
+        ro = torch.empty(dl.experts.n_local + 2, dtype=torch.int32, device="cuda")
+        ws_f = torch.empty(max(om.ordermoe_forward_workspace_size(dl.experts, T, cfg.k), 1),
+                           dtype=torch.uint8, device="cuda")
+
+        def step():
+            om.ordermoe_route_select(dl.layer, x, T, loc, qh, out, ws_r)
+            om.ordermoe_local_moe_forward(dl.experts, x, T, cfg.k, out["w"], out["exec_k"], out["exec_m"],
+                                          loc, cfg.m0, y, ro, ws_f)
+
+        step()
+        torch.cuda.synchronize()
+        want = [host(out[n]) for n in ("exec_k", "exec_m", "counters")] + [host(y)]
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            step()
+        for rep in range(3):
+            y.zero_()
+            out["exec_k"].fill_(-7)
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            got = [host(out[n]) for n in ("exec_k", "exec_m", "counters")] + [host(y)]
+            for a_, b_ in zip(got, want):
+                np.testing.assert_array_equal(a_, b_)
+        del g
