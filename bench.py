@@ -112,9 +112,18 @@ def _setup(cfg, torch, om):
         om.ordermoe_pack_gate_up(gd.unsqueeze(0), ud.unsqueeze(0), w_gu[i:i + 1])
         w_dn[i] = up(dn)
         del gd, ud
-    experts = om.make_experts(code, cfg.d, cfg.f, cfg.E, local, w_gu, w_dn)
+    w_sh_gu = w_sh_dn = None
+    if cfg.n_shared:
+        sh = [wl.shared_expert(cfg, i) for i in range(cfg.n_shared)]
+        sg = torch.cat([up(a[0]) for a in sh], 0).unsqueeze(0).contiguous()
+        su = torch.cat([up(a[1]) for a in sh], 0).unsqueeze(0).contiguous()
+        w_sh_gu = torch.empty((1, 2 * cfg.n_shared * cfg.f, cfg.d), dtype=tdt, device=dev)
+        om.ordermoe_pack_gate_up(sg, su, w_sh_gu)
+        w_sh_dn = torch.cat([up(a[2]) for a in sh], 1).contiguous()
+        del sg, su
+    experts = om.make_experts(code, cfg.d, cfg.f, cfg.E, local, w_gu, w_dn, cfg.n_shared, w_sh_gu, w_sh_dn)
     X = wl.tokens(cfg)
-    st = dict(layer=layer, experts=experts, keep=(w_router, tabs_dev, w_gu, w_dn), local=local,
+    st = dict(layer=layer, experts=experts, keep=(w_router, tabs_dev, w_gu, w_dn, w_sh_gu, w_sh_dn), local=local,
               x=up(X), loc=torch.from_numpy(wl.token_locations(cfg)).to(dev),
               qhat=torch.from_numpy(wl.accumulated_loss(cfg)).to(dev), X=X, W=W, model=model,
               x_dep=x_dep, net=net, c=c, dref=dref, z_bits=z_bits)
@@ -212,6 +221,54 @@ def _simbuild(torch, om, reps: int = 5):
             "kernels_avg_us": {k: v[0] / v[1] * 1e3 for k, v in kt.items()},
             "hbm_bytes": nbytes, "achieved_GBs": nbytes / us / 1e3,
             "hbm_frac": nbytes / us / 1e3 / PEAK_HBM_GBS}
+
+
+def _other_layers(torch, om, steps: int = 10, warmup: int = 3):
+    """The Qwen-MoE-shaped (8192 tokens, 60 experts + 4 shared, top-4) and
+    DeepSeek-MoE-shaped (16384 tokens, 64 experts + 2 shared, top-6) layers of
+    server 0: step time, the FFN GEMMs' MFMA rates and routing's HBM rate."""
+    import workloads as wl
+    res = {}
+    for key, cfg in (("C3", wl.C3), ("C4", wl.C4)):
+        st = _setup(cfg, torch, om)
+        for _ in range(warmup):
+            _step(cfg, st, om)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            _step(cfg, st, om)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        om.ordermoe_timing_read(reset=True)
+        om.ordermoe_timing_enable(True)
+        for _ in range(steps):
+            _step(cfg, st, om)
+        torch.cuda.synchronize()
+        om.ordermoe_timing_enable(False)
+        kt = om.ordermoe_timing_read(reset=True)
+        avg = {n: v[0] / v[1] * 1e3 for n, v in kt.items()}
+        ro = st["ro"].cpu().numpy()
+        n_loc = len(st["local"])
+        r_routed = int(ro[n_loc])
+        r_shared = int(ro[-1]) - r_routed
+        fl_gu = 2.0 * cfg.d * 2 * cfg.f * r_routed + 2.0 * cfg.d * 2 * cfg.n_shared * cfg.f * r_shared
+        fl_dn = fl_gu / 2
+        gu_us = avg.get("gemm_gate_up", 0.0) + avg.get("gemm_gate_up_tail", 0.0)
+        rt_bytes = cfg.T * cfg.d * 2 + cfg.E * cfg.d * 2 + cfg.T * cfg.k * 14 + cfg.T * 11
+        rt_us = avg.get("route_select", float("nan"))
+        res[key] = {"workload": cfg.name, "ms_per_step": ms, "tokens_per_s": cfg.T / (ms / 1e3),
+                    "local_rows_routed": r_routed, "local_rows_shared": r_shared,
+                    "gemm_gate_up_TFLOPs": fl_gu / gu_us / 1e6,
+                    "gemm_gate_up_frac": fl_gu / gu_us / 1e6 / PEAK_BF16_TFLOPS,
+                    "gemm_down_TFLOPs": fl_dn / avg["gemm_down"] / 1e6,
+                    "gemm_down_frac": fl_dn / avg["gemm_down"] / 1e6 / PEAK_BF16_TFLOPS,
+                    "route_select_us": rt_us, "route_hbm_frac": rt_bytes / rt_us / 1e3 / PEAK_HBM_GBS,
+                    "kernels_avg_us": dict(sorted(avg.items()))}
+        del st
+        torch.cuda.empty_cache()
+    return res
 
 
 def _decode_stream(torch, om, steps: int = 10, warmup: int = 2):
@@ -368,6 +425,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-simbuild", action="store_true",
                     help="skip the similarity-build measurement (65536 x 4096 calibration tokens)")
+    ap.add_argument("--no-other-layers", action="store_true",
+                    help="skip the Qwen-MoE- and DeepSeek-MoE-shaped layer measurements")
     ap.add_argument("--no-stream", action="store_true",
                     help="skip the 32-layer decode-stream measurement")
     ap.add_argument("--only", choices=("layer", "simbuild", "stream"),
@@ -402,7 +461,7 @@ def main():
         print(json.dumps(_decode_stream(torch, om, steps=args.steps, warmup=args.warmup)))
         return
     if args.only == "layer":
-        args.no_simbuild = args.no_stream = args.no_cpu_baseline = True
+        args.no_simbuild = args.no_stream = args.no_cpu_baseline = args.no_other_layers = True
     print("bench: setting up %s" % cfg.name, file=sys.stderr, flush=True)
     st = _setup(cfg, torch, om)
     torch.cuda.synchronize()
@@ -460,6 +519,9 @@ def main():
     if not args.no_simbuild:
         print("bench: similarity build", file=sys.stderr, flush=True)
         res["similarity_build"] = _simbuild(torch, om)
+    if not args.no_other_layers:
+        print("bench: C3 and C4 layers", file=sys.stderr, flush=True)
+        res["other_layers"] = _other_layers(torch, om)
     if not args.no_stream:
         print("bench: decode stream", file=sys.stderr, flush=True)
         del st["experts"], st["keep"]

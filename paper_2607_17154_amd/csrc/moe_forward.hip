@@ -266,10 +266,15 @@ struct TileLoc {
     int g, m0, n0, R, N, K, rowbase;
 };
 
+// Tile order: the shared group first (its down projection has the longest K,
+// so its tiles start first and the shorter routed tiles fill in around them),
+// then the routed groups; inside a group tiles are m-fastest.
 template <int BM, int BN>
 __device__ inline bool decode_tile(const GemmArgs& p, int tile, TileLoc& L) {
     int rem = tile;
-    for (int g = 0; g < p.G; ++g) {
+    const bool has_sh = p.G > p.n_routed;
+    for (int gi = 0; gi < p.G; ++gi) {
+        const int g = has_sh ? (gi == 0 ? p.n_routed : gi - 1) : gi;
         const int off = p.offsets[g];
         const int R = p.offsets[g + 1] - off;
         const bool sh = g >= p.n_routed;
@@ -353,7 +358,15 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
     const int head = PART == 0 ? total : (total / p.head_grid) * p.head_grid;
     const int ntile = PART == 2 ? 2 * (total - head) : head;
 
-    for (int tile = vid; tile < ntile; tile += gridDim.x) {
+    // rounds of G tiles in snake order (odd rounds reversed), so that the
+    // workgroups that took the long tiles at the head of the list take the last
+    // tiles of the next round
+    for (int r = 0;; ++r) {
+        const int tile = r * (int)gridDim.x + ((r & 1) ? (int)gridDim.x - 1 - vid : vid);
+        if (tile >= ntile) {
+            if (r & 1) continue;     // a partial odd round: the high tiles are missing
+            break;
+        }
         TileLoc L;
         if (PART == 2) {
             if (!decode_tile<BM, 2 * BN>(p, head + (tile >> 1), L)) break;

@@ -105,19 +105,36 @@ __device__ inline void router_k_loop(const RouteArgs& a, int wave, int lane, int
     }
 }
 
-// global -> LDS copy of n 32-bit words by the block, 8 reads in flight per thread
-__device__ inline void stage_copy(int32_t* dst, const int32_t* src, int n, int tid) {
-    for (int i0 = 0; i0 < n; i0 += 8 * RT_THREADS) {
+// global -> LDS copy of five arrays of 32-bit words by the block, as one
+// index space with 8 reads in flight per thread before their stores
+__device__ inline void stage_copy5(int32_t* const* dst, const int32_t* const* src, const int* len,
+                                   int tid) {
+    int end[5];
+    int tot = 0;
+#pragma unroll
+    for (int q = 0; q < 5; ++q) { tot += len[q]; end[q] = tot; }
+    auto locate = [&](int i, int& q, int& o) {
+        q = 0;
+        o = i;
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+            if (i >= end[c]) { q = c + 1; o = i - end[c]; }
+    };
+    for (int i0 = 0; i0 < tot; i0 += 8 * RT_THREADS) {
         int32_t v[8];
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
             const int i = i0 + u * RT_THREADS + tid;
-            v[u] = i < n ? src[i] : 0;
+            int q, o;
+            locate(i, q, o);
+            v[u] = i < tot ? src[q][o] : 0;
         }
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
             const int i = i0 + u * RT_THREADS + tid;
-            if (i < n) dst[i] = v[u];
+            int q, o;
+            locate(i, q, o);
+            if (i < tot) dst[q][o] = v[u];
         }
     }
 }
@@ -165,7 +182,7 @@ __global__ void __launch_bounds__(64) router_split_kernel(const RouteArgs a) {
 }
 
 template <int NBT>
-__global__ void __launch_bounds__(RT_THREADS)
+__global__ void __launch_bounds__(RT_THREADS, 2)
 route_select_kernel(const RouteArgs a) {
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -187,12 +204,14 @@ route_select_kernel(const RouteArgs a) {
 
     // stage the candidate tables (small) and clear the block counters; the
     // copies issue several reads per thread before their LDS stores
-    stage_copy(s_t1k, a.t1_k, E * a.gmax, tid);
-    stage_copy((int32_t*)s_t1q, (const int32_t*)a.t1_q, E * a.gmax, tid);
-    stage_copy(s_t1n, a.t1_n, E, tid);
-    stage_copy((int32_t*)s_mask, (const int32_t*)a.srvmask, E, tid);
+    {
+        const int32_t* src[5] = {a.t1_k, (const int32_t*)a.t1_q, a.t1_n, (const int32_t*)a.srvmask,
+                                 (const int32_t*)a.S};
+        int32_t* dst[5] = {s_t1k, (int32_t*)s_t1q, s_t1n, (int32_t*)s_mask, (int32_t*)s_S};
+        const int len[5] = {E * a.gmax, E * a.gmax, E, E, a.S_in_lds ? M * M * E : 0};
+        stage_copy5(dst, src, len, tid);
+    }
     for (int i = tid; i < 8 + M; i += RT_THREADS) s_cnt[i] = 0;
-    if (a.S_in_lds) stage_copy((int32_t*)s_S, (const int32_t*)a.S, M * M * E, tid);
     // this thread's token location and budget, read before the router loop so
     // that their latency is hidden behind it (lanes of waves 0-3 own tokens)
     int loc_pre = 0;
@@ -223,11 +242,12 @@ route_select_kernel(const RouteArgs a) {
         f32x4 acc[NBT];
 #pragma unroll
         for (int i = 0; i < NBT; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-        // unroll depth: every wave keeps 16-32 loads of 16 bytes in flight
-        if constexpr (NBT == 1) router_k_loop<1, 16>(a, wave, lane, t0, acc);
-        else if constexpr (NBT == 2) router_k_loop<2, 8>(a, wave, lane, t0, acc);
-        else if constexpr (NBT == 4) router_k_loop<4, 4>(a, wave, lane, t0, acc);
-        else if constexpr (NBT == 8) router_k_loop<8, 2>(a, wave, lane, t0, acc);
+        // unroll depth: every wave keeps 9-16 loads of 16 bytes in flight, within
+        // 128 registers so that two blocks share a CU
+        if constexpr (NBT == 1) router_k_loop<1, 8>(a, wave, lane, t0, acc);
+        else if constexpr (NBT == 2) router_k_loop<2, 4>(a, wave, lane, t0, acc);
+        else if constexpr (NBT == 4) router_k_loop<4, 2>(a, wave, lane, t0, acc);
+        else if constexpr (NBT == 8) router_k_loop<8, 1>(a, wave, lane, t0, acc);
         else router_k_loop<16, 1>(a, wave, lane, t0, acc);
         // acc[nb][i] = partial logit of token (lane/16)*4 + i, expert nb*16 + lane%16.
         // Two-round reduction over the 8 waves in a fixed order: waves 4-7 hand
@@ -286,8 +306,13 @@ route_select_kernel(const RouteArgs a) {
     const bool valid = t < a.T;
     const float* lg = s_logit + tr * Epad;
 
-    // top-(k+1) selection by (logit desc, index asc)
+    // top-(k+1) selection by (logit desc, index asc); this lane's logits (experts
+    // j + 16 i) are read once and kept as order-preserving keys
+    constexpr int PER_LANE = ORDERMOE_MAX_EXPERTS / 16;
     const int kk1 = (k + 1 < E) ? k + 1 : E;
+    uint32_t okey[PER_LANE];
+#pragma unroll
+    for (int i = 0; i < PER_LANE; ++i) okey[i] = (j + 16 * i < E) ? f2ord(lg[j + 16 * i]) : 0u;
     uint32_t removed = 0;                    // bit i: local element j + 16 i taken
     int sel_e[ORDERMOE_MAX_TOPK + 1];
     float sel_v[ORDERMOE_MAX_TOPK + 1];
@@ -295,9 +320,11 @@ route_select_kernel(const RouteArgs a) {
     for (int r = 0; r < ORDERMOE_MAX_TOPK + 1; ++r) {
         if (r < kk1) {
             uint64_t best = 0;
-            for (int i = 0, e = j; e < E; ++i, e += 16) {
-                if (removed & (1u << i)) continue;
-                uint64_t key = ((uint64_t)f2ord(lg[e]) << 32) | (uint32_t)(0xFFFFu - (uint32_t)e);
+#pragma unroll
+            for (int i = 0; i < PER_LANE; ++i) {
+                const int e = j + 16 * i;
+                if (e >= E || (removed & (1u << i))) continue;
+                const uint64_t key = ((uint64_t)okey[i] << 32) | (uint32_t)(0xFFFFu - (uint32_t)e);
                 best = key > best ? key : best;
             }
 #pragma unroll
