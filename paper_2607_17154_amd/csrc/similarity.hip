@@ -81,7 +81,6 @@ __global__ void __launch_bounds__(ST_THREADS, 1) sim_tile_kernel(const SimArgs a
     const uint32_t bstride = 128u * (uint32_t)d;        // 64 rows, in bytes
     const int brow_off = (lane & 31) * LDK + (lane >> 5) * 8;
     constexpr uint32_t OOR = 0x80000000u;
-    const int ti = tid >> 4, tj = tid & 15;             // Gram tile: rows 4 ti .. +3, columns 8 tj .. +7
     float* gp = a.gram_part + (int64_t)blockIdx.x * SIM_EMAX * SIM_EMAX;
     bool first_tile = true;
 
@@ -207,32 +206,41 @@ __global__ void __launch_bounds__(ST_THREADS, 1) sim_tile_kernel(const SimArgs a
                 if (r < k && te[r] >= 0) atomicAdd(&s_cnt[te[r]], 1);
         }
         // Gram += H^T H over this tile's tokens (padding experts are zero
-        // columns), accumulated in the workgroup's workspace slot
+        // columns) by v_mfma_f32_32x32x2f32 -- fp32 operands, so the products
+        // are those of fp32 FMAs -- accumulated in the workgroup's workspace
+        // slot.  Wave w owns the 32 x 32 blocks (w / 2, 2 (w % 2)) and
+        // (w / 2, 2 (w % 2) + 1); operand lane l holds row/column l % 32 of
+        // token t + l / 32 of each pair.
         {
-            float gacc[4][8];
+            const int bi = wave >> 1, bj0 = (wave & 1) * 2;
+            f32x16 g0, g1;
+            // element e of a block: row (e/4)*8 + (lane/32)*4 + e%4, column lane%32
 #pragma unroll
-            for (int u = 0; u < 4; ++u)
-#pragma unroll
-                for (int v = 0; v < 8; ++v)
-                    gacc[u][v] = first_tile ? 0.f : gp[(4 * ti + u) * SIM_EMAX + 8 * tj + v];
+            for (int e = 0; e < 16; ++e) {
+                const int gr = bi * 32 + (e >> 2) * 8 + (lane >> 5) * 4 + (e & 3);
+                const int gc = lane & 31;
+                g0[e] = first_tile ? 0.f : gp[gr * SIM_EMAX + bj0 * 32 + gc];
+                g1[e] = first_tile ? 0.f : gp[gr * SIM_EMAX + (bj0 + 1) * 32 + gc];
+            }
+            const int tl = lane >> 5, cl = lane & 31;
 #pragma unroll 4
-            for (int t = 0; t < nt; ++t) {
-                const float* hr = sH + t * ST_LDH;
-                const f32x4 hu = *(const f32x4*)(hr + 4 * ti);
-                const f32x4 hv0 = *(const f32x4*)(hr + 8 * tj);
-                const f32x4 hv1 = *(const f32x4*)(hr + 8 * tj + 4);
-#pragma unroll
-                for (int u = 0; u < 4; ++u)
-#pragma unroll
-                    for (int v = 0; v < 4; ++v) {
-                        gacc[u][v] = fmaf(hu[u], hv0[v], gacc[u][v]);
-                        gacc[u][v + 4] = fmaf(hu[u], hv1[v], gacc[u][v + 4]);
-                    }
+            for (int t = 0; t < nt; t += 2) {
+                const int tt = t + tl;
+                const bool ok = tt < nt;
+                const float* hr = sH + (ok ? tt : 0) * ST_LDH;
+                const float av = ok ? hr[bi * 32 + cl] : 0.f;
+                const float bv0 = ok ? hr[bj0 * 32 + cl] : 0.f;
+                const float bv1 = ok ? hr[(bj0 + 1) * 32 + cl] : 0.f;
+                g0 = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv0, g0, 0, 0, 0);
+                g1 = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv1, g1, 0, 0, 0);
             }
 #pragma unroll
-            for (int u = 0; u < 4; ++u)
-#pragma unroll
-                for (int v = 0; v < 8; ++v) gp[(4 * ti + u) * SIM_EMAX + 8 * tj + v] = gacc[u][v];
+            for (int e = 0; e < 16; ++e) {
+                const int gr = bi * 32 + (e >> 2) * 8 + (lane >> 5) * 4 + (e & 3);
+                const int gc = lane & 31;
+                gp[gr * SIM_EMAX + bj0 * 32 + gc] = g0[e];
+                gp[gr * SIM_EMAX + (bj0 + 1) * 32 + gc] = g1[e];
+            }
         }
         first_tile = false;
         __syncthreads();   // before the next tile's W overwrites H
