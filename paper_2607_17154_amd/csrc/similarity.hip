@@ -8,9 +8,9 @@
 //                        tokens streamed from HBM once, straight into operand
 //                        registers several K steps ahead, W_r through LDS; the
 //                        fp32 H tile then parked in LDS for the per-token top-k
-//                        counts (and top-1) and Gram += H^T H with an 8 x 8
-//                        register tile per thread; per-workgroup partial Gram
-//                        and counts to the workspace
+//                        counts (and top-1), then Gram += H^T H by bf16 MFMAs
+//                        on a two-term bf16 split of H; per-workgroup partial
+//                        Gram and counts to the workspace
 //   sim_partial_kernel   fp32 storage: chunks of 128 tokens, fp64 dot products
 //                        rounded to fp32, same partial outputs
 //   sim_reduce_kernel    fixed-order fp64 sum of the partials: 16 slices of
@@ -28,6 +28,7 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 
 constexpr int SIM_TC = 128;        // tokens per chunk
 constexpr int SIM_EMAX = 128;      // experts supported by the fused kernel
@@ -42,9 +43,12 @@ constexpr int ST_THREADS = ST_WAVES * 64;
 constexpr int ST_BK = 64, ST_LDK = ST_BK + 8;
 constexpr int ST_STAGES = 4;               // K steps of reads in flight per wave
 constexpr int ST_LDH = SIM_EMAX + 4;       // row stride of the parked H tile (floats)
+constexpr int ST_LDT = ST_BM + 8;          // row stride of the h / l planes of H^T (bf16)
 constexpr size_t ST_LDS_KLOOP = (size_t)2 * SIM_EMAX * ST_LDK * 2;
 constexpr size_t ST_LDS_H = (size_t)ST_BM * ST_LDH * 4;
-constexpr size_t ST_LDS = ST_LDS_KLOOP > ST_LDS_H ? ST_LDS_KLOOP : ST_LDS_H;
+constexpr size_t ST_LDS_HL = (size_t)2 * SIM_EMAX * ST_LDT * 2;
+constexpr size_t ST_LDS_MAX2 = ST_LDS_KLOOP > ST_LDS_H ? ST_LDS_KLOOP : ST_LDS_H;
+constexpr size_t ST_LDS = ST_LDS_MAX2 > ST_LDS_HL ? ST_LDS_MAX2 : ST_LDS_HL;
 
 __device__ inline bf16x8 st_load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
     u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, 0);
@@ -57,8 +61,9 @@ __device__ inline bf16x8 st_load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint
 // lane%32, K elements 8*(lane/32) .. +7 of each 16); the router rows W_r (L2
 // resident) go through a double-buffered LDS tile shared by the waves.  The
 // reads of a K step are issued ST_STAGES steps ahead.  After the K loop the
-// fp32 H tile is parked in LDS for the top-k counts and the Gram update; the
-// Gram partial of a workgroup lives in its workspace slot.
+// fp32 H tile is parked in LDS for the top-k counts, then replaced by the bf16
+// h / l planes of H^T for the Gram update; the Gram partial of a workgroup
+// lives in its workspace slot.
 __global__ void __launch_bounds__(ST_THREADS, 1) sim_tile_kernel(const SimArgs a) {
     constexpr int BN = SIM_EMAX, BK = ST_BK, LDK = ST_LDK, S = ST_STAGES;
     constexpr int FN = BN / 32;                         // per wave: 32 tokens x 128 experts
@@ -168,50 +173,87 @@ __global__ void __launch_bounds__(ST_THREADS, 1) sim_tile_kernel(const SimArgs a
         __syncthreads();
 
         // activation counts: top-k of each token's logits, ties to the lower
-        // index.  One thread per token scans the logits in expert order and keeps
-        // a sorted top-k list in registers, branch-free: a logit's place is the
-        // number of kept logits >= it (so equal logits keep their index order),
-        // the entries from that place on move down one, and a place of k or more
-        // leaves the list unchanged.
-        for (int tt = tid; tt < nt; tt += ST_THREADS) {
+        // index.  Two threads per token: lanes l and l + 32 of wave w take token
+        // 32 w + l % 32, the first scanning experts 0..63, the second 64..127.
+        // Each keeps a sorted top list in registers by a branch-free insertion
+        // network: the incoming logit moves down the list past every entry it
+        // does not exceed, so an equal logit never passes one of lower index.
+        // The lower half then inserts the upper half's list, whose indices are
+        // all higher, in its sorted order.
+        {
             constexpr int MK = ORDERMOE_MAX_TOPK;
-            const int k = a.k;
+            const int tt = wave * 32 + (lane & 31);
+            const int half = lane >> 5;
             float tv[MK];
             int te[MK];
 #pragma unroll
             for (int r = 0; r < MK; ++r) { tv[r] = -__builtin_inff(); te[r] = -1; }
-            const float* row = sH + tt * ST_LDH;
-            for (int e4 = 0; e4 < E; e4 += 4) {
+            auto insert = [&](float v, int e) {
+#pragma unroll
+                for (int r = 0; r < MK; ++r) {
+                    const bool c = v > tv[r];
+                    const float kv = c ? v : tv[r];
+                    const int ke = c ? e : te[r];
+                    v = c ? tv[r] : v;
+                    e = c ? te[r] : e;
+                    tv[r] = kv;
+                    te[r] = ke;
+                }
+            };
+            const float* row = sH + (tt < nt ? tt : 0) * ST_LDH + half * (SIM_EMAX / 2);
+#pragma unroll 2
+            for (int e4 = 0; e4 < SIM_EMAX / 2; e4 += 4) {
                 const f32x4 v4 = *(const f32x4*)(row + e4);
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
-                    const int e = e4 + q;
-                    const float v = v4[q];
-                    int pos = 0;
-#pragma unroll
-                    for (int r = 0; r < MK; ++r) pos += (r < k && te[r] >= 0 && tv[r] >= v) ? 1 : 0;
-                    if (e >= E) pos = MK;             // padding column: no change
-#pragma unroll
-                    for (int r = MK - 1; r >= 0; --r) {
-                        const float below_v = r > 0 ? tv[r - 1] : v;
-                        const int below_e = r > 0 ? te[r - 1] : e;
-                        tv[r] = r < pos ? tv[r] : (r == pos ? v : below_v);
-                        te[r] = r < pos ? te[r] : (r == pos ? e : below_e);
-                    }
+                    const int e = half * (SIM_EMAX / 2) + e4 + q;
+                    insert(e < E ? v4[q] : -__builtin_inff(), e);   // padding: never kept
                 }
             }
-            if (a.top1) a.top1[t0 + tt] = te[0];
+            float pv[MK];
+            int pe[MK];
 #pragma unroll
-            for (int r = 0; r < MK; ++r)
-                if (r < k && te[r] >= 0) atomicAdd(&s_cnt[te[r]], 1);
+            for (int r = 0; r < MK; ++r) { pv[r] = __shfl_xor(tv[r], 32); pe[r] = __shfl_xor(te[r], 32); }
+#pragma unroll
+            for (int r = 0; r < MK; ++r) insert(pv[r], pe[r]);
+            if (half == 0 && tt < nt) {
+                if (a.top1) a.top1[t0 + tt] = te[0];
+#pragma unroll
+                for (int r = 0; r < MK; ++r)
+                    if (r < a.k && te[r] >= 0) atomicAdd(&s_cnt[te[r]], 1);
+            }
         }
-        // Gram += H^T H over this tile's tokens (padding experts are zero
-        // columns) by v_mfma_f32_32x32x2f32 -- fp32 operands, so the products
-        // are those of fp32 FMAs -- accumulated in the workgroup's workspace
-        // slot.  Wave w owns the 32 x 32 blocks (w / 2, 2 (w % 2)) and
-        // (w / 2, 2 (w % 2) + 1); operand lane l holds row/column l % 32 of
-        // token t + l / 32 of each pair.
+        __syncthreads();   // the top-k is done with the fp32 H tile
+        // Gram += H^T H over this tile's tokens by v_mfma_f32_32x32x16_bf16 on
+        // a two-term bf16 split H = h + l (h = bf16(H), l = bf16(H - h)):
+        // H_i H_j ~ h_i h_j + h_i l_j + l_i h_j, leaving out l_i l_j and the
+        // rounding of l, each below 2^-17 |H_i H_j|; the products are exact in
+        // the fp32 accumulators.  H^T goes to LDS as h and l planes [expert]
+        // [token] straight from the K-loop accumulators (tokens past the tile
+        // end are zero rows).  Wave w owns the 32 x 32 Gram blocks
+        // (w / 2, 2 (w % 2)) and (w / 2, 2 (w % 2) + 1).
         {
+            constexpr int LDT = ST_LDT;
+            __bf16* sHh = (__bf16*)lds_raw;                 // [SIM_EMAX][LDT]
+            __bf16* sHl = sHh + SIM_EMAX * LDT;
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const int ex = j * 32 + (lane & 31);
+                    const int tk = wave * 32 + g * 8 + (lane >> 5) * 4;
+                    bf16x4 hv, lv;
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const float x = acc[j][4 * g + q];
+                        const __bf16 h = (__bf16)x;
+                        hv[q] = h;
+                        lv[q] = (__bf16)(x - (float)h);
+                    }
+                    *(bf16x4*)(sHh + ex * LDT + tk) = hv;
+                    *(bf16x4*)(sHl + ex * LDT + tk) = lv;
+                }
+            __syncthreads();
             const int bi = wave >> 1, bj0 = (wave & 1) * 2;
             f32x16 g0, g1;
             // element e of a block: row (e/4)*8 + (lane/32)*4 + e%4, column lane%32
@@ -222,17 +264,23 @@ __global__ void __launch_bounds__(ST_THREADS, 1) sim_tile_kernel(const SimArgs a
                 g0[e] = first_tile ? 0.f : gp[gr * SIM_EMAX + bj0 * 32 + gc];
                 g1[e] = first_tile ? 0.f : gp[gr * SIM_EMAX + (bj0 + 1) * 32 + gc];
             }
-            const int tl = lane >> 5, cl = lane & 31;
+            // operand lane l: expert row l % 32 of the block, tokens t + 8 (l / 32) .. +7
+            const int ro = (lane & 31) * LDT + (lane >> 5) * 8;
+            const __bf16* pa = sHh + bi * 32 * LDT + ro;
+            const __bf16* pb0 = sHh + bj0 * 32 * LDT + ro;
+            const __bf16* pb1 = sHh + (bj0 + 1) * 32 * LDT + ro;
+            constexpr int PL = SIM_EMAX * LDT;              // h plane -> l plane
 #pragma unroll 4
-            for (int t = 0; t < nt; t += 2) {
-                const int tt = t + tl;
-                const bool ok = tt < nt;
-                const float* hr = sH + (ok ? tt : 0) * ST_LDH;
-                const float av = ok ? hr[bi * 32 + cl] : 0.f;
-                const float bv0 = ok ? hr[bj0 * 32 + cl] : 0.f;
-                const float bv1 = ok ? hr[(bj0 + 1) * 32 + cl] : 0.f;
-                g0 = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv0, g0, 0, 0, 0);
-                g1 = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv1, g1, 0, 0, 0);
+            for (int t = 0; t < ST_BM; t += 16) {
+                const bf16x8 ah = *(const bf16x8*)(pa + t), al = *(const bf16x8*)(pa + PL + t);
+                const bf16x8 b0h = *(const bf16x8*)(pb0 + t), b0l = *(const bf16x8*)(pb0 + PL + t);
+                const bf16x8 b1h = *(const bf16x8*)(pb1 + t), b1l = *(const bf16x8*)(pb1 + PL + t);
+                g0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, b0h, g0, 0, 0, 0);
+                g1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, b1h, g1, 0, 0, 0);
+                g0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, b0l, g0, 0, 0, 0);
+                g1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, b1l, g1, 0, 0, 0);
+                g0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, b0h, g0, 0, 0, 0);
+                g1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, b1h, g1, 0, 0, 0);
             }
 #pragma unroll
             for (int e = 0; e < 16; ++e) {
