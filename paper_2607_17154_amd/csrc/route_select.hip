@@ -1,22 +1,26 @@
 // Routing and runtime server-expert selection of one MoE layer on gfx950.
 //
-// Kernel 1 (route_select_kernel), one block per RT_TB tokens:
+// Kernel 1 (route_select_kernel), one block of 8 waves per TB tokens (TB = 16,
+// or 32 for large batches of at most 64 experts):
+//   * the first words of the candidate tables are read into registers first,
+//     so that their latency hides behind the router loop, and stored to LDS
+//     after it;
 //   * router logits l = x W_r^T (eq 3, one token at a time):
-//       bf16: v_mfma_f32_16x16x32_bf16, the block's 16 tokens x all experts,
-//             d split over the 4 waves, partial sums added in wave order;
+//       bf16: v_mfma_f32_16x16x32_bf16 on 16-token row groups, the K steps of a
+//             row group split over its waves, partial sums added in wave order;
 //       fp32: fp64 dot products (exact products), rounded once to fp32;
-//   * per token (16 lanes each): top-(k+1) by a 64-bit (logit, -index) key
-//     max-reduced over the lanes, gates, margin and flag;
+//   * per token (16 lanes, one DPP row): top-(k+1) by a 64-bit (logit, -index)
+//     key max-reduced over the row with DPP rotations, gates, margin and flag;
 //   * per slot in rank order: the candidate search of eq (40)/(43) -- lane 0
 //     takes the exact candidate, lane j the (j-1)-th substitute of the LDS-
 //     staged table; each lane scans the servers holding its expert and keeps a
-//     64-bit key (J, position, remote, server); a min-reduce over the 16 lanes
-//     gives (m*, k*); the budget is updated as eq (44);
+//     64-bit key (J, position, remote, server); a min-reduce over the row gives
+//     (m*, k*); the budget is updated as eq (44);
 //   * per-block counters and per-destination remote-slot counts.
 // Kernel 2 (dispatch_scan_kernel), one block: exclusive scans of the
 //   per-block destination counts (one wave per destination), totals of the
 //   counters.
-// Kernel 3 (dispatch_scatter_kernel), one block per RT_TB tokens: stable
+// Kernel 3 (dispatch_scatter_kernel), one block per TB tokens: stable
 //   placement of the block's remote slots into the (destination, token, slot)
 //   ordered dispatch list.
 #include <hip/hip_runtime.h>
@@ -28,11 +32,12 @@
 namespace ordermoe {
 namespace {
 
-constexpr int RT_TB = 16;        // tokens per block
-constexpr int RT_THREADS = 512;  // 8 waves share the router's K loop; waves 0-3 then
-                                 // run the token stage, 16 lanes per token
+constexpr int RT_TB = 16;        // tokens per block (RT_TB2 for large batches)
+constexpr int RT_TB2 = 32;
+constexpr int RT_THREADS = 512;  // 8 waves share the router's K loop, then run the
+                                 // token stage, 16 lanes per token
 constexpr int RT_WAVES = RT_THREADS / 64;
-constexpr int RT_SLOTS = 4;      // partial-sum slots of the two-round wave reduction
+constexpr int RT_SLOTS = 4;      // partial-sum slots of the wave reduction
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -47,95 +52,141 @@ __device__ inline float ord2f(uint32_t o) {
     return __uint_as_float(u);
 }
 
-__device__ inline uint64_t shfl_xor64(uint64_t v, int mask) {
-    uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
-    lo = __shfl_xor(lo, mask, 16);
-    hi = __shfl_xor(hi, mask, 16);
+// Reductions over each row of 16 lanes (one token's lanes) with DPP row
+// rotations by 8, 4, 2, 1: after the four steps every lane of the row holds
+// the result.  Max and min are exact in any order; the float sum is used by
+// lane 0 of the row only.
+template <int CTRL>
+__device__ inline uint32_t dpp_u32(uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
+}
+template <int CTRL>
+__device__ inline uint64_t dpp_u64(uint64_t v) {
+    const uint32_t lo = dpp_u32<CTRL>((uint32_t)v), hi = dpp_u32<CTRL>((uint32_t)(v >> 32));
     return ((uint64_t)hi << 32) | lo;
 }
+constexpr int DPP_ROR8 = 0x128, DPP_ROR4 = 0x124, DPP_ROR2 = 0x122, DPP_ROR1 = 0x121;
+__device__ inline uint64_t row_max_u64(uint64_t v) {
+    uint64_t o;
+    o = dpp_u64<DPP_ROR8>(v); v = o > v ? o : v;
+    o = dpp_u64<DPP_ROR4>(v); v = o > v ? o : v;
+    o = dpp_u64<DPP_ROR2>(v); v = o > v ? o : v;
+    o = dpp_u64<DPP_ROR1>(v); v = o > v ? o : v;
+    return v;
+}
+__device__ inline uint64_t row_min_u64(uint64_t v) {
+    uint64_t o;
+    o = dpp_u64<DPP_ROR8>(v); v = o < v ? o : v;
+    o = dpp_u64<DPP_ROR4>(v); v = o < v ? o : v;
+    o = dpp_u64<DPP_ROR2>(v); v = o < v ? o : v;
+    o = dpp_u64<DPP_ROR1>(v); v = o < v ? o : v;
+    return v;
+}
+__device__ inline float row_sum_f32(float v) {
+    v += __uint_as_float(dpp_u32<DPP_ROR8>(__float_as_uint(v)));
+    v += __uint_as_float(dpp_u32<DPP_ROR4>(__float_as_uint(v)));
+    v += __uint_as_float(dpp_u32<DPP_ROR2>(__float_as_uint(v)));
+    v += __uint_as_float(dpp_u32<DPP_ROR1>(__float_as_uint(v)));
+    return v;
+}
 
-// Router partial logits of this block's 16 tokens over the K steps of 32 that
-// belong to this wave (steps wave, wave + 8, ...): v_mfma_f32_16x16x32_bf16
-// with the tokens as rows and 16 experts per block as columns.  U steps are
-// loaded before they are multiplied so that each wave keeps U * (1 + NB)
-// 16-byte loads in flight.
-template <int NB, int U>
-__device__ inline void router_k_loop(const RouteArgs& a, int wave, int lane, int64_t t0, f32x4* acc) {
-    const __bf16* X = (const __bf16*)a.x;
-    const __bf16* W = (const __bf16*)a.w_router;
+// Raw buffer loads: the hardware range check returns zeros for offsets at or
+// past the resource's size, so rows and experts outside the batch need no
+// branch (their offset is set to RT_OOR).
+constexpr uint32_t RT_OOR = 0x80000000u;
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+__device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+__device__ inline bf16x8 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    return __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, 0));
+}
+
+// Router partial logits of one 16-token row group (first token tr0) over the
+// K steps of 32 that belong to wave kw of the KW waves sharing the row group
+// (steps kw, kw + KW, ...): v_mfma_f32_16x16x32_bf16 with the tokens as rows
+// and 16 experts per block as columns.  The steps go in groups of U with two
+// register sets: the reads of the next group are in flight while the current
+// group is multiplied.  Steps past the end read zeros and add nothing.
+template <int NB, int U, int KW>
+__device__ inline void router_k_loop(const RouteArgs& a, int kw, int lane, int64_t tr0, f32x4* acc) {
     const int d = a.d, E = a.E;
     const int r16 = lane & 15, kg = (lane >> 4) * 8;
-    const int64_t tok = t0 + r16;
-    const bool tok_ok = tok < a.T;
-    const __bf16* xrow = X + (tok_ok ? tok : 0) * (int64_t)d + kg;
-    const __bf16* wrow[NB];
-    bool wok[NB];
+    const int64_t left = a.T - tr0;
+    const int nrows = left < 0 ? 0 : (left > 16 ? 16 : (int)left);
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc((const __bf16*)a.x + (tr0 < a.T ? tr0 : 0) * (int64_t)d,
+                                                (uint32_t)nrows * (uint32_t)d * 2u);
+    const __amdgpu_buffer_rsrc_t rw = make_rsrc(a.w_router, (uint32_t)E * (uint32_t)d * 2u);
+    const uint32_t xo = r16 < nrows ? ((uint32_t)r16 * (uint32_t)d + kg) * 2u : RT_OOR;
+    uint32_t wo[NB];
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
         const int e = nb * 16 + r16;
-        wok[nb] = e < E;
-        wrow[nb] = W + (int64_t)(wok[nb] ? e : 0) * d + kg;
+        wo[nb] = e < E ? ((uint32_t)e * (uint32_t)d + kg) * 2u : RT_OOR;
     }
-    const bf16x8 zero8 = {};
     const int nsteps = d / 32;
-    int s0 = wave;
-    for (; s0 + (U - 1) * RT_WAVES < nsteps; s0 += U * RT_WAVES) {
-        bf16x8 av[U], bv[U][NB];
+    const int ns = (nsteps - kw + KW - 1) / KW;       // steps of this wave
+    const int ngroups = (ns + U - 1) / U;
+    bf16x8 av[2][U], bv[2][U][NB];
+    auto load = [&](int buf, int grp) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int k = (s0 + u * RT_WAVES) * 32;
-            av[u] = tok_ok ? *(const bf16x8*)(xrow + k) : zero8;
+            const int i = grp * U + u;
+            const uint32_t past = i < ns ? 0u : RT_OOR;
+            const uint32_t so = (uint32_t)(kw + KW * (i < ns ? i : 0)) * 64u;   // bytes
+            av[buf][u] = buf_load16(rx, xo | past, so);
 #pragma unroll
-            for (int nb = 0; nb < NB; ++nb) bv[u][nb] = wok[nb] ? *(const bf16x8*)(wrow[nb] + k) : zero8;
+            for (int nb = 0; nb < NB; ++nb) bv[buf][u][nb] = buf_load16(rw, wo[nb] | past, so);
         }
+    };
+    auto mma = [&](int buf) {
 #pragma unroll
         for (int u = 0; u < U; ++u)
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb)
-                acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[u], bv[u][nb], acc[nb], 0, 0, 0);
-    }
-    for (; s0 < nsteps; s0 += RT_WAVES) {
-        const int k = s0 * 32;
-        const bf16x8 x8 = tok_ok ? *(const bf16x8*)(xrow + k) : zero8;
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-            const bf16x8 w8 = wok[nb] ? *(const bf16x8*)(wrow[nb] + k) : zero8;
-            acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(x8, w8, acc[nb], 0, 0, 0);
-        }
+                acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[buf][u], bv[buf][u][nb], acc[nb], 0, 0, 0);
+    };
+    load(0, 0);
+    for (int g = 0; g < ngroups; g += 2) {
+        load(1, g + 1);
+        __builtin_amdgcn_sched_barrier(0);
+        mma(0);
+        __builtin_amdgcn_sched_barrier(0);
+        load(0, g + 2);
+        __builtin_amdgcn_sched_barrier(0);
+        mma(1);
+        __builtin_amdgcn_sched_barrier(0);
     }
 }
 
-// global -> LDS copy of five arrays of 32-bit words by the block, as one
-// index space with 8 reads in flight per thread before their stores
-__device__ inline void stage_copy5(int32_t* const* dst, const int32_t* const* src, const int* len,
-                                   int tid) {
-    int end[5];
-    int tot = 0;
+// One candidate table (T1 experts, T1 losses, T1 lengths, server masks, or the
+// cost table when it is staged) copied to LDS by the block: its first
+// P * RT_THREADS words are read into registers before the router loop and
+// stored after it, so that their latency hides behind the loop; the rest is
+// copied after the loop, 4 reads in flight per thread.
+template <int P>
+__device__ inline void table_issue(const int32_t* src, int n, int tid, int32_t* v) {
 #pragma unroll
-    for (int q = 0; q < 5; ++q) { tot += len[q]; end[q] = tot; }
-    auto locate = [&](int i, int& q, int& o) {
-        q = 0;
-        o = i;
+    for (int u = 0; u < P; ++u) {
+        const int i = u * RT_THREADS + tid;
+        v[u] = i < n ? src[i] : 0;
+    }
+}
+
+template <int P>
+__device__ inline void table_store(const int32_t* src, int32_t* dst, int n, int tid, const int32_t* v) {
 #pragma unroll
-        for (int c = 0; c < 4; ++c)
-            if (i >= end[c]) { q = c + 1; o = i - end[c]; }
-    };
-    for (int i0 = 0; i0 < tot; i0 += 8 * RT_THREADS) {
-        int32_t v[8];
+    for (int u = 0; u < P; ++u) {
+        const int i = u * RT_THREADS + tid;
+        if (i < n) dst[i] = v[u];
+    }
+    for (int i0 = P * RT_THREADS + tid; i0 < n; i0 += 4 * RT_THREADS) {
+        int32_t w[4];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const int i = i0 + u * RT_THREADS + tid;
-            int q, o;
-            locate(i, q, o);
-            v[u] = i < tot ? src[q][o] : 0;
-        }
+        for (int u = 0; u < 4; ++u) w[u] = i0 + u * RT_THREADS < n ? src[i0 + u * RT_THREADS] : 0;
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const int i = i0 + u * RT_THREADS + tid;
-            int q, o;
-            locate(i, q, o);
-            if (i < tot) dst[q][o] = v[u];
-        }
+        for (int u = 0; u < 4; ++u)
+            if (i0 + u * RT_THREADS < n) dst[i0 + u * RT_THREADS] = w[u];
     }
 }
 
@@ -181,20 +232,24 @@ __global__ void __launch_bounds__(64) router_split_kernel(const RouteArgs a) {
     }
 }
 
-template <int NBT>
-__global__ void __launch_bounds__(RT_THREADS, 2)
+// up to 64 experts: at most 128 VGPRs (4 waves per SIMD), so two blocks share a CU
+template <int NBT, int TB>
+__global__ void __launch_bounds__(RT_THREADS) __attribute__((amdgpu_waves_per_eu(NBT <= 4 ? 4 : 2)))
 route_select_kernel(const RouteArgs a) {
+    constexpr int RG = TB / 16;                 // 16-token row groups of the router
+    constexpr int KW = RT_WAVES / RG;           // waves sharing one row group's K loop
+    static_assert(KW == 8 || KW == RT_SLOTS, "one or two reduction rounds");
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int64_t t0 = (int64_t)blockIdx.x * RT_TB;
+    const int64_t t0 = (int64_t)blockIdx.x * TB;
     const int E = a.E, d = a.d, k = a.k, M = a.M;
     const int Epad = (E + 15) & ~15;
 
     extern __shared__ float smem[];
-    float* s_part = smem;                               // [RT_SLOTS][RT_TB][Epad]
+    float* s_part = smem;                               // [RT_SLOTS][TB][Epad]
     float* s_logit = smem;                              // reuses slot 0 after the sum
-    int32_t* s_t1k = (int32_t*)(smem + RT_SLOTS * RT_TB * Epad);   // [E][gmax]
+    int32_t* s_t1k = (int32_t*)(smem + RT_SLOTS * TB * Epad);      // [E][gmax]
     float* s_t1q = (float*)(s_t1k + E * a.gmax);                   // [E][gmax]
     int32_t* s_t1n = (int32_t*)(s_t1q + E * a.gmax);               // [E]
     uint32_t* s_mask = (uint32_t*)(s_t1n + E);                     // [E]
@@ -202,30 +257,29 @@ route_select_kernel(const RouteArgs a) {
     float* s_S = (float*)(s_cnt + 8 + M);                          // [M][M][E] if a.S_in_lds
     const float* Stab = a.S_in_lds ? s_S : a.S;
 
-    // stage the candidate tables (small) and clear the block counters; the
-    // copies issue several reads per thread before their LDS stores
-    {
-        const int32_t* src[5] = {a.t1_k, (const int32_t*)a.t1_q, a.t1_n, (const int32_t*)a.srvmask,
-                                 (const int32_t*)a.S};
-        int32_t* dst[5] = {s_t1k, (int32_t*)s_t1q, s_t1n, (int32_t*)s_mask, (int32_t*)s_S};
-        const int len[5] = {E * a.gmax, E * a.gmax, E, E, a.S_in_lds ? M * M * E : 0};
-        stage_copy5(dst, src, len, tid);
-    }
+    // the candidate tables: reads issued now, LDS stores after the router loop
+    const int n1 = E * a.gmax, nS = a.S_in_lds ? M * M * E : 0;
+    int32_t pk[2], pq[2], pn[1], pm[1], ps[2];
+    table_issue<2>(a.t1_k, n1, tid, pk);
+    table_issue<2>((const int32_t*)a.t1_q, n1, tid, pq);
+    table_issue<1>(a.t1_n, E, tid, pn);
+    table_issue<1>((const int32_t*)a.srvmask, E, tid, pm);
+    table_issue<2>((const int32_t*)a.S, nS, tid, ps);
     for (int i = tid; i < 8 + M; i += RT_THREADS) s_cnt[i] = 0;
     // this thread's token location and budget, read before the router loop so
-    // that their latency is hidden behind it (lanes of waves 0-3 own tokens)
+    // that their latency is hidden behind it (lanes of waves 0 .. TB/4-1 own tokens)
     int loc_pre = 0;
     float qhat_pre = 0.f;
     {
         const int64_t tp = t0 + (wave * 4 + (lane >> 4));
-        if (wave < RT_TB / 4 && tp < a.T) { loc_pre = a.loc_in[tp]; qhat_pre = a.qhat_in[tp]; }
+        if (wave < TB / 4 && tp < a.T) { loc_pre = a.loc_in[tp]; qhat_pre = a.qhat_in[tp]; }
     }
 
     // ---------------- router logits ----------------
     if (a.ksplit > 0) {
         // split router: add the K slices in slice order (the reads of all
         // slices of an element are issued before the additions)
-        for (int i = tid; i < RT_TB * Epad; i += RT_THREADS) {
+        for (int i = tid; i < TB * Epad; i += RT_THREADS) {
             const int64_t tok = t0 + i / Epad;
             float pv[RT_SPLIT_MAX_K];
 #pragma unroll
@@ -239,49 +293,52 @@ route_select_kernel(const RouteArgs a) {
         }
     } else if (a.dtype == ORDERMOE_BF16) {
         const int nblk = Epad / 16;
+        const int rg = wave / KW, kw = wave % KW;
         f32x4 acc[NBT];
 #pragma unroll
         for (int i = 0; i < NBT; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-        // unroll depth: every wave keeps 9-16 loads of 16 bytes in flight, within
-        // 128 registers so that two blocks share a CU
-        if constexpr (NBT == 1) router_k_loop<1, 8>(a, wave, lane, t0, acc);
-        else if constexpr (NBT == 2) router_k_loop<2, 4>(a, wave, lane, t0, acc);
-        else if constexpr (NBT == 4) router_k_loop<4, 2>(a, wave, lane, t0, acc);
-        else if constexpr (NBT == 8) router_k_loop<8, 1>(a, wave, lane, t0, acc);
-        else router_k_loop<16, 1>(a, wave, lane, t0, acc);
-        // acc[nb][i] = partial logit of token (lane/16)*4 + i, expert nb*16 + lane%16.
-        // Two-round reduction over the 8 waves in a fixed order: waves 4-7 hand
-        // their sums to waves 0-3, then the four slots are added.
+        // group size: two groups of reads in flight per wave, within 128
+        // registers so that two blocks share a CU
+        if constexpr (NBT == 1) router_k_loop<1, 4, KW>(a, kw, lane, t0 + rg * 16, acc);
+        else if constexpr (NBT == 2) router_k_loop<2, 2, KW>(a, kw, lane, t0 + rg * 16, acc);
+        else if constexpr (NBT == 4) router_k_loop<4, 2, KW>(a, kw, lane, t0 + rg * 16, acc);
+        else if constexpr (NBT == 8) router_k_loop<8, 1, KW>(a, kw, lane, t0 + rg * 16, acc);
+        else router_k_loop<16, 1, KW>(a, kw, lane, t0 + rg * 16, acc);
+        // acc[nb][i] = partial logit of token rg*16 + (lane/16)*4 + i, expert
+        // nb*16 + lane%16.  Slots are added in a fixed order: with 8 waves per
+        // row group, waves 4-7 first hand their sums to waves 0-3.
         const int r16 = lane & 15;
-        if (wave >= RT_SLOTS) {
+        const int trow = rg * 16 + (lane >> 4) * 4;
+        if (KW == 8 && wave >= RT_SLOTS) {
 #pragma unroll
             for (int nb = 0; nb < NBT; ++nb)
                 if (nb < nblk)
 #pragma unroll
                     for (int i = 0; i < 4; ++i)
-                        s_part[((wave - RT_SLOTS) * RT_TB + (lane >> 4) * 4 + i) * Epad + nb * 16 + r16] = acc[nb][i];
+                        s_part[((wave - RT_SLOTS) * TB + trow + i) * Epad + nb * 16 + r16] = acc[nb][i];
         }
-        __syncthreads();
-        if (wave < RT_SLOTS) {
+        if (KW == 8) __syncthreads();
+        if (KW == RT_SLOTS || wave < RT_SLOTS) {
+            const int slot = KW == 8 ? wave : kw;
 #pragma unroll
             for (int nb = 0; nb < NBT; ++nb)
                 if (nb < nblk)
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        float* sp = &s_part[(wave * RT_TB + (lane >> 4) * 4 + i) * Epad + nb * 16 + r16];
-                        *sp = acc[nb][i] + *sp;
+                        float* sp = &s_part[(slot * TB + trow + i) * Epad + nb * 16 + r16];
+                        *sp = KW == 8 ? acc[nb][i] + *sp : acc[nb][i];
                     }
         }
         __syncthreads();
-        for (int i = tid; i < RT_TB * Epad; i += RT_THREADS) {
+        for (int i = tid; i < TB * Epad; i += RT_THREADS) {
             float v = s_part[i];
-            for (int w = 1; w < RT_SLOTS; ++w) v += s_part[w * RT_TB * Epad + i];
+            for (int w = 1; w < RT_SLOTS; ++w) v += s_part[w * TB * Epad + i];
             s_logit[i] = v;
         }
     } else {
         const float* X = (const float*)a.x;
         const float* W = (const float*)a.w_router;
-        for (int p = tid; p < RT_TB * Epad; p += RT_THREADS) {
+        for (int p = tid; p < TB * Epad; p += RT_THREADS) {
             const int tr = p / Epad, e = p % Epad;
             const int64_t tok = t0 + tr;
             float v = 0.f;
@@ -295,12 +352,17 @@ route_select_kernel(const RouteArgs a) {
             s_logit[p] = v;
         }
     }
+    table_store<2>(a.t1_k, s_t1k, n1, tid, pk);
+    table_store<2>((const int32_t*)a.t1_q, (int32_t*)s_t1q, n1, tid, pq);
+    table_store<1>(a.t1_n, s_t1n, E, tid, pn);
+    table_store<1>((const int32_t*)a.srvmask, (int32_t*)s_mask, E, tid, pm);
+    table_store<2>((const int32_t*)a.S, (int32_t*)s_S, nS, tid, ps);
     __syncthreads();
 
-    // ---------------- per-token stage: 16 lanes per token, waves 0-3 ----------------
-    if (wave < RT_TB / 4) {
+    // ---------------- per-token stage: 16 lanes (one DPP row) per token ----------------
+    if (wave < TB / 4) {
     const int g = lane >> 4;                 // token within the wave
-    const int j = lane & 15;                 // lane within the token group
+    const int j = lane & 15;                 // lane within the token's row
     const int tr = wave * 4 + g;             // token within the block
     const int64_t t = t0 + tr;
     const bool valid = t < a.T;
@@ -308,11 +370,10 @@ route_select_kernel(const RouteArgs a) {
 
     // top-(k+1) selection by (logit desc, index asc); this lane's logits (experts
     // j + 16 i) are read once and kept as order-preserving keys
-    constexpr int PER_LANE = ORDERMOE_MAX_EXPERTS / 16;
     const int kk1 = (k + 1 < E) ? k + 1 : E;
-    uint32_t okey[PER_LANE];
+    uint32_t okey[NBT];
 #pragma unroll
-    for (int i = 0; i < PER_LANE; ++i) okey[i] = (j + 16 * i < E) ? f2ord(lg[j + 16 * i]) : 0u;
+    for (int i = 0; i < NBT; ++i) okey[i] = (j + 16 * i < E) ? f2ord(lg[j + 16 * i]) : 0u;
     uint32_t removed = 0;                    // bit i: local element j + 16 i taken
     int sel_e[ORDERMOE_MAX_TOPK + 1];
     float sel_v[ORDERMOE_MAX_TOPK + 1];
@@ -321,17 +382,13 @@ route_select_kernel(const RouteArgs a) {
         if (r < kk1) {
             uint64_t best = 0;
 #pragma unroll
-            for (int i = 0; i < PER_LANE; ++i) {
+            for (int i = 0; i < NBT; ++i) {
                 const int e = j + 16 * i;
                 if (e >= E || (removed & (1u << i))) continue;
                 const uint64_t key = ((uint64_t)okey[i] << 32) | (uint32_t)(0xFFFFu - (uint32_t)e);
                 best = key > best ? key : best;
             }
-#pragma unroll
-            for (int off = 8; off >= 1; off >>= 1) {
-                uint64_t o = shfl_xor64(best, off);
-                best = o > best ? o : best;
-            }
+            best = row_max_u64(best);
             const int e = (int)(0xFFFFu - (uint32_t)(best & 0xFFFFu));
             sel_e[r] = e;
             sel_v[r] = ord2f((uint32_t)(best >> 32));
@@ -354,16 +411,66 @@ route_select_kernel(const RouteArgs a) {
             if (r < k) den += expf(sel_v[r] - sel_v[0]);
     } else {
         for (int e = j; e < E; e += 16) den += expf(lg[e] - sel_v[0]);
-#pragma unroll
-        for (int off = 8; off >= 1; off >>= 1) den += __shfl_xor(den, off, 16);
+        den = row_sum_f32(den);
     }
 
-    // server-expert selection, slots in rank order
+    // server-expert selection.  Lane j holds candidate j of every slot: j = 0
+    // the exact target, j >= 1 its (j-1)-th substitute in the LDS-staged table.
+    // The search does not depend on the budget, so it runs for all slots at
+    // once: each lane keeps, per slot, the smallest 64-bit key (J, position,
+    // remote, server, expert) over the servers holding its expert.  Then the
+    // slots are taken in rank order: the budget test of eq (40) masks the
+    // substitutes, a min over the row picks (m*, k*) (eq 43) and the budget is
+    // updated as eq (44).
     const int s_loc = loc_pre;
     const bool loc_ok = s_loc < M;
     float qhat = qhat_pre;
     const bool subs_on = a.allow_sub && a.Qbar > 0.f;
     const uint32_t mmask = M >= 32 ? 0xFFFFFFFFu : ((1u << M) - 1u);   // servers that exist
+    const int jm1 = j >= 1 ? j - 1 : 0;
+    int ke[ORDERMOE_MAX_TOPK];
+    float qe[ORDERMOE_MAX_TOPK];
+    uint32_t msv[ORDERMOE_MAX_TOPK];
+    uint64_t key[ORDERMOE_MAX_TOPK];
+    bool search[ORDERMOE_MAX_TOPK];
+#pragma unroll
+    for (int slot = 0; slot < ORDERMOE_MAX_TOPK; ++slot) {
+        ke[slot] = -1; qe[slot] = 0.f; msv[slot] = 0u; key[slot] = ~0ull; search[slot] = false;
+        if (slot < k) {
+            const int r = sel_e[slot];
+            const uint32_t rmask = s_mask[r];
+            const int nsub = s_t1n[r];
+            const int tk = s_t1k[r * a.gmax + jm1];
+            const float tq = s_t1q[r * a.gmax + jm1];
+            // uniform over the token's row: the reductions below read only lanes of the row
+            search[slot] = loc_ok && !(a.pin && ((rmask >> s_loc) & 1u));
+            if (j == 0) { ke[slot] = r; qe[slot] = 0.f; }
+            else if (subs_on && j - 1 < nsub) { ke[slot] = tk; qe[slot] = tq; }
+            if (ke[slot] < 0 || ke[slot] >= E) ke[slot] = -1;
+        }
+    }
+#pragma unroll
+    for (int slot = 0; slot < ORDERMOE_MAX_TOPK; ++slot)
+        if (slot < k && search[slot] && ke[slot] >= 0) msv[slot] = s_mask[ke[slot]] & mmask;
+    // servers holding each candidate, one per round for every slot together
+    for (;;) {
+        uint32_t any = 0;
+#pragma unroll
+        for (int slot = 0; slot < ORDERMOE_MAX_TOPK; ++slot) any |= msv[slot];
+        if (!__builtin_amdgcn_ballot_w64(any != 0)) break;
+#pragma unroll
+        for (int slot = 0; slot < ORDERMOE_MAX_TOPK; ++slot) {
+            if (msv[slot]) {
+                const int m = __builtin_ctz(msv[slot]);
+                msv[slot] &= msv[slot] - 1;
+                const float J = fmaf(a.cq, qe[slot], Stab[((int64_t)s_loc * M + m) * E + ke[slot]]);
+                const uint64_t cand = ((uint64_t)__float_as_uint(J) << 32) | ((uint32_t)j << 16) |
+                                      ((uint32_t)(m != s_loc) << 15) | ((uint32_t)m << 8) |
+                                      (uint32_t)ke[slot];
+                key[slot] = cand < key[slot] ? cand : key[slot];
+            }
+        }
+    }
     int first_m = s_loc, ncls[4] = {0, 0, 0, 0}, nremote = 0;
     uint32_t dstmask = 0;
 #pragma unroll
@@ -372,39 +479,15 @@ route_select_kernel(const RouteArgs a) {
         const int r = sel_e[slot];
         int km = r, mm = s_loc;
         float qsel = 0.f;
-        const uint32_t rmask = s_mask[r];
-        if (loc_ok && !(a.pin && ((rmask >> s_loc) & 1u))) {
-            // lane j holds candidate expert: j = 0 exact, j >= 1 substitute j-1
-            uint64_t key = ~0ull;
-            int ke = -1;
-            float qe = 0.f;
-            if (j == 0) { ke = r; qe = 0.f; }
-            else if (subs_on && j - 1 < s_t1n[r]) {
-                ke = s_t1k[r * a.gmax + j - 1];
-                qe = s_t1q[r * a.gmax + j - 1];
-                if (!(qhat + qe <= a.Qbar)) ke = -1;        // eq 40 budget test
-            }
-            if (ke >= 0 && ke < E) {
-                uint32_t ms = s_mask[ke] & mmask;
-                while (ms) {
-                    const int m = __builtin_ctz(ms);
-                    ms &= ms - 1;
-                    const float J = fmaf(a.cq, qe, Stab[((int64_t)s_loc * M + m) * E + ke]);
-                    const uint64_t cand = ((uint64_t)__float_as_uint(J) << 32) |
-                                          ((uint32_t)j << 6) | ((uint32_t)(m != s_loc) << 5) |
-                                          (uint32_t)m;
-                    key = cand < key ? cand : key;
-                }
-            }
-#pragma unroll
-            for (int off = 8; off >= 1; off >>= 1) {
-                uint64_t o = shfl_xor64(key, off);
-                key = o < key ? o : key;
-            }
-            const int pos = (int)((key >> 6) & 15u);
-            mm = (int)(key & 31u);
-            if (pos == 0) { km = r; qsel = 0.f; }
-            else { km = s_t1k[r * a.gmax + pos - 1]; qsel = s_t1q[r * a.gmax + pos - 1]; }
+        if (search[slot]) {
+            // eq (40): a substitute must fit the remaining budget; the exact target always does
+            uint64_t kk = (j == 0 || qhat + qe[slot] <= a.Qbar) ? key[slot] : ~0ull;
+            kk = row_min_u64(kk);
+            const int pos = (int)((kk >> 16) & 15u);
+            mm = (int)((kk >> 8) & 31u);
+            km = (int)(kk & 0xFFu);
+            // the chosen candidate's loss, from its lane (a sum of one term: exact)
+            qsel = row_sum_f32(j == pos ? qe[slot] : 0.f);
         }
         const int remote = mm != s_loc;
         const int c = (remote << 1) | (km != r);
@@ -485,12 +568,12 @@ dispatch_scan_kernel(const int32_t* blk_dst, const int64_t* blk_cnt, int nblk, i
 }
 
 __global__ void __launch_bounds__(RT_THREADS)
-dispatch_scatter_kernel(const uint8_t* exec_m, const uint8_t* loc_in, int64_t T, int k, int M,
+dispatch_scatter_kernel(const uint8_t* exec_m, const uint8_t* loc_in, int64_t T, int k, int M, int tb,
                         const int32_t* dst_base, const int32_t* dst_count, int32_t* dispatch) {
-    __shared__ int8_t s_dst[RT_TB * ORDERMOE_MAX_TOPK];
+    __shared__ int8_t s_dst[RT_TB2 * ORDERMOE_MAX_TOPK];
     const int tid = threadIdx.x;
-    const int64_t t0 = (int64_t)blockIdx.x * RT_TB;
-    const int n = RT_TB * k;
+    const int64_t t0 = (int64_t)blockIdx.x * tb;
+    const int n = tb * k;
     if (tid < n) {
         const int64_t t = t0 + tid / k;
         int dst = -1;
@@ -513,27 +596,37 @@ dispatch_scatter_kernel(const uint8_t* exec_m, const uint8_t* loc_in, int64_t T,
     }
 }
 
-template <int NBT>
+template <int NBT, int TB>
 int launch_route_kernel(const RouteArgs& a, size_t smem, hipStream_t st) {
     if (smem > 65536) {
-        hipError_t e = hipFuncSetAttribute((const void*)route_select_kernel<NBT>,
+        hipError_t e = hipFuncSetAttribute((const void*)route_select_kernel<NBT, TB>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
         if (e != hipSuccess) return (int)e;
     }
     KernelTimer kt_("route_select", st);
-    hipLaunchKernelGGL(route_select_kernel<NBT>, dim3(a.nblk), dim3(RT_THREADS), smem, st, a);
+    hipLaunchKernelGGL((route_select_kernel<NBT, TB>), dim3(a.nblk), dim3(RT_THREADS), smem, st, a);
     return (int)hipGetLastError();
+}
+
+size_t route_smem(int tb, int E, int gmax, int M, bool S_in_lds) {
+    const int Epad = (E + 15) & ~15;
+    return sizeof(float) * (size_t)RT_SLOTS * tb * Epad + (size_t)E * gmax * 8 + (size_t)E * 8 +
+           sizeof(int) * (size_t)(8 + M) + (S_in_lds ? sizeof(float) * (size_t)M * M * E : 0);
+}
+
+// the cost table is staged in LDS when it is small enough to leave room for
+// two blocks per CU, or, for batches of at most one block per CU, when it fits
+bool route_S_in_lds(int tb, int E, int gmax, int M, int nblk) {
+    const size_t b = route_smem(tb, E, gmax, M, true);
+    return b <= 64 * 1024 || (nblk <= 256 && b <= 150 * 1024);
 }
 
 }  // namespace
 
+// the workspace is sized for blocks of RT_TB tokens, the smallest block
 int route_tokens_per_block() { return RT_TB; }
 
-size_t route_smem_bytes(int E, int gmax, int M, bool S_in_lds) {
-    const int Epad = (E + 15) & ~15;
-    return sizeof(float) * (size_t)RT_SLOTS * RT_TB * Epad + (size_t)E * gmax * 8 + (size_t)E * 8 +
-           sizeof(int) * (size_t)(8 + M) + (S_in_lds ? sizeof(float) * (size_t)M * M * E : 0);
-}
+size_t route_smem_bytes(int E, int gmax, int M, bool S_in_lds) { return route_smem(RT_TB, E, gmax, M, S_in_lds); }
 
 // partial logits of the split router: at most 256 blocks of RT_TB tokens times
 // the K slices (the launcher keeps slices * blocks <= 256), every expert count
@@ -542,57 +635,64 @@ size_t route_split_buffer_floats(int64_t T) {
     return (size_t)(rows > 0 ? rows : 1) * ORDERMOE_MAX_EXPERTS;
 }
 
-// the cost table is staged in LDS when it is small enough to leave room for
-// two blocks per CU, or, for batches of at most one block per CU, when it fits
-static bool route_S_in_lds(int E, int gmax, int M, int nblk) {
-    const size_t b = route_smem_bytes(E, gmax, M, true);
-    return b <= 64 * 1024 || (nblk <= 256 && b <= 150 * 1024);
-}
-
 int launch_route_select(const RouteArgs& a, void* stream) {
     hipStream_t st = (hipStream_t)stream;
-    if (a.nblk > 0) {
-        RouteArgs b = a;
-        b.S_in_lds = route_S_in_lds(a.E, a.gmax, a.M, a.nblk) ? 1 : 0;
-        const size_t smem = route_smem_bytes(a.E, a.gmax, a.M, b.S_in_lds != 0);
+    const int nb = (a.E + 15) / 16;
+    const int nbt = nb <= 1 ? 1 : nb <= 2 ? 2 : nb <= 4 ? 4 : nb <= 8 ? 8 : 16;
+    const bool split = a.dtype == ORDERMOE_BF16 && a.T <= RT_SPLIT_MAX_T && a.logit_part;
+    // large bf16 batches (more than two blocks of 16 tokens per CU) of at most 64
+    // experts take blocks of 32 tokens: the router weights are read half as often
+    // and all 8 waves run the token stage
+    const int64_t nb16 = (a.T + RT_TB - 1) / RT_TB;
+    const int tb = (a.dtype == ORDERMOE_BF16 && !split && nbt <= 4 && nb16 > 512) ? RT_TB2 : RT_TB;
+    RouteArgs b = a;
+    b.nblk = (int)((a.T + tb - 1) / tb);
+    if (b.nblk > 0) {
+        b.S_in_lds = route_S_in_lds(tb, a.E, a.gmax, a.M, b.nblk) ? 1 : 0;
+        const size_t smem = route_smem(tb, a.E, a.gmax, a.M, b.S_in_lds != 0);
         b.ksplit = 0;
-        if (a.dtype == ORDERMOE_BF16 && a.T <= RT_SPLIT_MAX_T && a.logit_part) {
+        if (split) {
             // enough waves to cover the CUs, K slices a multiple of 32
-            const int nbe = (a.E + 15) / 16;
-            int ks = 256 / (a.nblk * nbe);
+            int ks = 256 / (b.nblk * nb);
             ks = ks < 1 ? 1 : (ks > RT_SPLIT_MAX_K ? RT_SPLIT_MAX_K : ks);
             while (ks > 1 && a.d % (32 * ks) != 0) --ks;
             b.ksplit = ks;
             KernelTimer kt_("router_split", st);
-            router_split_kernel<<<dim3((unsigned)a.nblk, (unsigned)nbe, (unsigned)ks), dim3(64), 0, st>>>(b);
+            router_split_kernel<<<dim3((unsigned)b.nblk, (unsigned)nb, (unsigned)ks), dim3(64), 0, st>>>(b);
             hipError_t e = hipGetLastError();
             if (e != hipSuccess) return (int)e;
         }
-        const int nb = (a.E + 15) / 16;
-        const int nbt = nb <= 1 ? 1 : nb <= 2 ? 2 : nb <= 4 ? 4 : nb <= 8 ? 8 : 16;
         int e = 0;
-        switch (nbt) {
-            case 1: e = launch_route_kernel<1>(b, smem, st); break;
-            case 2: e = launch_route_kernel<2>(b, smem, st); break;
-            case 4: e = launch_route_kernel<4>(b, smem, st); break;
-            case 8: e = launch_route_kernel<8>(b, smem, st); break;
-            default: e = launch_route_kernel<16>(b, smem, st); break;
+        if (tb == RT_TB2) {
+            switch (nbt) {
+                case 1: e = launch_route_kernel<1, RT_TB2>(b, smem, st); break;
+                case 2: e = launch_route_kernel<2, RT_TB2>(b, smem, st); break;
+                default: e = launch_route_kernel<4, RT_TB2>(b, smem, st); break;
+            }
+        } else {
+            switch (nbt) {
+                case 1: e = launch_route_kernel<1, RT_TB>(b, smem, st); break;
+                case 2: e = launch_route_kernel<2, RT_TB>(b, smem, st); break;
+                case 4: e = launch_route_kernel<4, RT_TB>(b, smem, st); break;
+                case 8: e = launch_route_kernel<8, RT_TB>(b, smem, st); break;
+                default: e = launch_route_kernel<16, RT_TB>(b, smem, st); break;
+            }
         }
         if (e) return e;
     }
     {
         KernelTimer kt_("dispatch_scan", st);
-        hipLaunchKernelGGL(dispatch_scan_kernel, dim3(1), dim3(SCAN_THREADS), 0, st, a.blk_dst,
-                       a.blk_cnt, a.nblk, a.M, a.dst_base, a.out.dst_count, a.out.counters);
-        }
+        hipLaunchKernelGGL(dispatch_scan_kernel, dim3(1), dim3(SCAN_THREADS), 0, st, b.blk_dst,
+                           b.blk_cnt, b.nblk, b.M, b.dst_base, b.out.dst_count, b.out.counters);
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return (int)e;
-    if (a.nblk > 0) {
+    if (b.nblk > 0) {
         {
-        KernelTimer kt_("dispatch_scatter", st);
-        hipLaunchKernelGGL(dispatch_scatter_kernel, dim3(a.nblk), dim3(RT_THREADS), 0, st,
-                           a.out.exec_m, a.loc_in, a.T, a.k, a.M, a.dst_base, a.out.dst_count,
-                           a.out.dispatch);
+            KernelTimer kt_("dispatch_scatter", st);
+            hipLaunchKernelGGL(dispatch_scatter_kernel, dim3(b.nblk), dim3(RT_THREADS), 0, st,
+                               b.out.exec_m, b.loc_in, b.T, b.k, b.M, tb, b.dst_base, b.out.dst_count,
+                               b.out.dispatch);
         }
         e = hipGetLastError();
         if (e != hipSuccess) return (int)e;
