@@ -535,17 +535,25 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
 // workgroup computes 32 rows x 64 weight rows (a gate/up granule pair, or 64
 // output columns of the down projection) over the whole K.  Its 4 waves take
 // interleaved K steps of 64 (wave w: steps w, w+4, ...), so the workgroup
-// streams 512 contiguous bytes of each weight row per round.  Operands go from
-// global memory straight into MFMA registers in the v_mfma_f32_32x32x16_bf16
-// layout (lane: row lane%32, K elements 8*(lane/32) .. +7 of each 16), the
-// next step's reads issued before the current step's MFMAs.  The waves'
-// partial sums meet in LDS and are added in wave order, then the epilogue of
-// ggemm_bf16 runs on the sums.
+// streams 512 contiguous bytes of each weight row per round.  The weight rows
+// are read coalesced (a wave instruction covers 8 rows x 128 bytes, whole cache
+// lines) into registers, passed through the wave's own LDS rows (padded by 16
+// bytes) into the v_mfma_f32_32x32x16_bf16 layout (lane: row lane%32, K
+// elements 8*(lane/32) .. +7 of each 16); the activation rows go from global
+// memory straight into MFMA registers.  Two register sets keep the next step's
+// reads in flight during the current step.  The waves' partial sums meet in LDS
+// and are added in wave order, then the epilogue of ggemm_bf16 runs on the
+// sums.
 constexpr int TH_BM = 32, TH_BN = 64, TH_WAVES = 4;
+constexpr int TH_LDK = 144;                        // bytes per staged weight row
+constexpr int TH_LDS = TH_WAVES * TH_BN * TH_LDK;  // staging; reused for the partial sums
 
 template <int MODE>
-__global__ void __launch_bounds__(256, 2) ggemm_thin(const GemmArgs p) {
-    __shared__ float red[TH_WAVES][2][16][64];
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3)))
+ggemm_thin(const GemmArgs p) {
+    __shared__ __attribute__((aligned(16))) char th_lds[TH_LDS];
+    static_assert(sizeof(float) * TH_WAVES * 2 * 16 * 64 <= TH_LDS, "partial sums fit the staging rows");
+    float (*red)[2][16][64] = (float (*)[2][16][64])th_lds;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: K offsets go in SGPRs
     const int c = lane & 31, h = lane >> 5;
@@ -562,8 +570,12 @@ __global__ void __launch_bounds__(256, 2) ggemm_thin(const GemmArgs p) {
         const __bf16* Bw = shared ? (const __bf16*)p.Ws
                                   : (const __bf16*)p.Wr + (size_t)L.g * L.N * K;
         const __amdgpu_buffer_rsrc_t rb_rs = make_rsrc(Bw, (uint32_t)((size_t)L.N * K * 2));
-        const uint32_t boff0 = ((uint32_t)(L.n0 + c) * (uint32_t)K + 8u * h) * 2u;
-        const uint32_t boff1 = boff0 + 64u * (uint32_t)K;          // 32 rows further
+        // weight reads: lane l takes row 8i + l/8, 16-byte chunk l%8 of the step's 128 bytes
+        const uint32_t wrow0 = ((uint32_t)(L.n0 + (lane >> 3)) * (uint32_t)K + 8u * (lane & 7)) * 2u;
+        const uint32_t wstride8 = 16u * (uint32_t)K;                 // 8 rows, in bytes
+        char* stg = th_lds + wave * (TH_BN * TH_LDK);
+        char* wdst = stg + (lane >> 3) * TH_LDK + (lane & 7) * 16;
+        const char* frag = stg + c * TH_LDK + h * 16;                  // row c, chunk 2i + h
         const int row = L.m0 + c;
         __amdgpu_buffer_rsrc_t ra_rs;
         uint32_t aoff;
@@ -581,30 +593,33 @@ __global__ void __launch_bounds__(256, 2) ggemm_thin(const GemmArgs p) {
         f32x16 acc0, acc1;
 #pragma unroll
         for (int e = 0; e < 16; ++e) { acc0[e] = 0.f; acc1[e] = 0.f; }
-        bf16x8 a[2][4], b0[2][4], b1[2][4];
+        bf16x8 w[2][8], a[2][4];
         auto load = [&](int buf, int it) {
             const int st = wave + it * TH_WAVES;
-            // a step past the end reads zeros through the range check and is never used
+            // a step past the end reads zeros through the range check and adds nothing
             const uint32_t ok = it < nst ? 0u : OOR;
             const uint32_t k0 = (uint32_t)st * 128u;   // bytes
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const uint32_t so = k0 + 32u * i;
-                b0[buf][i] = buf_load16(rb_rs, boff0 | ok, so);
-                b1[buf][i] = buf_load16(rb_rs, boff1 | ok, so);
-                a[buf][i] = buf_load16(ra_rs, aoff | ok, so);
-            }
+            for (int i = 0; i < 8; ++i) w[buf][i] = buf_load16(rb_rs, (wrow0 + i * wstride8) | ok, k0);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) a[buf][i] = buf_load16(ra_rs, aoff | ok, k0 + 32u * i);
         };
         auto mma = [&](int buf) {
+            // the wave's own LDS rows: stores, then fragment reads, in program order
+#pragma unroll
+            for (int i = 0; i < 8; ++i) *(bf16x8*)(wdst + i * 8 * TH_LDK) = w[buf][i];
+            bf16x8 b0[4], b1[4];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[buf][i], b0[buf][i], acc0, 0, 0, 0);
-                acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[buf][i], b1[buf][i], acc1, 0, 0, 0);
+                b0[i] = *(const bf16x8*)(frag + i * 32);
+                b1[i] = *(const bf16x8*)(frag + 32 * TH_LDK + i * 32);
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[buf][i], b0[i], acc0, 0, 0, 0);
+                acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[buf][i], b1[i], acc1, 0, 0, 0);
             }
         };
-        // two register sets, one step of reads always in flight; fences keep
-        // the reads ahead of the MFMAs.  With an odd step count the last mma(1)
-        // multiplies zeros read past the end, which leaves the sums unchanged.
         load(0, 0);
         for (int it = 0; it < nst; it += 2) {
             load(1, it + 1);
@@ -616,7 +631,7 @@ __global__ void __launch_bounds__(256, 2) ggemm_thin(const GemmArgs p) {
             mma(1);
             __builtin_amdgcn_sched_barrier(0);
         }
-
+        __syncthreads();     // every wave is done with its staging rows
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
             red[wave][0][e][lane] = acc0[e];
