@@ -44,7 +44,9 @@ constexpr int ST_BK = 64, ST_LDK = ST_BK + 8;
 constexpr int ST_STAGES = 4;               // K steps of reads in flight per wave
 constexpr int ST_LDH = SIM_EMAX + 4;       // row stride of the parked H tile (floats)
 constexpr int ST_LDT = ST_BM + 8;          // row stride of the h / l planes of H^T (bf16)
-constexpr size_t ST_LDS_KLOOP = (size_t)2 * SIM_EMAX * ST_LDK * 2;
+constexpr int ST_LDA = 144;                // bytes per staged token row (64 bf16 + 16)
+constexpr size_t ST_LDS_A = (size_t)ST_BM * ST_LDA;      // token staging, 32 rows per wave
+constexpr size_t ST_LDS_KLOOP = (size_t)2 * SIM_EMAX * ST_LDK * 2 + ST_LDS_A;
 constexpr size_t ST_LDS_H = (size_t)ST_BM * ST_LDH * 4;
 constexpr size_t ST_LDS_HL = (size_t)2 * SIM_EMAX * ST_LDT * 2;
 constexpr size_t ST_LDS_MAX2 = ST_LDS_KLOOP > ST_LDS_H ? ST_LDS_KLOOP : ST_LDS_H;
@@ -57,10 +59,12 @@ __device__ inline bf16x8 st_load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint
 
 // One workgroup per tile of 256 calibration tokens; wave w owns tokens
 // 32w .. 32w+31 against all 128 experts (4 blocks of 32x32).  The tokens are
-// streamed from HBM once, straight into MFMA operand registers (lane: token
-// lane%32, K elements 8*(lane/32) .. +7 of each 16); the router rows W_r (L2
-// resident) go through a double-buffered LDS tile shared by the waves.  The
-// reads of a K step are issued ST_STAGES steps ahead.  After the K loop the
+// streamed from HBM once: a wave reads its 32 token rows coalesced (an
+// instruction covers 8 rows x 128 bytes, whole cache lines) into registers,
+// then passes them through its own padded LDS rows into the MFMA operand
+// layout (lane: token lane%32, K elements 8*(lane/32) .. +7 of each 16); the
+// router rows W_r (L2 resident) go through a double-buffered LDS tile shared by
+// the waves.  The reads of a K step are issued ST_STAGES steps ahead.  After the K loop the
 // fp32 H tile is parked in LDS for the top-k counts, then replaced by the bf16
 // h / l planes of H^T for the Gram update; the Gram partial of a workgroup
 // lives in its workspace slot.
@@ -85,6 +89,10 @@ __global__ void __launch_bounds__(ST_THREADS, 1) sim_tile_kernel(const SimArgs a
     const uint32_t boff0 = ((uint32_t)lrow * (uint32_t)d + lch) * 2u;
     const uint32_t bstride = 128u * (uint32_t)d;        // 64 rows, in bytes
     const int brow_off = (lane & 31) * LDK + (lane >> 5) * 8;
+    // this wave's token staging rows, after the W buffers
+    char* astg = lds_raw + (size_t)2 * BN * LDK * 2 + (size_t)wave * 32 * ST_LDA;
+    char* adst = astg + (lane >> 3) * ST_LDA + (lane & 7) * 16;
+    const char* afrag = astg + (lane & 31) * ST_LDA + (lane >> 5) * 16;   // row lane%32, chunk 2ks + h
     constexpr uint32_t OOR = 0x80000000u;
     float* gp = a.gram_part + (int64_t)blockIdx.x * SIM_EMAX * SIM_EMAX;
     bool first_tile = true;
@@ -97,7 +105,9 @@ __global__ void __launch_bounds__(ST_THREADS, 1) sim_tile_kernel(const SimArgs a
         // this tile's tokens only: rows past the end read zeros through the range check
         const __amdgpu_buffer_rsrc_t ra_rs = __builtin_amdgcn_make_buffer_rsrc(
             const_cast<__bf16*>((const __bf16*)a.x_cal + t0 * d), (short)0, nt * d * 2, 0x00020000);
-        const uint32_t aoff = ((uint32_t)(wave * 32 + (lane & 31)) * (uint32_t)d + 8u * (lane >> 5)) * 2u;
+        // token reads: lane l takes row 8i + l/8 of the wave's 32, 16-byte chunk l%8 of the step
+        const uint32_t aoff = ((uint32_t)(wave * 32 + (lane >> 3)) * (uint32_t)d + 8u * (lane & 7)) * 2u;
+        const uint32_t astride8 = 16u * (uint32_t)d;    // 8 rows, in bytes
 
         f32x16 acc[FN];
 #pragma unroll
@@ -110,7 +120,7 @@ __global__ void __launch_bounds__(ST_THREADS, 1) sim_tile_kernel(const SimArgs a
             const uint32_t ok = step < KT ? 0u : OOR;    // past the end: zeros, never used
             const uint32_t k0 = (uint32_t)step * BK * 2u;
 #pragma unroll
-            for (int ks = 0; ks < 4; ++ks) ax[st][ks] = st_load16(ra_rs, aoff | ok, k0 + 32u * ks);
+            for (int i = 0; i < 4; ++i) ax[st][i] = st_load16(ra_rs, (aoff + i * astride8) | ok, k0);
         };
         auto loadB = [&](int st, int step) {
             const uint32_t ok = step < KT ? 0u : OOR;
@@ -125,13 +135,19 @@ __global__ void __launch_bounds__(ST_THREADS, 1) sim_tile_kernel(const SimArgs a
         };
         auto mma = [&](int st, int buf) {
             const __bf16* pb = sB + buf * BN * LDK + brow_off;
+            // the wave's own token rows: stores, then fragment reads, in program order
+#pragma unroll
+            for (int i = 0; i < 4; ++i) *(bf16x8*)(adst + i * 8 * ST_LDA) = ax[st][i];
+            bf16x8 af[4];
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks) af[ks] = *(const bf16x8*)(afrag + ks * 32);
 #pragma unroll
             for (int ks = 0; ks < 4; ++ks) {
 #pragma unroll
                 for (int j = 0; j < FN; ++j) bfr[j] = *(const bf16x8*)(pb + j * 32 * LDK + ks * 16);
 #pragma unroll
                 for (int j = 0; j < FN; ++j)
-                    acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ax[st][ks], bfr[j], acc[j], 0, 0, 0);
+                    acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[ks], bfr[j], acc[j], 0, 0, 0);
             }
         };
         // The reads of one K step (tokens, then W rows) form a batch issued S
