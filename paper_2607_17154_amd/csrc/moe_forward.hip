@@ -9,6 +9,8 @@
 //                        offsets, tile counts of the two GEMMs
 //   rows_scatter_kernel  stable placement of every row (token order inside a
 //                        group), merged gate weight, token -> rows map
+//   rows_small_kernel    the three row kernels as one block (batches of at
+//                        most 1024 tokens)
 //   ggemm_bf16<.., 0>    gate/up projection, X rows gathered through row_tok,
 //                        packed [2f][d] weights, epilogue silu(g) * u -> bf16
 //   ggemm_bf16<.., 1>    down projection of the activations, epilogue scales
@@ -64,18 +66,18 @@ __device__ inline int token_rows(const RowsArgs& a, const int32_t* s_lidx, int64
                                  float* wsum) {
     int m[ORDERMOE_MAX_TOPK], ek[ORDERMOE_MAX_TOPK];
     float wv[ORDERMOE_MAX_TOPK];
+    // all slot reads issued together: unused slots re-read the last slot (in
+    // range) and are discarded, so no branch separates the reads
 #pragma unroll
     for (int s = 0; s < ORDERMOE_MAX_TOPK; ++s) {
-        m[s] = -1;
-        ek[s] = -1;
-        wv[s] = 0.f;
-        if (s < a.k) {
-            const int64_t o = t * a.k + s;
-            m[s] = a.exec_m[o];
-            ek[s] = a.exec_k[o];
-            wv[s] = a.w[o];
-        }
+        const int64_t o = t * a.k + (s < a.k ? s : a.k - 1);
+        m[s] = a.exec_m[o];
+        ek[s] = a.exec_k[o];
+        wv[s] = a.w[o];
     }
+#pragma unroll
+    for (int s = 0; s < ORDERMOE_MAX_TOPK; ++s)
+        if (s >= a.k) { m[s] = -1; ek[s] = -1; wv[s] = 0.f; }
     const int loc = a.has_shared ? (int)a.loc_in[t] : -1;
 #pragma unroll
     for (int q = 0; q < MAXR; ++q) { grp[q] = -1; wsum[q] = 0.f; }
@@ -104,6 +106,26 @@ __device__ inline int token_rows(const RowsArgs& a, const int32_t* s_lidx, int64
         ++n;
     }
     return n;
+}
+
+// Ranks of a wave's rows inside their groups (token order): each lane ORs its
+// bit into the 64-bit lane mask of every group it has a row in (LDS atomics),
+// then a row's rank is the number of lower lanes in its group's mask.  The
+// wave's LDS operations run in program order, so the reads see every OR.  Also
+// writes the wave's row count of every group to wcnt[0 .. G).
+__device__ inline void wave_group_ranks(unsigned long long* msk, int G, int lane, const int* grp, int n,
+                                        int* rank, int32_t* wcnt) {
+    for (int g = lane; g < G; g += 64) msk[g] = 0ull;
+    const unsigned long long bit = 1ull << lane;
+#pragma unroll
+    for (int q = 0; q < MAXR; ++q)
+        if (q < n) atomicOr(&msk[grp[q]], bit);
+#pragma unroll
+    for (int q = 0; q < MAXR; ++q) {
+        rank[q] = 0;
+        if (q < n) rank[q] = __popcll(msk[grp[q]] & (bit - 1ull));
+    }
+    for (int g = lane; g < G; g += 64) wcnt[g] = __popcll(msk[g]);
 }
 
 __global__ void __launch_bounds__(FT_TB) rows_count_kernel(const RowsArgs a) {
@@ -193,6 +215,7 @@ __global__ void __launch_bounds__(SCAN_THREADS) rows_scan_kernel(const RowsArgs 
 __global__ void __launch_bounds__(FT_TB) rows_scatter_kernel(const RowsArgs a) {
     __shared__ int32_t s_lidx[ORDERMOE_MAX_EXPERTS];
     __shared__ int32_t s_wcnt[FT_TB / 64][MAXG];
+    __shared__ unsigned long long s_msk[FT_TB / 64][MAXG];
     __shared__ int32_t s_first[MAXG];        // first row of this block in each group
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int G = a.n_local + a.has_shared;
@@ -209,19 +232,86 @@ __global__ void __launch_bounds__(FT_TB) rows_scatter_kernel(const RowsArgs a) {
 #pragma unroll
         for (int q = 0; q < MAXR; ++q) { grp[q] = -1; ws[q] = 0.f; }
     }
+    wave_group_ranks(s_msk[wave], G, lane, grp, n, rank, s_wcnt[wave]);
+    __syncthreads();
+    if (t < a.T) {
+        const int stride = a.k + 1;
 #pragma unroll
-    for (int q = 0; q < MAXR; ++q) rank[q] = 0;
-    for (int g = 0; g < G; ++g) {
-        int has = -1;
+        for (int q = 0; q < MAXR; ++q) {
+            if (q < n) {
+                const int g = grp[q];
+                int32_t pos = s_first[g] + rank[q];
+                for (int w = 0; w < wave; ++w) pos += s_wcnt[w][g];
+                a.row_tok[pos] = (int32_t)t;
+                a.row_w[pos] = ws[q];
+                a.tok_rows[t * stride + q] = pos;
+            } else if (q < stride) {
+                a.tok_rows[t * stride + q] = -1;
+            }
+        }
+    }
+}
+
+// Batches of at most SCAN_THREADS tokens (decode): the three row kernels as one
+// block, one token per thread -- group ranks by wave lane masks, group totals,
+// row offsets and tile counts (as rows_scan_kernel), then the placement (as
+// rows_scatter_kernel).
+__global__ void __launch_bounds__(SCAN_THREADS) rows_small_kernel(const RowsArgs a) {
+    __shared__ int32_t s_lidx[ORDERMOE_MAX_EXPERTS];
+    __shared__ int32_t s_wcnt[SCAN_WAVES][MAXG];
+    __shared__ unsigned long long s_msk[SCAN_WAVES][MAXG];
+    __shared__ int32_t s_first[MAXG];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int G = a.n_local + a.has_shared;
+    for (int i = tid; i < a.E; i += SCAN_THREADS) s_lidx[i] = a.lidx[i];
+    __syncthreads();
+    const int64_t t = tid;
+    int grp[MAXR], rank[MAXR];
+    float ws[MAXR];
+    int n = 0;
+    if (t < a.T) {
+        n = token_rows(a, s_lidx, t, grp, ws);
+    } else {
 #pragma unroll
-        for (int q = 0; q < MAXR; ++q)
-            if (q < n && grp[q] == g) has = q;
-        const uint64_t bal = __ballot(has >= 0);
-        if (lane == 0) s_wcnt[wave][g] = __popcll(bal);
-        const int r = __popcll(bal & ((1ull << lane) - 1ull));
-#pragma unroll
-        for (int q = 0; q < MAXR; ++q)
-            if (q == has) rank[q] = r;
+        for (int q = 0; q < MAXR; ++q) { grp[q] = -1; ws[q] = 0.f; }
+    }
+    wave_group_ranks(s_msk[wave], G, lane, grp, n, rank, s_wcnt[wave]);
+    __syncthreads();
+    if (wave == 0) {
+        int32_t base = 0;
+        int64_t tiles_gu = 0, tiles_dn = 0;
+        for (int g0 = 0; g0 <= a.n_local; g0 += 64) {
+            const int g = g0 + lane;
+            int32_t R = 0;
+            if (g < G)
+                for (int w = 0; w < SCAN_WAVES; ++w) R += s_wcnt[w][g];
+            int32_t inc = R;
+            for (int off = 1; off < 64; off <<= 1) {
+                const int32_t o = __shfl_up(inc, off);
+                if (lane >= off) inc += o;
+            }
+            if (g <= a.n_local) { a.row_offsets[g] = base + inc - R; s_first[g] = base + inc - R; }
+            int64_t tg = 0, td = 0;
+            if (g < G) {
+                const bool sh = g == a.n_local;
+                tg = (int64_t)((R + a.bm_gu - 1) / a.bm_gu) * ((sh ? a.n_gu_s : a.n_gu_r) / a.bn_gu);
+                td = (int64_t)((R + a.bm_dn - 1) / a.bm_dn) * (a.n_dn / a.bn_dn);
+            }
+            for (int off = 32; off >= 1; off >>= 1) {
+                tg += __shfl_xor(tg, off);
+                td += __shfl_xor(td, off);
+            }
+            tiles_gu += tg;
+            tiles_dn += td;
+            base += __shfl(inc, 63);
+        }
+        if (lane == 0) {
+            a.row_offsets[a.n_local + 1] = base;
+            a.tile_info[0] = (int32_t)tiles_gu;
+            a.tile_info[1] = (int32_t)tiles_dn;
+            a.tile_info[2] = base;
+            a.tile_info[3] = 0;
+        }
     }
     __syncthreads();
     if (t < a.T) {
@@ -860,24 +950,30 @@ int launch_local_forward(const ForwardArgs& f, void* stream) {
     r.n_gu_r = 2 * f.f; r.n_gu_s = 2 * f.n_shared * f.f; r.n_dn = f.d;
 
     hipError_t e;
-    if (f.nblk > 0) {
+    if (f.T <= SCAN_THREADS) {
         {
-        KernelTimer kt_("rows_count", st);
-        hipLaunchKernelGGL(rows_count_kernel, dim3(f.nblk), dim3(FT_TB), 0, st, r);
+            KernelTimer kt_("rows_small", st);
+            hipLaunchKernelGGL(rows_small_kernel, dim3(1), dim3(SCAN_THREADS), 0, st, r);
+        }
+        if ((e = hipGetLastError()) != hipSuccess) return (int)e;
+        if (f.nblk == 0) return 0;
+    } else {
+        {
+            KernelTimer kt_("rows_count", st);
+            hipLaunchKernelGGL(rows_count_kernel, dim3(f.nblk), dim3(FT_TB), 0, st, r);
+        }
+        if ((e = hipGetLastError()) != hipSuccess) return (int)e;
+        {
+            KernelTimer kt_("rows_scan", st);
+            hipLaunchKernelGGL(rows_scan_kernel, dim3(1), dim3(SCAN_THREADS), 0, st, r);
+        }
+        if ((e = hipGetLastError()) != hipSuccess) return (int)e;
+        {
+            KernelTimer kt_("rows_scatter", st);
+            hipLaunchKernelGGL(rows_scatter_kernel, dim3(f.nblk), dim3(FT_TB), 0, st, r);
         }
         if ((e = hipGetLastError()) != hipSuccess) return (int)e;
     }
-    {
-        KernelTimer kt_("rows_scan", st);
-        hipLaunchKernelGGL(rows_scan_kernel, dim3(1), dim3(SCAN_THREADS), 0, st, r);
-        }
-    if ((e = hipGetLastError()) != hipSuccess) return (int)e;
-    if (f.nblk == 0) return 0;
-    {
-        KernelTimer kt_("rows_scatter", st);
-        hipLaunchKernelGGL(rows_scatter_kernel, dim3(f.nblk), dim3(FT_TB), 0, st, r);
-        }
-    if ((e = hipGetLastError()) != hipSuccess) return (int)e;
 
     GemmArgs g{};
     g.offsets = f.row_offsets; g.G = G; g.n_routed = f.n_local;

@@ -23,6 +23,8 @@
 // Kernel 3 (dispatch_scatter_kernel), one block per TB tokens: stable
 //   placement of the block's remote slots into the (destination, token, slot)
 //   ordered dispatch list.
+// Batches of at most 1024 slots run kernels 2 and 3 as one single-block
+// kernel (dispatch_small_kernel).
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -166,10 +168,13 @@ __device__ inline void router_k_loop(const RouteArgs& a, int kw, int lane, int64
 // copied after the loop, 4 reads in flight per thread.
 template <int P>
 __device__ inline void table_issue(const int32_t* src, int n, int tid, int32_t* v) {
+    // reads past the table re-read its first word (discarded), so that no
+    // branch separates the reads; an empty table reads nothing
+    if (n <= 0) return;
 #pragma unroll
     for (int u = 0; u < P; ++u) {
         const int i = u * RT_THREADS + tid;
-        v[u] = i < n ? src[i] : 0;
+        v[u] = src[i < n ? i : 0];
     }
 }
 
@@ -596,6 +601,59 @@ dispatch_scatter_kernel(const uint8_t* exec_m, const uint8_t* loc_in, int64_t T,
     }
 }
 
+// Batches of at most DS_THREADS slots (decode): the dispatch list in one block,
+// one slot per thread -- totals of the routing blocks' counters, each slot's
+// rank among its wave's slots to the same destination (ballots), destination
+// totals and segment starts, placement.  Replaces the scan and scatter kernels.
+constexpr int DS_THREADS = 1024;
+constexpr int DS_WAVES = DS_THREADS / 64;
+
+__global__ void __launch_bounds__(DS_THREADS)
+dispatch_small_kernel(const int64_t* blk_cnt, int nblk, const uint8_t* exec_m, const uint8_t* loc_in,
+                      int64_t T, int k, int M, int32_t* dst_count, int64_t* counters, int32_t* dispatch) {
+    __shared__ int32_t s_wcnt[DS_WAVES][ORDERMOE_MAX_SERVERS];
+    __shared__ int32_t s_tot[ORDERMOE_MAX_SERVERS];
+    __shared__ int32_t s_start[ORDERMOE_MAX_SERVERS];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    if (wave < 8) {
+        int64_t v = 0;
+        for (int b = lane; b < nblk; b += 64) v += blk_cnt[(int64_t)b * 8 + wave];
+        for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+        if (lane == 0) counters[wave] = v;
+    }
+    const int n = (int)(T * k);
+    int dst = -1;
+    if (tid < n) {
+        const int s = loc_in[tid / k];
+        const int m = exec_m[tid];
+        if (s < M && m != s) dst = m;
+    }
+    int rank = 0;
+    for (int m = 0; m < M; ++m) {
+        const uint64_t bal = __ballot(dst == m);
+        if (lane == 0) s_wcnt[wave][m] = __popcll(bal);
+        if (dst == m) rank = __popcll(bal & ((1ull << lane) - 1ull));
+    }
+    __syncthreads();
+    if (tid < M) {
+        int32_t tot = 0;
+        for (int w = 0; w < DS_WAVES; ++w) tot += s_wcnt[w][tid];
+        s_tot[tid] = tot;
+        dst_count[tid] = tot;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        int32_t acc = 0;
+        for (int m = 0; m < M; ++m) { s_start[m] = acc; acc += s_tot[m]; }
+    }
+    __syncthreads();
+    if (dst >= 0) {
+        int32_t pos = s_start[dst] + rank;
+        for (int w = 0; w < wave; ++w) pos += s_wcnt[w][dst];
+        dispatch[pos] = tid;                      // slot index token * k + slot
+    }
+}
+
 template <int NBT, int TB>
 int launch_route_kernel(const RouteArgs& a, size_t smem, hipStream_t st) {
     if (smem > 65536) {
@@ -680,12 +738,20 @@ int launch_route_select(const RouteArgs& a, void* stream) {
         }
         if (e) return e;
     }
+    hipError_t e;
+    if (b.T * b.k <= DS_THREADS) {
+        KernelTimer kt_("dispatch_small", st);
+        hipLaunchKernelGGL(dispatch_small_kernel, dim3(1), dim3(DS_THREADS), 0, st, b.blk_cnt, b.nblk,
+                           b.out.exec_m, b.loc_in, b.T, b.k, b.M, b.out.dst_count, b.out.counters,
+                           b.out.dispatch);
+        return (int)hipGetLastError();
+    }
     {
         KernelTimer kt_("dispatch_scan", st);
         hipLaunchKernelGGL(dispatch_scan_kernel, dim3(1), dim3(SCAN_THREADS), 0, st, b.blk_dst,
                            b.blk_cnt, b.nblk, b.M, b.dst_base, b.out.dst_count, b.out.counters);
     }
-    hipError_t e = hipGetLastError();
+    e = hipGetLastError();
     if (e != hipSuccess) return (int)e;
     if (b.nblk > 0) {
         {
