@@ -4,7 +4,7 @@
 // or 32 for large batches of at most 64 experts):
 //   * the first words of the candidate tables are read into registers first,
 //     so that their latency hides behind the router loop, and stored to LDS
-//     after it;
+//     after it together with the rest;
 //   * router logits l = x W_r^T (eq 3, one token at a time):
 //       bf16: v_mfma_f32_16x16x32_bf16 on 16-token row groups, the K steps of a
 //             row group split over its waves, partial sums added in wave order;
@@ -162,35 +162,40 @@ __device__ inline void router_k_loop(const RouteArgs& a, int kw, int lane, int64
 }
 
 // One candidate table (T1 experts, T1 losses, T1 lengths, server masks, or the
-// cost table when it is staged) copied to LDS by the block: its first
-// P * RT_THREADS words are read into registers before the router loop and
-// stored after it, so that their latency hides behind the loop; the rest is
-// copied after the loop, 4 reads in flight per thread.
-template <int P>
-__device__ inline void table_issue(const int32_t* src, int n, int tid, int32_t* v) {
-    // reads past the table re-read its first word (discarded), so that no
-    // branch separates the reads; an empty table reads nothing
-    if (n <= 0) return;
+// cost table when it is staged) copied to LDS by the block in batches of whole
+// block rounds: words [B * RT_THREADS, (B + P) * RT_THREADS) are read into P
+// registers per thread (reads past the table re-read word 0 and are
+// discarded, so no branch separates them) and stored later.  The first batch
+// is read before the router loop, so that its latency hides behind the loop;
+// the second batches of all tables are read together after it; whatever is
+// left is copied by table_copy_from.
+template <int B, int P>
+__device__ inline void table_read(const int32_t* src, int n, int tid, int32_t* v) {
+    if (n <= B * RT_THREADS) return;
 #pragma unroll
     for (int u = 0; u < P; ++u) {
-        const int i = u * RT_THREADS + tid;
+        const int i = (B + u) * RT_THREADS + tid;
         v[u] = src[i < n ? i : 0];
     }
 }
 
-template <int P>
-__device__ inline void table_store(const int32_t* src, int32_t* dst, int n, int tid, const int32_t* v) {
+template <int B, int P>
+__device__ inline void table_write(int32_t* dst, int n, int tid, const int32_t* v) {
 #pragma unroll
     for (int u = 0; u < P; ++u) {
-        const int i = u * RT_THREADS + tid;
+        const int i = (B + u) * RT_THREADS + tid;
         if (i < n) dst[i] = v[u];
     }
-    for (int i0 = P * RT_THREADS + tid; i0 < n; i0 += 4 * RT_THREADS) {
-        int32_t w[4];
+}
+
+template <int B>
+__device__ inline void table_copy_from(const int32_t* src, int32_t* dst, int n, int tid) {
+    for (int i0 = B * RT_THREADS + tid; i0 < n; i0 += 16 * RT_THREADS) {
+        int32_t w[16];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) w[u] = i0 + u * RT_THREADS < n ? src[i0 + u * RT_THREADS] : 0;
+        for (int u = 0; u < 16; ++u) w[u] = src[i0 + u * RT_THREADS < n ? i0 + u * RT_THREADS : i0];
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
+        for (int u = 0; u < 16; ++u)
             if (i0 + u * RT_THREADS < n) dst[i0 + u * RT_THREADS] = w[u];
     }
 }
@@ -265,11 +270,11 @@ route_select_kernel(const RouteArgs a) {
     // the candidate tables: reads issued now, LDS stores after the router loop
     const int n1 = E * a.gmax, nS = a.S_in_lds ? M * M * E : 0;
     int32_t pk[2], pq[2], pn[1], pm[1], ps[2];
-    table_issue<2>(a.t1_k, n1, tid, pk);
-    table_issue<2>((const int32_t*)a.t1_q, n1, tid, pq);
-    table_issue<1>(a.t1_n, E, tid, pn);
-    table_issue<1>((const int32_t*)a.srvmask, E, tid, pm);
-    table_issue<2>((const int32_t*)a.S, nS, tid, ps);
+    table_read<0, 2>(a.t1_k, n1, tid, pk);
+    table_read<0, 2>((const int32_t*)a.t1_q, n1, tid, pq);
+    table_read<0, 1>(a.t1_n, E, tid, pn);
+    table_read<0, 1>((const int32_t*)a.srvmask, E, tid, pm);
+    table_read<0, 2>((const int32_t*)a.S, nS, tid, ps);
     for (int i = tid; i < 8 + M; i += RT_THREADS) s_cnt[i] = 0;
     // this thread's token location and budget, read before the router loop so
     // that their latency is hidden behind it (lanes of waves 0 .. TB/4-1 own tokens)
@@ -284,17 +289,28 @@ route_select_kernel(const RouteArgs a) {
     if (a.ksplit > 0) {
         // split router: add the K slices in slice order (the reads of all
         // slices of an element are issued before the additions)
-        for (int i = tid; i < TB * Epad; i += RT_THREADS) {
-            const int64_t tok = t0 + i / Epad;
-            float pv[RT_SPLIT_MAX_K];
+        // two elements per round; reads past the slices or the batch re-read
+        // the first partial (discarded), so that no branch separates the reads
+        for (int i0 = tid; i0 < TB * Epad; i0 += 2 * RT_THREADS) {
+            float pv[2][RT_SPLIT_MAX_K];
 #pragma unroll
-            for (int z = 0; z < RT_SPLIT_MAX_K; ++z)
-                pv[z] = (z < a.ksplit && tok < a.T) ? a.logit_part[((int64_t)z * a.T + tok) * Epad + i % Epad] : 0.f;
-            float v = 0.f;
+            for (int u = 0; u < 2; ++u) {
+                const int i = i0 + u * RT_THREADS;
+                const int64_t tok = t0 + i / Epad;
+                const bool ok = i < TB * Epad && tok < a.T;
 #pragma unroll
-            for (int z = 0; z < RT_SPLIT_MAX_K; ++z)
-                if (z < a.ksplit) v += pv[z];
-            s_logit[i] = v;
+                for (int z = 0; z < RT_SPLIT_MAX_K; ++z)
+                    pv[u][z] = a.logit_part[(z < a.ksplit && ok) ? ((int64_t)z * a.T + tok) * Epad + i % Epad : 0];
+            }
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                const int i = i0 + u * RT_THREADS;
+                float v = 0.f;
+#pragma unroll
+                for (int z = 0; z < RT_SPLIT_MAX_K; ++z)
+                    if (z < a.ksplit) v += pv[u][z];
+                if (i < TB * Epad) s_logit[i] = (t0 + i / Epad < a.T) ? v : 0.f;
+            }
         }
     } else if (a.dtype == ORDERMOE_BF16) {
         const int nblk = Epad / 16;
@@ -357,11 +373,26 @@ route_select_kernel(const RouteArgs a) {
             s_logit[p] = v;
         }
     }
-    table_store<2>(a.t1_k, s_t1k, n1, tid, pk);
-    table_store<2>((const int32_t*)a.t1_q, (int32_t*)s_t1q, n1, tid, pq);
-    table_store<1>(a.t1_n, s_t1n, E, tid, pn);
-    table_store<1>((const int32_t*)a.srvmask, (int32_t*)s_mask, E, tid, pm);
-    table_store<2>((const int32_t*)a.S, (int32_t*)s_S, nS, tid, ps);
+    {
+        // second batches of the larger tables, read together
+        int32_t qk[2], qq[2], qs[14];
+        table_read<2, 2>(a.t1_k, n1, tid, qk);
+        table_read<2, 2>((const int32_t*)a.t1_q, n1, tid, qq);
+        table_read<2, 14>((const int32_t*)a.S, nS, tid, qs);
+        table_write<0, 2>(s_t1k, n1, tid, pk);
+        table_write<0, 2>((int32_t*)s_t1q, n1, tid, pq);
+        table_write<0, 1>(s_t1n, E, tid, pn);
+        table_write<0, 1>((int32_t*)s_mask, E, tid, pm);
+        table_write<0, 2>((int32_t*)s_S, nS, tid, ps);
+        table_write<2, 2>(s_t1k, n1, tid, qk);
+        table_write<2, 2>((int32_t*)s_t1q, n1, tid, qq);
+        table_write<2, 14>((int32_t*)s_S, nS, tid, qs);
+        table_copy_from<4>(a.t1_k, s_t1k, n1, tid);
+        table_copy_from<4>((const int32_t*)a.t1_q, (int32_t*)s_t1q, n1, tid);
+        table_copy_from<1>(a.t1_n, s_t1n, E, tid);
+        table_copy_from<1>((const int32_t*)a.srvmask, (int32_t*)s_mask, E, tid);
+        table_copy_from<16>((const int32_t*)a.S, (int32_t*)s_S, nS, tid);
+    }
     __syncthreads();
 
     // ---------------- per-token stage: 16 lanes (one DPP row) per token ----------------
