@@ -69,16 +69,17 @@ def _calibrate_copy(torch, gib: int = 1):
     print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "launches": 3}))
 
 
-def _setup(cfg, torch, om):
-    """Library-side layer: similarity build on the GPU, deployment and tables
-    on the host, expert weights of this server packed on the device."""
+def _upload(cfg, torch, a):
+    t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32))
+    return (t.to(torch.bfloat16) if cfg.dtype == "bf16" else t).to("cuda")
+
+
+def _layer_model(cfg, torch, om):
+    """The layer's offline model through the library: similarity build on the
+    GPU, deployment (Algorithm 1) and decision tables on the host."""
     import workloads as wl
     dev = "cuda"
-
-    def up(a):
-        t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32))
-        return (t.to(torch.bfloat16) if cfg.dtype == "bf16" else t).to(dev)
-
+    up = lambda a: _upload(cfg, torch, a)
     W = wl.router(cfg)
     Xc = wl.calibration(cfg)
     ws = torch.empty(om.ordermoe_similarity_workspace_size(Xc.shape[0], cfg.d, cfg.E),
@@ -99,6 +100,19 @@ def _setup(cfg, torch, om):
     tabs_dev["srvmask"] = torch.from_numpy(tabs["srvmask"].view(np.int32)).to(dev)
     w_router = up(W)
     code = om.BF16 if cfg.dtype == "bf16" else om.F32
+    return dict(W=W, Xc=Xc, model=model, x_dep=x_dep, net=net, c=c, dref=dref, z_bits=z_bits,
+                tabs_dev=tabs_dev, w_router=w_router, code=code)
+
+
+def _setup(cfg, torch, om):
+    """Library-side layer: similarity build on the GPU, deployment and tables
+    on the host, expert weights of this server packed on the device."""
+    import workloads as wl
+    dev = "cuda"
+    up = lambda a: _upload(cfg, torch, a)
+    lm = _layer_model(cfg, torch, om)
+    W, model, x_dep, net, c, dref, z_bits = (lm[n] for n in ("W", "model", "x_dep", "net", "c", "dref", "z_bits"))
+    tabs_dev, w_router, code = lm["tabs_dev"], lm["w_router"], lm["code"]
     layer = om.make_layer(code, cfg.d, cfg.E, cfg.k, cfg.M, 15, w_router, tabs_dev, cfg.Qbar,
                           cfg.omega_Q, cfg.pin_local_exact, cfg.allow_sub, cfg.renorm)
     local = [int(j) for j in np.nonzero(x_dep[cfg.m0])[0]]
@@ -271,6 +285,72 @@ def _other_layers(torch, om, steps: int = 10, warmup: int = 3):
     return res
 
 
+def _quality_sweep(torch, om):
+    """Quality-budget sweep of the DeepSeek-MoE-shaped layer (16384 tokens,
+    64 experts + 2 shared, top-6, 8 servers): for each budget Qbar, routing
+    and selection, then the local FFN of every simulated server; the servers'
+    outputs add up to the system output.  Reports the share of slots executed
+    on another server and the relative deviation (Frobenius) of the system
+    output from the zero-budget one, which is the exact top-k MoE output.
+    Expert weights are drawn on the device, N(0, 0.02^2) in bf16."""
+    import workloads as wl
+    cfg = wl.C4
+    dev = "cuda"
+    lm = _layer_model(cfg, torch, om)
+    x_dep, code = lm["x_dep"], lm["code"]
+    E, d, f, M, T, k, nsh = cfg.E, cfg.d, cfg.f, cfg.M, cfg.T, cfg.k, cfg.n_shared
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(cfg.seed)
+    bf = torch.bfloat16
+    g = torch.randn((E, f, d), generator=gen, device=dev, dtype=bf) * 0.02
+    u = torch.randn((E, f, d), generator=gen, device=dev, dtype=bf) * 0.02
+    w_gu_all = torch.empty((E, 2 * f, d), dtype=bf, device=dev)
+    om.ordermoe_pack_gate_up(g, u, w_gu_all)
+    del g, u
+    w_dn_all = torch.randn((E, d, f), generator=gen, device=dev, dtype=bf) * 0.02
+    sg = torch.randn((1, nsh * f, d), generator=gen, device=dev, dtype=bf) * 0.02
+    su = torch.randn((1, nsh * f, d), generator=gen, device=dev, dtype=bf) * 0.02
+    w_sh_gu = torch.empty((1, 2 * nsh * f, d), dtype=bf, device=dev)
+    om.ordermoe_pack_gate_up(sg, su, w_sh_gu)
+    del sg, su
+    w_sh_dn = torch.randn((d, nsh * f), generator=gen, device=dev, dtype=bf) * 0.02
+    servers = []
+    for m in range(M):
+        local = [int(j) for j in np.nonzero(x_dep[m])[0]]
+        sel = torch.tensor(local, dtype=torch.long, device=dev)
+        w_gu, w_dn = w_gu_all[sel].contiguous(), w_dn_all[sel].contiguous()
+        ex = om.make_experts(code, d, f, E, local, w_gu, w_dn, nsh, w_sh_gu, w_sh_dn)
+        servers.append((ex, (w_gu, w_dn), torch.empty(len(local) + 2, dtype=torch.int32, device=dev)))
+    x = _upload(cfg, torch, wl.tokens(cfg))
+    loc = torch.from_numpy(wl.token_locations(cfg)).to(dev)
+    qh = torch.zeros(T, dtype=torch.float32, device=dev)
+    out = om.alloc_route_out(T, k, M, dev)
+    ws_r = torch.empty(om.ordermoe_route_workspace_size(T, k, M), dtype=torch.uint8, device=dev)
+    ws_f = torch.empty(max(om.ordermoe_forward_workspace_size(sv[0], T, k) for sv in servers),
+                       dtype=torch.uint8, device=dev)
+    y = torch.empty((T, d), dtype=bf, device=dev)
+    ysum = torch.empty((T, d), dtype=torch.float32, device=dev)
+    points, y0 = [], None
+    for qbar in wl.C4_QBAR_SWEEP:
+        layer = om.make_layer(code, d, E, k, M, 15, lm["w_router"], lm["tabs_dev"], qbar, cfg.omega_Q,
+                              cfg.pin_local_exact, cfg.allow_sub, cfg.renorm)
+        om.ordermoe_route_select(layer, x, T, loc, qh, out, ws_r)
+        ysum.zero_()
+        for m, (ex, _, ro) in enumerate(servers):
+            om.ordermoe_local_moe_forward(ex, x, T, k, out["w"], out["exec_k"], out["exec_m"], loc, m, y,
+                                          ro, ws_f)
+            ysum += y.float()
+        cnt = out["counters"].cpu().numpy()
+        if y0 is None:
+            y0 = ysum.clone()          # the sweep starts at Qbar = 0: exact top-k MoE
+        rel = float(torch.linalg.norm(ysum - y0) / torch.linalg.norm(y0))
+        points.append({"Qbar": qbar, "remote_ratio": float(cnt[6]) / (T * k),
+                       "classes_LE_LS_RE_RS": [int(v) for v in cnt[:4]],
+                       "flagged_tokens": int(cnt[4]), "rel_deviation": rel})
+    return {"workload": cfg.name, "servers": M, "points": points,
+            "weights": "device draws, N(0, 0.02^2) bf16; routers, tokens and deployment as the layer"}
+
+
 def _decode_stream(torch, om, steps: int = 10, warmup: int = 2):
     """Decode stream through a 32-layer stack of 128-expert top-8 layers (64
     tokens, hidden 4096, FFN 1536, 8 servers, memory ratio 2.0, H = 3), server
@@ -427,9 +507,11 @@ def main():
                     help="skip the similarity-build measurement (65536 x 4096 calibration tokens)")
     ap.add_argument("--no-other-layers", action="store_true",
                     help="skip the Qwen-MoE- and DeepSeek-MoE-shaped layer measurements")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="skip the quality-budget sweep of the DeepSeek-MoE-shaped layer")
     ap.add_argument("--no-stream", action="store_true",
                     help="skip the 32-layer decode-stream measurement")
-    ap.add_argument("--only", choices=("layer", "simbuild", "stream"),
+    ap.add_argument("--only", choices=("layer", "simbuild", "stream", "sweep"),
                     help="run one leg alone (for profiling): the layer step without the other "
                          "legs, or only the similarity build / decode stream (prints that leg's "
                          "JSON object)")
@@ -460,8 +542,12 @@ def main():
     if args.only == "stream":
         print(json.dumps(_decode_stream(torch, om, steps=args.steps, warmup=args.warmup)))
         return
+    if args.only == "sweep":
+        print(json.dumps(_quality_sweep(torch, om)))
+        return
     if args.only == "layer":
         args.no_simbuild = args.no_stream = args.no_cpu_baseline = args.no_other_layers = True
+        args.no_sweep = True
     print("bench: setting up %s" % cfg.name, file=sys.stderr, flush=True)
     st = _setup(cfg, torch, om)
     torch.cuda.synchronize()
@@ -522,6 +608,10 @@ def main():
     if not args.no_other_layers:
         print("bench: C3 and C4 layers", file=sys.stderr, flush=True)
         res["other_layers"] = _other_layers(torch, om)
+    if not args.no_sweep:
+        print("bench: quality-budget sweep", file=sys.stderr, flush=True)
+        res["quality_sweep"] = _quality_sweep(torch, om)
+        torch.cuda.empty_cache()
     if not args.no_stream:
         print("bench: decode stream", file=sys.stderr, flush=True)
         del st["experts"], st["keep"]
