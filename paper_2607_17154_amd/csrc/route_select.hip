@@ -161,6 +161,87 @@ __device__ inline void router_k_loop(const RouteArgs& a, int kw, int lane, int64
     }
 }
 
+// Router partial logits for 32-token blocks of more than 16 experts: the
+// router rows are shared by both 16-token row groups through LDS.  The K axis
+// goes in chunks of RT_CK = 128 (one 32-step per K wave of a row group); the
+// block reads each chunk of W_r coalesced (a wave instruction covers 4 rows x
+// 256 bytes) two chunks ahead into registers and stores it to one of two
+// padded LDS buffers; token rows go from global memory straight into MFMA
+// registers four chunks ahead.  One barrier per chunk.  Requires d % 512 == 0.
+constexpr int RT_CK = 128;
+constexpr int RT_WLD = RT_CK + 8;            // bf16 per LDS row of a W chunk
+constexpr int RT_XD = 4;                     // token chunks in flight per wave
+
+template <int NB>
+__device__ inline void router_lds_loop(const RouteArgs& a, int kw, int lane, int tid, int64_t tr0,
+                                       f32x4* acc, __bf16* sW) {
+    constexpr int KW = 4;
+    constexpr int TPR = RT_CK / 8;                   // threads per W row (16 bytes each)
+    constexpr int RPR = RT_THREADS / TPR;            // W rows per block round
+    constexpr int WR = NB * 16 / RPR;                // rounds per chunk (NB * 16 rows)
+    static_assert(WR >= 1 && NB * 16 % RPR == 0, "whole rounds of W rows");
+    const int d = a.d, E = a.E;
+    const int r16 = lane & 15, kg = (lane >> 4) * 8;
+    const int64_t left = a.T - tr0;
+    const int nrows = left < 0 ? 0 : (left > 16 ? 16 : (int)left);
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc((const __bf16*)a.x + (tr0 < a.T ? tr0 : 0) * (int64_t)d,
+                                                (uint32_t)nrows * (uint32_t)d * 2u);
+    const __amdgpu_buffer_rsrc_t rw = make_rsrc(a.w_router, (uint32_t)E * (uint32_t)d * 2u);
+    const uint32_t xo = r16 < nrows ? ((uint32_t)r16 * (uint32_t)d + kg + 32 * kw) * 2u : RT_OOR;
+    // W staging slot of this thread: row wrow + RPR * i, 8 elements at wcol of the chunk
+    const int wrow = tid / TPR, wcol = (tid % TPR) * 8;
+    uint32_t wo[WR];
+#pragma unroll
+    for (int i = 0; i < WR; ++i) {
+        const int e = wrow + RPR * i;
+        wo[i] = e < E ? ((uint32_t)e * (uint32_t)d + wcol) * 2u : RT_OOR;
+    }
+    const int NC = d / RT_CK;
+    bf16x8 xr[RT_XD], wreg[2][WR];
+    auto xload = [&](int slot, int c) {
+        const uint32_t past = c < NC ? 0u : RT_OOR;
+        xr[slot] = buf_load16(rx, xo | past, (uint32_t)(c < NC ? c : 0) * (RT_CK * 2u));
+    };
+    auto wload = [&](int set, int c) {
+#pragma unroll
+        for (int i = 0; i < WR; ++i) wreg[set][i] = buf_load16(rw, wo[i], (uint32_t)c * (RT_CK * 2u));
+    };
+    auto wstore = [&](int buf, int set) {
+        __bf16* p = sW + buf * (NB * 16 * RT_WLD) + wrow * RT_WLD + wcol;
+#pragma unroll
+        for (int i = 0; i < WR; ++i) *(bf16x8*)(p + i * RPR * RT_WLD) = wreg[set][i];
+    };
+    const __bf16* frag = sW + r16 * RT_WLD + kw * 32 + kg;
+    auto mma = [&](int buf, int slot) {
+        bf16x8 bf[NB];
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) bf[nb] = *(const bf16x8*)(frag + buf * (NB * 16 * RT_WLD) + nb * 16 * RT_WLD);
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+            acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xr[slot], bf[nb], acc[nb], 0, 0, 0);
+    };
+#pragma unroll
+    for (int u = 0; u < RT_XD; ++u) xload(u, u);
+    wload(0, 0);
+    wload(1, 1);
+    wstore(0, 0);
+    __syncthreads();
+    // chunk c: store chunk c+1 (read one chunk ago) to the other buffer, read
+    // chunk c+2 into the freed register set, multiply chunk c, read token
+    // chunk c + RT_XD into the freed slot; unrolled by RT_XD (NC % 4 == 0)
+    for (int c0 = 0; c0 < NC; c0 += RT_XD) {
+#pragma unroll
+        for (int u = 0; u < RT_XD; ++u) {
+            const int c = c0 + u;
+            if (c + 1 < NC) wstore((u + 1) & 1, (u + 1) & 1);
+            if (c + 2 < NC) wload(u & 1, c + 2);
+            mma(u & 1, u);
+            xload(u, c + RT_XD);
+            __syncthreads();
+        }
+    }
+}
+
 // One candidate table (T1 experts, T1 losses, T1 lengths, server masks, or the
 // cost table when it is staged) copied to LDS by the block in batches of whole
 // block rounds: words [B * RT_THREADS, (B + P) * RT_THREADS) are read into P
@@ -242,6 +323,17 @@ __global__ void __launch_bounds__(64) router_split_kernel(const RouteArgs a) {
     }
 }
 
+// floats of the first LDS region: the partial-sum slots, or (32-token blocks of
+// more than 16 experts) the two staged router-row buffers if larger
+__host__ __device__ inline int route_region0_floats(int tb, int E) {
+    const int Epad = (E + 15) & ~15;
+    const int part = RT_SLOTS * tb * Epad;
+    // the staged loop keeps NBT * 16 rows per buffer (32 or 64), two buffers of bf16
+    const int rows = Epad <= 32 ? 32 : 64;
+    const int wbuf = (tb == RT_TB2 && Epad > 16 && Epad <= 64) ? rows * RT_WLD : 0;
+    return part > wbuf ? part : wbuf;
+}
+
 // up to 64 experts: at most 128 VGPRs (4 waves per SIMD), so two blocks share a CU
 template <int NBT, int TB>
 __global__ void __launch_bounds__(RT_THREADS) __attribute__((amdgpu_waves_per_eu(NBT <= 4 ? 4 : 2)))
@@ -259,7 +351,7 @@ route_select_kernel(const RouteArgs a) {
     extern __shared__ float smem[];
     float* s_part = smem;                               // [RT_SLOTS][TB][Epad]
     float* s_logit = smem;                              // reuses slot 0 after the sum
-    int32_t* s_t1k = (int32_t*)(smem + RT_SLOTS * TB * Epad);      // [E][gmax]
+    int32_t* s_t1k = (int32_t*)(smem + route_region0_floats(TB, E));   // [E][gmax]
     float* s_t1q = (float*)(s_t1k + E * a.gmax);                   // [E][gmax]
     int32_t* s_t1n = (int32_t*)(s_t1q + E * a.gmax);               // [E]
     uint32_t* s_mask = (uint32_t*)(s_t1n + E);                     // [E]
@@ -321,6 +413,8 @@ route_select_kernel(const RouteArgs a) {
         // group size: two groups of reads in flight per wave, within 128
         // registers so that two blocks share a CU
         if constexpr (NBT == 1) router_k_loop<1, 4, KW>(a, kw, lane, t0 + rg * 16, acc);
+        else if constexpr (TB == RT_TB2 && NBT == 2) router_lds_loop<2>(a, kw, lane, tid, t0 + rg * 16, acc, (__bf16*)smem);
+        else if constexpr (TB == RT_TB2 && NBT == 4) router_lds_loop<4>(a, kw, lane, tid, t0 + rg * 16, acc, (__bf16*)smem);
         else if constexpr (NBT == 2) router_k_loop<2, 2, KW>(a, kw, lane, t0 + rg * 16, acc);
         else if constexpr (NBT == 4) router_k_loop<4, 2, KW>(a, kw, lane, t0 + rg * 16, acc);
         else if constexpr (NBT == 8) router_k_loop<8, 1, KW>(a, kw, lane, t0 + rg * 16, acc);
@@ -330,6 +424,8 @@ route_select_kernel(const RouteArgs a) {
         // row group, waves 4-7 first hand their sums to waves 0-3.
         const int r16 = lane & 15;
         const int trow = rg * 16 + (lane >> 4) * 4;
+        // the staged router rows share LDS with the partial-sum slots
+        if constexpr (TB == RT_TB2 && (NBT == 2 || NBT == 4)) __syncthreads();
         if (KW == 8 && wave >= RT_SLOTS) {
 #pragma unroll
             for (int nb = 0; nb < NBT; ++nb)
@@ -698,8 +794,7 @@ int launch_route_kernel(const RouteArgs& a, size_t smem, hipStream_t st) {
 }
 
 size_t route_smem(int tb, int E, int gmax, int M, bool S_in_lds) {
-    const int Epad = (E + 15) & ~15;
-    return sizeof(float) * (size_t)RT_SLOTS * tb * Epad + (size_t)E * gmax * 8 + (size_t)E * 8 +
+    return sizeof(float) * (size_t)route_region0_floats(tb, E) + (size_t)E * gmax * 8 + (size_t)E * 8 +
            sizeof(int) * (size_t)(8 + M) + (S_in_lds ? sizeof(float) * (size_t)M * M * E : 0);
 }
 
@@ -729,11 +824,15 @@ int launch_route_select(const RouteArgs& a, void* stream) {
     const int nb = (a.E + 15) / 16;
     const int nbt = nb <= 1 ? 1 : nb <= 2 ? 2 : nb <= 4 ? 4 : nb <= 8 ? 8 : 16;
     const bool split = a.dtype == ORDERMOE_BF16 && a.T <= RT_SPLIT_MAX_T && a.logit_part;
-    // large bf16 batches (more than two blocks of 16 tokens per CU) of at most 64
-    // experts take blocks of 32 tokens: the router weights are read half as often
-    // and all 8 waves run the token stage
+    // Large bf16 batches take blocks of 32 tokens, so that all 8 waves run the
+    // token stage: at most 16 experts from more than 512 blocks of 16 tokens,
+    // 17..64 experts from 512 such blocks on (their router rows are then staged
+    // in LDS and shared by the two row groups, which needs d % 512 == 0; the
+    // 32-token kernels of 17..64 experts always take that loop).
     const int64_t nb16 = (a.T + RT_TB - 1) / RT_TB;
-    const int tb = (a.dtype == ORDERMOE_BF16 && !split && nbt <= 4 && nb16 > 512) ? RT_TB2 : RT_TB;
+    const bool bf = a.dtype == ORDERMOE_BF16 && !split;
+    const bool staged = bf && (nbt == 2 || nbt == 4) && a.d % 512 == 0 && nb16 >= 512;
+    const int tb = staged || (bf && nbt == 1 && nb16 > 512) ? RT_TB2 : RT_TB;
     RouteArgs b = a;
     b.nblk = (int)((a.T + tb - 1) / tb);
     if (b.nblk > 0) {

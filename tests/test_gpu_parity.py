@@ -34,7 +34,10 @@ DECODE = {
     "C3d": wl.C3.with_(T=128, T_cal=4096),
     "C4d": wl.C4.with_(T=97, T_cal=4096),
 }
-FULL = {"C2": wl.C2.with_(T_cal=4096), "C3": wl.C3.with_(T_cal=4096), "C4": wl.C4.with_(T_cal=4096)}
+FULL = {"C2": wl.C2.with_(T_cal=4096), "C3": wl.C3.with_(T_cal=4096), "C4": wl.C4.with_(T_cal=4096),
+        # large batches with a ragged last block of the 32-token routing kernels:
+        # at most 16 experts, and 17..64 experts (router rows staged in LDS)
+        "C2x": wl.C2.with_(T=8192 + 33, T_cal=4096), "C3x": wl.C3.with_(T=8192 + 17, T_cal=4096)}
 
 _cache = {}
 
