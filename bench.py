@@ -351,22 +351,15 @@ def _quality_sweep(torch, om):
             "weights": "device draws, N(0, 0.02^2) bf16; routers, tokens and deployment as the layer"}
 
 
-def _decode_stream(torch, om, steps: int = 10, warmup: int = 2):
-    """Decode stream through a 32-layer stack of 128-expert top-8 layers (64
-    tokens, hidden 4096, FFN 1536, 8 servers, memory ratio 2.0, H = 3), server
-    0's share: per layer route/select with the location and accumulated loss
-    carried on the device from the previous layer, then the local expert FFN.
-    The offline model is built by the library (similarity on the device,
-    transitions, deployment, look-ahead and tables on the host).  Expert
-    weights of server 0 (32 per layer, 38.7 GB in all) are drawn on the device,
-    N(0, 0.02^2) in bf16, and stay resident.  The 32-layer step is timed as a
-    HIP graph replay (also with eager launches); reports time per layer and the
-    HBM fraction of the weights the layer has to stream."""
+def _stream_model(torch, om, cfg):
+    """The stack's offline model through the library: per layer the similarity
+    build on the GPU (with the top-1 of each calibration token), then the
+    transition estimate (eq 41) and the joint deployment (Algorithm 1) on the
+    host."""
     import workloads as wl
-    cfg = wl.C5_STREAM
     dev = "cuda"
     up = lambda a: torch.from_numpy(wl.bf16_bits(a).view(np.int16)).view(torch.bfloat16).to(dev)
-    N, E, M, T, k = cfg.N, cfg.E, cfg.M, cfg.T, cfg.k
+    N, E, M, k = cfg.N, cfg.E, cfg.M, cfg.k
     W = wl.stream_routers(cfg)
     theta = [om.ordermoe_theta_layer(l + 1, N, cfg.theta_min, cfg.theta_max) for l in range(N)]
     ws = torch.empty(om.ordermoe_similarity_workspace_size(cfg.T_cal, cfg.d, E), dtype=torch.uint8,
@@ -386,22 +379,137 @@ def _decode_stream(torch, om, steps: int = 10, warmup: int = 2):
     c = np.full(E, 6.0 * cfg.d * cfg.f)
     dref = float(np.mean(c)) / float(np.mean(net.F))
     z_bits = 8.0 * cfg.d * cfg.bytes_per_el
-    phi = om.ordermoe_build_lookahead(cfg.H, P, np.stack(x_dep), np.stack([m["sim"] for m in models]),
-                                      np.stack([m["group_of"] for m in models]),
-                                      np.array(theta, np.float32), np.full(N, z_bits), np.tile(c, (N, 1)),
-                                      np.full(N, dref), net.B, net.tau, net.F, cfg.omega_T, cfg.omega_Q,
-                                      cfg.Qbar, cfg.pin_local_exact, cfg.allow_sub)
+    return dict(theta=theta, w_router=w_router, models=models, P=P, x_dep=x_dep, net=net, c=c, dref=dref,
+                z_bits=z_bits, X=[up(x) for x in wl.stream_tokens(cfg)])
+
+
+def _stream_lookahead(om, cfg, sm, H, omega_T, omega_Q, allow_sub=None):
+    """Phi_l^(H-1) of every layer (eq 42) by the library."""
+    N = cfg.N
+    return om.ordermoe_build_lookahead(H, sm["P"], np.stack(sm["x_dep"]), np.stack([m["sim"] for m in sm["models"]]),
+                                      np.stack([m["group_of"] for m in sm["models"]]),
+                                      np.array(sm["theta"], np.float32), np.full(N, sm["z_bits"]),
+                                      np.tile(sm["c"], (N, 1)), np.full(N, sm["dref"]), sm["net"].B,
+                                      sm["net"].tau, sm["net"].F, omega_T, omega_Q, cfg.Qbar,
+                                      cfg.pin_local_exact, cfg.allow_sub if allow_sub is None else allow_sub)
+
+
+def _stream_layers(torch, om, cfg, sm, phi, omega_T, omega_Q, allow_sub=None):
+    """Per layer: the decision tables (eq 7, 18, 37-38 with Phi) on the device
+    and the layer struct."""
+    out = []
+    for l in range(cfg.N):
+        md = sm["models"][l]
+        tabs = om.ordermoe_build_tables(md["sim"], md["group_of"], sm["theta"][l], sm["x_dep"][l], sm["net"].B,
+                                        sm["net"].tau, sm["net"].F, sm["z_bits"], sm["c"], sm["dref"], omega_T,
+                                        phi[l])
+        tdev = {n: torch.from_numpy(np.ascontiguousarray(v)).to("cuda") for n, v in tabs.items()
+                if n != "srvmask"}
+        tdev["srvmask"] = torch.from_numpy(tabs["srvmask"].view(np.int32)).to("cuda")
+        L = om.make_layer(om.BF16, cfg.d, cfg.E, cfg.k, cfg.M, 15, sm["w_router"][l], tdev, cfg.Qbar, omega_Q,
+                          cfg.pin_local_exact, cfg.allow_sub if allow_sub is None else allow_sub, cfg.renorm)
+        out.append((L, tdev))
+    return out
+
+
+def _route_chain(torch, om, cfg, sm, layers, qh0=None):
+    """The route/select chain through the stack for the decode batch (the
+    location and accumulated loss carried on the device); per layer the host
+    copies of the decisions and counters."""
+    T, k, M = cfg.T, cfg.k, cfg.M
+    loc = torch.zeros(T, dtype=torch.uint8, device="cuda")
+    qh = torch.zeros(T, dtype=torch.float32, device="cuda") if qh0 is None else qh0
+    ws = torch.empty(om.ordermoe_route_workspace_size(T, k, M), dtype=torch.uint8, device="cuda")
+    recs = []
+    for l, (L, _) in enumerate(layers):
+        out = om.alloc_route_out(T, k, M, "cuda")
+        om.ordermoe_route_select(L, sm["X"][l], T, loc, qh, out, ws)
+        recs.append((loc, out))
+        loc, qh = out["loc_out"], out["qhat_out"]
+    torch.cuda.synchronize()
+    return [dict(loc_in=li.cpu().numpy(), exec_m=o["exec_m"].cpu().numpy(), exec_k=o["exec_k"].cpu().numpy(),
+                 counters=o["counters"].cpu().numpy(), qhat_out=o["qhat_out"].cpu().numpy()) for li, o in recs]
+
+
+def _trajectory_metrics(cfg, sm, recs):
+    """Along the realized trajectories: the modeled delay of every executed slot,
+    d(m, k | s) of eq 37 (transfer from the token's location s when m != s, plus
+    compute c_k / F_m), summed per token over slots and layers; cross-server
+    transfers (distinct token-destination pairs per layer); slot classes; the
+    budget used at the end."""
+    net, c, z = sm["net"], sm["c"], sm["z_bits"]
+    T, k = cfg.T, cfg.k
+    delay = np.zeros(T)
+    cls = np.zeros(4, np.int64)
+    transfers = 0
+    for r in recs:
+        s = r["loc_in"].astype(np.int64)[:, None].repeat(k, 1)
+        m = r["exec_m"].astype(np.int64)
+        kk = r["exec_k"].astype(np.int64)
+        trans = np.where(s != m, z / net.B[s, m] + net.tau[s, m], 0.0)
+        delay += (trans + c[kk] / net.F[m]).sum(axis=1)
+        cls += r["counters"][:4].astype(np.int64)
+        transfers += int(r["counters"][5])
+    slots = cls.sum()
+    return {"delay_ms_per_token": float(delay.mean() * 1e3), "transfers_per_token_layer": transfers / (T * cfg.N),
+            "remote_ratio": float(cls[2] + cls[3]) / slots, "classes_LE_LS_RE_RS": [int(v) for v in cls],
+            "budget_used": float(np.mean(recs[-1]["qhat_out"]) / cfg.Qbar)}
+
+
+def _horizon_sweep(torch, om):
+    """Look-ahead depth sweep (Fig. 7 of the paper) on the 32-layer decode stack,
+    at memory ratios 2.0 and 1.0: for H = 1 .. 5 the library builds Phi^(H-1)
+    (eq 42) on the host, then the
+    route/select chain runs through the 32 layers for the 64-token batch.
+    Reports the modeled delay and cross-server transfers of the realized
+    trajectories, slot classes, budget used, and the host time of the Phi
+    build (the per-token decision cost on the GPU does not depend on H: Phi is
+    a table lookup)."""
+    import workloads as wl
+    points = []
+    # memory ratio 2.0 (the paper's default: every server then holds a member of
+    # every group) and 1.0 (each server holds half of the groups)
+    for ratio in (2.0, 1.0):
+        cfg = wl.C5_STREAM.with_(memory_ratio=ratio)
+        sm = _stream_model(torch, om, cfg)
+        for H in (1, 2, 3, 4, 5):
+            t0 = time.perf_counter()
+            phi = _stream_lookahead(om, cfg, sm, H, cfg.omega_T, cfg.omega_Q)
+            t_phi = time.perf_counter() - t0
+            layers = _stream_layers(torch, om, cfg, sm, phi, cfg.omega_T, cfg.omega_Q)
+            met = _trajectory_metrics(cfg, sm, _route_chain(torch, om, cfg, sm, layers))
+            met.update(memory_ratio=ratio, H=H, phi_build_ms=t_phi * 1e3)
+            points.append(met)
+        del sm
+    return {"workload": wl.C5_STREAM.name, "points": points}
+
+
+def _decode_stream(torch, om, steps: int = 10, warmup: int = 2):
+    """Decode stream through a 32-layer stack of 128-expert top-8 layers (64
+    tokens, hidden 4096, FFN 1536, 8 servers, memory ratio 2.0, H = 3), server
+    0's share: per layer route/select with the location and accumulated loss
+    carried on the device from the previous layer, then the local expert FFN.
+    The offline model is built by the library (similarity on the device,
+    transitions, deployment, look-ahead and tables on the host).  Expert
+    weights of server 0 (32 per layer, 38.7 GB in all) are drawn on the device,
+    N(0, 0.02^2) in bf16, and stay resident.  The 32-layer step is timed as a
+    HIP graph replay (also with eager launches); reports time per layer and the
+    HBM fraction of the weights the layer has to stream."""
+    import workloads as wl
+    cfg = wl.C5_STREAM
+    dev = "cuda"
+    up = lambda a: torch.from_numpy(wl.bf16_bits(a).view(np.int16)).view(torch.bfloat16).to(dev)
+    N, E, M, T, k = cfg.N, cfg.E, cfg.M, cfg.T, cfg.k
+    sm = _stream_model(torch, om, cfg)
+    theta, w_router, models, x_dep, net, c, dref, z_bits = (
+        sm[n] for n in ("theta", "w_router", "models", "x_dep", "net", "c", "dref", "z_bits"))
+    phi = _stream_lookahead(om, cfg, sm, cfg.H, cfg.omega_T, cfg.omega_Q)
     gen = torch.Generator(device=dev)
     gen.manual_seed(cfg.seed)
     layers = []
+    tab_layers = _stream_layers(torch, om, cfg, sm, phi, cfg.omega_T, cfg.omega_Q)
     for l in range(N):
-        tabs = om.ordermoe_build_tables(models[l]["sim"], models[l]["group_of"], theta[l], x_dep[l],
-                                        net.B, net.tau, net.F, z_bits, c, dref, cfg.omega_T, phi[l])
-        tdev = {n: torch.from_numpy(np.ascontiguousarray(v)).to(dev) for n, v in tabs.items()
-                if n != "srvmask"}
-        tdev["srvmask"] = torch.from_numpy(tabs["srvmask"].view(np.int32)).to(dev)
-        L = om.make_layer(om.BF16, cfg.d, E, k, M, 15, w_router[l], tdev, cfg.Qbar, cfg.omega_Q,
-                          cfg.pin_local_exact, cfg.allow_sub, cfg.renorm)
+        L, tdev = tab_layers[l]
         local = [int(j) for j in np.nonzero(x_dep[l][cfg.m0])[0]]
         n = len(local)
         g = torch.randn((n, cfg.f, cfg.d), generator=gen, device=dev, dtype=torch.bfloat16) * 0.02
@@ -414,8 +522,7 @@ def _decode_stream(torch, om, steps: int = 10, warmup: int = 2):
         out = om.alloc_route_out(T, k, M, dev)
         layers.append(dict(L=L, keep=(tdev, w_gu, w_dn), ex=ex, out=out, os=om.route_out_struct(out),
                            ro=torch.empty(n + 2, dtype=torch.int32, device=dev), n_local=n))
-    X = wl.stream_tokens(cfg)
-    xs = [up(X[l]) for l in range(N)]
+    xs = sm["X"]
     ws_r = torch.empty(om.ordermoe_route_workspace_size(T, k, M), dtype=torch.uint8, device=dev)
     ws_f = torch.empty(max(max(om.ordermoe_forward_workspace_size(Ld["ex"], T, k) for Ld in layers), 1),
                        dtype=torch.uint8, device=dev)
@@ -509,9 +616,11 @@ def main():
                     help="skip the Qwen-MoE- and DeepSeek-MoE-shaped layer measurements")
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the quality-budget sweep of the DeepSeek-MoE-shaped layer")
+    ap.add_argument("--no-horizon", action="store_true",
+                    help="skip the look-ahead depth sweep H = 1..5 of the decode stack")
     ap.add_argument("--no-stream", action="store_true",
                     help="skip the 32-layer decode-stream measurement")
-    ap.add_argument("--only", choices=("layer", "simbuild", "stream", "sweep"),
+    ap.add_argument("--only", choices=("layer", "simbuild", "stream", "sweep", "horizon"),
                     help="run one leg alone (for profiling): the layer step without the other "
                          "legs, or only the similarity build / decode stream (prints that leg's "
                          "JSON object)")
@@ -545,9 +654,12 @@ def main():
     if args.only == "sweep":
         print(json.dumps(_quality_sweep(torch, om)))
         return
+    if args.only == "horizon":
+        print(json.dumps(_horizon_sweep(torch, om)))
+        return
     if args.only == "layer":
         args.no_simbuild = args.no_stream = args.no_cpu_baseline = args.no_other_layers = True
-        args.no_sweep = True
+        args.no_sweep = args.no_horizon = True
     print("bench: setting up %s" % cfg.name, file=sys.stderr, flush=True)
     st = _setup(cfg, torch, om)
     torch.cuda.synchronize()
@@ -611,6 +723,10 @@ def main():
     if not args.no_sweep:
         print("bench: quality-budget sweep", file=sys.stderr, flush=True)
         res["quality_sweep"] = _quality_sweep(torch, om)
+        torch.cuda.empty_cache()
+    if not args.no_horizon:
+        print("bench: look-ahead depth sweep", file=sys.stderr, flush=True)
+        res["horizon_sweep"] = _horizon_sweep(torch, om)
         torch.cuda.empty_cache()
     if not args.no_stream:
         print("bench: decode stream", file=sys.stderr, flush=True)

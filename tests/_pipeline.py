@@ -270,3 +270,17 @@ def stream_library_tables(sc: StreamCase, gmax: int = 15):
                                      sc.x_dep[l], sc.net.B, sc.net.tau, sc.net.F, sc.z_bits, sc.c,
                                      sc.dref, cfg.omega_T, phi[l], gmax) for l in range(N)]
     return theta32, phi, tabs
+
+
+def with_horizon(sc: StreamCase, H: int) -> StreamCase:
+    """The same stack with the look-ahead depth H (eq 42): the oracle's Phi and
+    cost tables recomputed, everything else shared."""
+    import dataclasses
+    cfg = dataclasses.replace(sc.cfg, H=H)
+    groups = [m["group_of"] for m in sc.models]
+    phi = tables.lookahead(H, sc.P, sc.x_dep, sc.sim32, groups, sc.theta, [sc.z_bits] * cfg.N, sc.net.B,
+                           sc.net.tau, [sc.c] * cfg.N, sc.net.F, [sc.dref] * cfg.N, cfg.omega_T, cfg.omega_Q,
+                           cfg.Qbar, cfg.pin_local_exact, cfg.allow_sub)
+    S = [tables.static_cost(cfg.M, cfg.E, sc.z_bits, sc.net.B, sc.net.tau, sc.c, sc.net.F, sc.dref,
+                            cfg.omega_T, phi[l]) for l in range(cfg.N)]
+    return dataclasses.replace(sc, cfg=cfg, phi=phi, S=S)

@@ -29,11 +29,10 @@ from paper_2607_17154_amd import ordermoe as om  # noqa: E402
 FORWARD_LAYERS = (0, 31)
 
 
-@pytest.fixture(scope="module")
-def chain(stream_case):
-    """Run the GPU chain once; keep every layer's outputs (host) and the device
-    inputs of the layers whose forward is checked."""
-    sc, cfg = stream_case, stream_case.cfg
+def _gpu_chain(sc, keep_layers=()):
+    """Run the route/select chain of the stack on the GPU; every layer's outputs
+    (host) and the device inputs of the layers in keep_layers."""
+    cfg = sc.cfg
     theta32, phi, tabs = stream_library_tables(sc)
     T = cfg.T
     loc = torch.zeros(T, dtype=torch.uint8, device="cuda")
@@ -56,43 +55,44 @@ def chain(stream_case):
         rec = {n: host(v) for n, v in out.items()}
         rec["loc_in"] = host(loc)
         layers.append(rec)
-        if l in FORWARD_LAYERS:
+        if l in keep_layers:
             keep[l] = (x, loc.clone(), out)
         loc, qh = out["loc_out"], out["qhat_out"]   # carried to the next layer on the device
     return dict(layers=layers, keep=keep)
 
 
-@pytest.fixture(scope="module")
-def oracle_chain(stream_case, chain):
+def _oracle_chain(sc, gpu_layers):
     """The oracle's own chain: per layer its decisions, the locations it started
     from, and the tokens not flagged (on either side) up to that layer."""
-    sc, cfg = stream_case, stream_case.cfg
+    cfg = sc.cfg
     loc = np.zeros(cfg.T, np.uint8)
     qh = np.zeros(cfg.T, np.float32)
     live = np.ones(cfg.T, bool)
     res = []
     for l in range(cfg.N):
         dec = stream_oracle_layer(sc, l, loc, qh)
-        flag = (dec["margin"] < 1e-4) | (chain["layers"][l]["margin"] < 1e-4)
+        flag = (dec["margin"] < 1e-4) | (gpu_layers[l]["margin"] < 1e-4)
         live = live & ~flag
         res.append(dict(dec=dec, loc_in=loc, live=live, flag=flag))
         loc, qh = dec["loc_out"], dec["qhat_out"]
     return res
 
 
-def test_chain_decisions_match_the_oracle(stream_case, chain, oracle_chain):
-    sc, cfg = stream_case, stream_case.cfg
+def _compare_chain(sc, gpu_layers, oracle_chain):
+    """Decisions bit-exact on live tokens at every layer, the GPU's inputs are
+    its previous outputs, Property 2, counters and dispatch lists; returns the
+    first layer at which substitution has stopped."""
+    cfg = sc.cfg
     T, k = cfg.T, cfg.k
     exhausted_layer = None
     for l in range(cfg.N):
-        g = chain["layers"][l]
+        g = gpu_layers[l]
         dec, loc, live, flag = (oracle_chain[l][n] for n in ("dec", "loc_in", "live", "flag"))
-        # the GPU's own inputs at this layer are its previous outputs
         if l > 0:
-            np.testing.assert_array_equal(g["loc_in"], chain["layers"][l - 1]["loc_out"])
+            np.testing.assert_array_equal(g["loc_in"], gpu_layers[l - 1]["loc_out"])
         ok = live
         for n in ("idx", "exec_k", "exec_m", "cls", "qhat_out", "loc_out"):
-            np.testing.assert_array_equal(g[n][ok], dec[n][ok], err_msg="layer %d %s" % (l, n))
+            np.testing.assert_array_equal(g[n][ok], dec[n][ok], err_msg="H %d layer %d %s" % (cfg.H, l, n))
         # Property 2 on every token, flagged or not
         assert np.all(g["qhat_out"] <= np.float32(cfg.Qbar)), l
         # class counters and the dispatch list of the GPU's own decisions
@@ -109,14 +109,39 @@ def test_chain_decisions_match_the_oracle(stream_case, chain, oracle_chain):
         subs = int(c[1] + c[3])
         if exhausted_layer is None and l > 0 and subs < 0.02 * T * k:
             exhausted_layer = l
-        print("layer %2d: LE/LS/RE/RS %s  flagged %d  compared %d  max Qhat %.4f" % (
-            l, list(c[:4]), int(flag.sum()), int(ok.sum()), float(g["qhat_out"].max())), flush=True)
+        print("H %d layer %2d: LE/LS/RE/RS %s  flagged %d  compared %d  max Qhat %.4f" % (
+            cfg.H, l, list(c[:4]), int(flag.sum()), int(ok.sum()), float(g["qhat_out"].max())), flush=True)
     live = oracle_chain[-1]["live"]
-    print("live tokens after %d layers: %d of %d; substitution stops at layer %s"
-          % (cfg.N, int(live.sum()), T, exhausted_layer), flush=True)
+    print("H %d: live tokens after %d layers: %d of %d; substitution stops at layer %s"
+          % (cfg.H, cfg.N, int(live.sum()), T, exhausted_layer), flush=True)
     assert live.sum() >= T // 2
+    return exhausted_layer
+
+
+@pytest.fixture(scope="module")
+def chain(stream_case):
+    return _gpu_chain(stream_case, FORWARD_LAYERS)
+
+
+@pytest.fixture(scope="module")
+def oracle_chain(stream_case, chain):
+    return _oracle_chain(stream_case, chain["layers"])
+
+
+def test_chain_decisions_match_the_oracle(stream_case, chain, oracle_chain):
+    exhausted_layer = _compare_chain(stream_case, chain["layers"], oracle_chain)
     # the budget binds mid-stream: substitutions give way to exact execution
-    assert exhausted_layer is not None and 4 <= exhausted_layer < cfg.N - 4
+    assert exhausted_layer is not None and 4 <= exhausted_layer < stream_case.cfg.N - 4
+
+
+@pytest.mark.parametrize("H", [1, 5])
+def test_chain_decisions_match_the_oracle_at_other_horizons(stream_case, H):
+    """The look-ahead sweep of Fig. 7: the myopic rule (H = 1) and the deepest
+    horizon swept (H = 5) run the same chain comparison."""
+    from ._pipeline import with_horizon
+    sc = with_horizon(stream_case, H)
+    g = _gpu_chain(sc)
+    _compare_chain(sc, g["layers"], _oracle_chain(sc, g["layers"]))
 
 
 @pytest.mark.parametrize("layer", FORWARD_LAYERS)

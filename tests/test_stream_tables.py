@@ -3,6 +3,7 @@ servers, memory ratio 2.0, H = 3): the oracle's construction against what the
 paper fixes, and the library's host tables (eq 6, 41, 42, 7, 37-38) against
 the oracle's, bit for bit."""
 import numpy as np
+import pytest
 
 import workloads as wl
 from oracle import tables
@@ -104,3 +105,20 @@ def test_library_theta_layer():
     for N in (1, 2, 5, 32):
         for l in range(1, N + 1):
             assert om.ordermoe_theta_layer(l, N, 0.5, 0.9) == np.float32(tables.theta_layer(l, N, 0.5, 0.9))
+
+
+@pytest.mark.parametrize("H", [1, 2, 5])
+def test_library_lookahead_matches_the_oracle_at_every_horizon(stream_case, H):
+    """The look-ahead sweep of Fig. 7 (H = 1 .. 5): the library's Phi (eq 42) and
+    cost tables equal the oracle's bit for bit at each depth; H = 1 is the
+    myopic rule (Phi = 0)."""
+    from tests._pipeline import stream_library_tables, with_horizon
+    sc = with_horizon(stream_case, H)
+    _, phi, tabs = stream_library_tables(sc)
+    for l in range(sc.cfg.N):
+        np.testing.assert_array_equal(phi[l], sc.phi[l])
+        np.testing.assert_array_equal(tabs[l]["S"].view(np.uint32), sc.S[l].view(np.uint32))
+    if H == 1:
+        assert all(np.all(p == 0) for p in phi)
+    else:
+        assert any(np.any(p > 0) for p in phi)
