@@ -431,23 +431,31 @@ def _route_chain(torch, om, cfg, sm, layers, qh0=None):
                  counters=o["counters"].cpu().numpy(), qhat_out=o["qhat_out"].cpu().numpy()) for li, o in recs]
 
 
+def _token_delays(cfg, sm, recs):
+    """Per token: the modeled delay of eq 37 summed over its executed slots and
+    the layers, along the realized trajectory (seconds)."""
+    net, c, z = sm["net"], sm["c"], sm["z_bits"]
+    delay = np.zeros(cfg.T)
+    for r in recs:
+        s = r["loc_in"].astype(np.int64)[:, None].repeat(cfg.k, 1)
+        m = r["exec_m"].astype(np.int64)
+        kk = r["exec_k"].astype(np.int64)
+        trans = np.where(s != m, z / net.B[s, m] + net.tau[s, m], 0.0)
+        delay += (trans + c[kk] / net.F[m]).sum(axis=1)
+    return delay
+
+
 def _trajectory_metrics(cfg, sm, recs):
     """Along the realized trajectories: the modeled delay of every executed slot,
     d(m, k | s) of eq 37 (transfer from the token's location s when m != s, plus
     compute c_k / F_m), summed per token over slots and layers; cross-server
     transfers (distinct token-destination pairs per layer); slot classes; the
     budget used at the end."""
-    net, c, z = sm["net"], sm["c"], sm["z_bits"]
-    T, k = cfg.T, cfg.k
-    delay = np.zeros(T)
+    T = cfg.T
+    delay = _token_delays(cfg, sm, recs)
     cls = np.zeros(4, np.int64)
     transfers = 0
     for r in recs:
-        s = r["loc_in"].astype(np.int64)[:, None].repeat(k, 1)
-        m = r["exec_m"].astype(np.int64)
-        kk = r["exec_k"].astype(np.int64)
-        trans = np.where(s != m, z / net.B[s, m] + net.tau[s, m], 0.0)
-        delay += (trans + c[kk] / net.F[m]).sum(axis=1)
         cls += r["counters"][:4].astype(np.int64)
         transfers += int(r["counters"][5])
     slots = cls.sum()
@@ -482,6 +490,36 @@ def _horizon_sweep(torch, om):
             points.append(met)
         del sm
     return {"workload": wl.C5_STREAM.name, "points": points}
+
+
+def _weight_adaptation(torch, om, windows: int = 14, kappa: float = 0.1):
+    """Weight adaptation (eq 45) as a host control loop on the 32-layer decode
+    stack (H = 3): each observation window is one decode step of the 64-token
+    batch through the stack.  After a window, T_bar = mean over tokens of the
+    modeled delay over the delay of pure exact execution on the same
+    deployment (the exact-only chain, allow_sub = 0), Q_bar = mean accumulated
+    loss over the per-token budget (eq 23's normalisation); the library's
+    eq-45 update gives the next (omega_Q, omega_T), with which Phi and the cost
+    tables are rebuilt."""
+    import workloads as wl
+    cfg = wl.C5_STREAM
+    sm = _stream_model(torch, om, cfg)
+    phi_x = _stream_lookahead(om, cfg, sm, cfg.H, cfg.omega_T, cfg.omega_Q, allow_sub=0)
+    t_ref = _token_delays(cfg, sm, _route_chain(torch, om, cfg, sm, _stream_layers(
+        torch, om, cfg, sm, phi_x, cfg.omega_T, cfg.omega_Q, allow_sub=0)))
+    wq, wt = cfg.omega_Q, cfg.omega_T
+    trace = []
+    for w in range(windows):
+        phi = _stream_lookahead(om, cfg, sm, cfg.H, wt, wq)
+        recs = _route_chain(torch, om, cfg, sm, _stream_layers(torch, om, cfg, sm, phi, wt, wq))
+        t_bar = float(np.mean(_token_delays(cfg, sm, recs) / t_ref))
+        q_bar = float(np.mean(recs[-1]["qhat_out"]) / cfg.Qbar)
+        met = _trajectory_metrics(cfg, sm, recs)
+        trace.append({"window": w, "omega_Q": wq, "omega_T": wt, "T_bar": t_bar, "Q_bar": q_bar,
+                      "remote_ratio": met["remote_ratio"], "classes_LE_LS_RE_RS": met["classes_LE_LS_RE_RS"]})
+        wq, wt = om.ordermoe_adapt_weights(wq, kappa, t_bar, q_bar)
+    return {"workload": cfg.name, "kappa": kappa, "H": cfg.H,
+            "exact_delay_ms_per_token": float(np.mean(t_ref) * 1e3), "windows": trace}
 
 
 def _decode_stream(torch, om, steps: int = 10, warmup: int = 2):
@@ -618,9 +656,11 @@ def main():
                     help="skip the quality-budget sweep of the DeepSeek-MoE-shaped layer")
     ap.add_argument("--no-horizon", action="store_true",
                     help="skip the look-ahead depth sweep H = 1..5 of the decode stack")
+    ap.add_argument("--no-adapt", action="store_true",
+                    help="skip the eq-45 weight-adaptation loop on the decode stack")
     ap.add_argument("--no-stream", action="store_true",
                     help="skip the 32-layer decode-stream measurement")
-    ap.add_argument("--only", choices=("layer", "simbuild", "stream", "sweep", "horizon"),
+    ap.add_argument("--only", choices=("layer", "simbuild", "stream", "sweep", "horizon", "adapt"),
                     help="run one leg alone (for profiling): the layer step without the other "
                          "legs, or only the similarity build / decode stream (prints that leg's "
                          "JSON object)")
@@ -657,9 +697,12 @@ def main():
     if args.only == "horizon":
         print(json.dumps(_horizon_sweep(torch, om)))
         return
+    if args.only == "adapt":
+        print(json.dumps(_weight_adaptation(torch, om)))
+        return
     if args.only == "layer":
         args.no_simbuild = args.no_stream = args.no_cpu_baseline = args.no_other_layers = True
-        args.no_sweep = args.no_horizon = True
+        args.no_sweep = args.no_horizon = args.no_adapt = True
     print("bench: setting up %s" % cfg.name, file=sys.stderr, flush=True)
     st = _setup(cfg, torch, om)
     torch.cuda.synchronize()
@@ -727,6 +770,10 @@ def main():
     if not args.no_horizon:
         print("bench: look-ahead depth sweep", file=sys.stderr, flush=True)
         res["horizon_sweep"] = _horizon_sweep(torch, om)
+        torch.cuda.empty_cache()
+    if not args.no_adapt:
+        print("bench: weight adaptation", file=sys.stderr, flush=True)
+        res["weight_adaptation"] = _weight_adaptation(torch, om)
         torch.cuda.empty_cache()
     if not args.no_stream:
         print("bench: decode stream", file=sys.stderr, flush=True)

@@ -224,6 +224,17 @@ int ordermoe_estimate_transitions(int32_t N, int32_t E, int64_t T_cal, const int
  * EINVAL unless 1 <= l <= N and theta_min <= theta_max. */
 int ordermoe_theta_layer(int32_t l, int32_t N, double theta_min, double theta_max, float* theta_out);
 
+/* Weight adaptation of the runtime cost (Section V-D, eq 45), host only: one
+ * update per observation window,
+ *   omega_Q' = min(1, max(0, omega_Q + kappa (Q_bar - T_bar))),  omega_T' = 1 - omega_Q',
+ * where T_bar is the window's average delay normalised by the delay of pure
+ * exact execution on the same deployment and Q_bar its average budget
+ * utilisation (accumulated loss over the per-token budget), both as in eq 23.
+ *   omega_Q in [0, 1]; kappa >= 0 (the step size); T_bar, Q_bar >= 0, finite;
+ *   omega_Q_out, omega_T_out host scalars.  EINVAL otherwise (nothing written). */
+int ordermoe_adapt_weights(double omega_Q, double kappa, double T_bar, double Q_bar, double* omega_Q_out,
+                           double* omega_T_out);
+
 /* ------------------------------------------------------------------------
  * Routing and server-expert selection of one layer (Section V, the per-layer
  * loop of Algorithm 2 for every token of a batch), on the device.

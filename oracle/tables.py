@@ -17,7 +17,9 @@
     estimated from top-1 transitions between consecutive layers on calibration
     tokens, rows with no observation are all zero; the future candidate sets
     drop the budget test (the future budget is unknown) and keep the pin rule;
-    Phi^{(0)} = 0 and the last layer's Phi = 0; the runtime uses Phi^{(H-1)}.
+    Phi^{(0)} = 0 and the last layer's Phi = 0; the runtime uses Phi^{(H-1)};
+  * weight adaptation (eq 45): omega_Q += kappa (Q_bar - T_bar), projected onto
+    [0, 1], omega_T = 1 - omega_Q.
 """
 from __future__ import annotations
 
@@ -151,3 +153,11 @@ def lookahead(H: int, P: Sequence[np.ndarray], x: Sequence[np.ndarray],
         return out
 
     return [phi(l, H - 1) for l in range(N)]
+
+
+def adapt_weights(omega_Q: float, kappa: float, T_bar: float, Q_bar: float):
+    """Section V-D, eq 45: omega_Q moves by kappa (Q_bar - T_bar), projected
+    onto [0, 1]; omega_T = 1 - omega_Q.  Returns (omega_Q, omega_T)."""
+    w = omega_Q + kappa * (Q_bar - T_bar)
+    w = min(1.0, max(0.0, w))
+    return w, 1.0 - w

@@ -337,3 +337,18 @@ extern "C" int ordermoe_theta_layer(int32_t l, int32_t N, double theta_min, doub
     clear_error();
     return ORDERMOE_OK;
 }
+
+extern "C" int ordermoe_adapt_weights(double omega_Q, double kappa, double T_bar, double Q_bar,
+                                      double* omega_Q_out, double* omega_T_out) {
+    if (!omega_Q_out || !omega_T_out || !(omega_Q >= 0.0 && omega_Q <= 1.0) || !(kappa >= 0.0) ||
+        !std::isfinite(kappa) || !(T_bar >= 0.0) || !std::isfinite(T_bar) || !(Q_bar >= 0.0) ||
+        !std::isfinite(Q_bar))
+        return fail(ORDERMOE_EINVAL, "adapt_weights: need omega_Q in [0,1], kappa >= 0, finite T_bar, Q_bar >= 0");
+    // eq 45: a projected step on omega_Q towards the objective that is further behind
+    double w = omega_Q + kappa * (Q_bar - T_bar);
+    w = w < 0.0 ? 0.0 : (w > 1.0 ? 1.0 : w);
+    *omega_Q_out = w;
+    *omega_T_out = 1.0 - w;
+    clear_error();
+    return ORDERMOE_OK;
+}

@@ -30,7 +30,7 @@ EXPORTS = ("ordermoe_last_error", "ordermoe_similarity_workspace_size", "ordermo
            "ordermoe_build_lookahead", "ordermoe_route_workspace_size", "ordermoe_route_select",
            "ordermoe_forward_workspace_size", "ordermoe_local_moe_forward",
            "ordermoe_pack_gate_up", "ordermoe_timing_enable", "ordermoe_timing_read",
-           "ordermoe_estimate_transitions", "ordermoe_theta_layer")
+           "ordermoe_estimate_transitions", "ordermoe_theta_layer", "ordermoe_adapt_weights")
 TIMING_NAME = 64
 
 
@@ -84,6 +84,8 @@ def lib() -> ctypes.CDLL:
     L.ordermoe_estimate_transitions.argtypes = [_I32, _I32, _I64, _P, _P]
     L.ordermoe_theta_layer.restype = ctypes.c_int
     L.ordermoe_theta_layer.argtypes = [_I32, _I32, _F64, _F64, _P]
+    L.ordermoe_adapt_weights.restype = ctypes.c_int
+    L.ordermoe_adapt_weights.argtypes = [_F64, _F64, _F64, _F64, _P, _P]
     L.ordermoe_group_experts.restype = ctypes.c_int
     L.ordermoe_group_experts.argtypes = [_I32, _P, _P, _F32, _F64, _P, _P, _P, _P]
     L.ordermoe_place.restype = ctypes.c_int
@@ -208,6 +210,15 @@ def ordermoe_theta_layer(l: int, N: int, theta_min: float, theta_max: float) -> 
     out = np.zeros(1, np.float32)
     _check(lib().ordermoe_theta_layer(l, N, theta_min, theta_max, out.ctypes.data_as(_P)))
     return float(out[0])
+
+
+def ordermoe_adapt_weights(omega_Q: float, kappa: float, T_bar: float, Q_bar: float):
+    """(omega_Q, omega_T) after one eq-45 update."""
+    wq = np.zeros(1, np.float64)
+    wt = np.zeros(1, np.float64)
+    _check(lib().ordermoe_adapt_weights(omega_Q, kappa, T_bar, Q_bar, wq.ctypes.data_as(_P),
+                                        wt.ctypes.data_as(_P)))
+    return float(wq[0]), float(wt[0])
 
 
 def ordermoe_group_experts(sim: np.ndarray, counts: np.ndarray, theta: float, alpha_f: float):

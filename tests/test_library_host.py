@@ -203,3 +203,34 @@ def test_workspace_sizes_are_monotone():
     s1 = om.lib().ordermoe_forward_workspace_size(ctypes.byref(ex), 100, 2)
     s2 = om.lib().ordermoe_forward_workspace_size(ctypes.byref(ex), 1000, 2)
     assert 0 < s1 < s2
+
+
+def test_weight_adaptation_oracle_pins():
+    """eq 45: a step of kappa (Q_bar - T_bar) on omega_Q, projected onto [0, 1],
+    with omega_T = 1 - omega_Q."""
+    from oracle import tables
+    # budget utilisation above the normalised delay: more weight on quality
+    wq, wt = tables.adapt_weights(0.5, 0.1, 0.8, 1.0)
+    assert wq == pytest.approx(0.52, rel=1e-15) and wt == pytest.approx(0.48, rel=1e-15)
+    # the other way round: more weight on delay
+    wq, _ = tables.adapt_weights(0.5, 0.1, 1.0, 0.2)
+    assert wq == pytest.approx(0.42, rel=1e-15)
+    # fixed point when both objectives are equally far behind
+    assert tables.adapt_weights(0.3, 0.7, 0.6, 0.6) == (0.3, 0.7)
+    # projection at both ends; kappa = 0 never moves
+    assert tables.adapt_weights(0.95, 1.0, 0.0, 1.0) == (1.0, 0.0)
+    assert tables.adapt_weights(0.05, 1.0, 1.0, 0.0) == (0.0, 1.0)
+    assert tables.adapt_weights(0.25, 0.0, 3.0, 0.0) == (0.25, 0.75)
+
+
+def test_library_weight_adaptation_matches_the_oracle():
+    from oracle import tables
+    from paper_2607_17154_amd import ordermoe as om
+    rng = np.random.default_rng(11)
+    for _ in range(200):
+        wq, kappa, tb, qb = rng.random(), rng.random() * 2, rng.random() * 2, rng.random() * 2
+        assert om.ordermoe_adapt_weights(wq, kappa, tb, qb) == tables.adapt_weights(wq, kappa, tb, qb)
+    for bad in ((-0.1, 0.1, 0.5, 0.5), (1.1, 0.1, 0.5, 0.5), (0.5, -1.0, 0.5, 0.5),
+                (0.5, 0.1, float("nan"), 0.5), (0.5, 0.1, 0.5, -0.1)):
+        with pytest.raises(om.OrderMoEError):
+            om.ordermoe_adapt_weights(*bad)
