@@ -269,7 +269,7 @@ def _other_layers(torch, om, steps: int = 10, warmup: int = 3):
         r_shared = int(ro[-1]) - r_routed
         fl_gu = 2.0 * cfg.d * 2 * cfg.f * r_routed + 2.0 * cfg.d * 2 * cfg.n_shared * cfg.f * r_shared
         fl_dn = fl_gu / 2
-        gu_us = avg.get("gemm_gate_up", 0.0) + avg.get("gemm_gate_up_tail", 0.0)
+        gu_us = sum(v for n, v in avg.items() if n.startswith("gemm_gate_up"))
         rt_bytes = cfg.T * cfg.d * 2 + cfg.E * cfg.d * 2 + cfg.T * cfg.k * 14 + cfg.T * 11
         rt_us = avg.get("route_select", float("nan"))
         res[key] = {"workload": cfg.name, "ms_per_step": ms, "tokens_per_s": cfg.T / (ms / 1e3),
@@ -728,7 +728,7 @@ def main():
     counters = st["out"]["counters"].cpu().numpy()
     # the gate/up GEMM is two launches per step: whole rounds of 256 x 256 tiles,
     # then the remaining tiles as 256 x 128 halves
-    gu_avg_s = sum(kt[n][0] / kt[n][1] for n in ("gemm_gate_up", "gemm_gate_up_tail") if n in kt) / 1e3
+    gu_avg_s = sum(v[0] / v[1] for n, v in kt.items() if n.startswith("gemm_gate_up")) / 1e3
     gu_flops = 2.0 * R * cfg.d * (2 * cfg.f)          # gate and up projections of R rows
     achieved = gu_flops / gu_avg_s / 1e12
     ms_step = ms / args.steps
