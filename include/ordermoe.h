@@ -194,7 +194,9 @@ int ordermoe_build_tables(int32_t E, int32_t M, const float* sim, const int32_t*
  *       layer l+1 of omega_T d_{l+1}(m',k''|m)/d_ref_{l+1}
  *       + omega_Q Q_{l+1}(k',k'')/Qbar + Phi_{l+1}^{(h-1)}(m',k'')
  * with Phi^{(0)} = 0 and 0 for the last layer.  The candidate sets drop the
- * budget test; with pin_local_exact a target deployed on m is kept on m.
+ * budget test; with pin_local_exact a target deployed on m is kept on m;
+ * allow_sub: 0 exact only, 1 substitutes on any server, 2 substitutes only on
+ * the source server m.
  *   N layers of E experts each (same E for all layers), M servers.
  *   P host [N-1][E][E] transition probabilities (rows may be all zero),
  *   x host [N][M][E], sim host [N][E][E] float, group_of host [N][E],
@@ -251,7 +253,8 @@ int ordermoe_adapt_weights(double omega_Q, double kappa, double T_bar, double Q_
  *   if pin_local_exact and r is deployed on s: (s, r), Q = 0;
  *   else argmin over the candidates of eq (40) -- (m, r) for every server m
  *   holding r, and (m, k) for k in t1[r] held by m with fp32 Qh + Q <= Qbar
- *   (only if allow_sub and Qbar > 0) -- of J = fmaf(omega_Q/Qbar, Q, S[s][m][k])
+ *   (only if allow_sub and Qbar > 0; allow_sub = 2 keeps only substitutes held by
+ *   s, the paper's Local Substitute Only baseline) -- of J = fmaf(omega_Q/Qbar, Q, S[s][m][k])
  *   (eq 43), ties by (Q, exact first, k, local first, m); then Qh += Q (eq 44).
  *   The token resides after the layer on slot 0's execution server.
  * Dispatch list: every (token, slot) whose execution server differs from

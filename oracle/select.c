@@ -97,6 +97,7 @@ int orc_select(int64_t T, int32_t k, int32_t E, int32_t M,
                     }
                     for (int m = 0; m < M; ++m) {
                         if (!x[(int64_t)m * E + kk]) continue;
+                        if (is_sub && allow_sub == 2 && m != s) continue;   /* local substitutes only */
                         cand_t c;
                         c.J = fmaf(cq, q, S[((int64_t)s * M + m) * E + kk]);
                         c.q = q; c.sub = is_sub; c.k = kk; c.remote = (m != s); c.m = m;

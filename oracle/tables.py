@@ -122,7 +122,9 @@ def lookahead(H: int, P: Sequence[np.ndarray], x: Sequence[np.ndarray],
             if (l1, r1) not in subs_memo:
                 subs_memo[(l1, r1)] = [kk for kk, _ in substitutes(sim32[l1], group_of[l1], theta[l1], r1)]
             ks += subs_memo[(l1, r1)]
-        return [(m1, k1) for k1 in ks for m1 in range(M) if x[l1][m1, k1]]
+        # allow_sub = 2: substitutes only on the source server (exact targets anywhere)
+        return [(m1, k1) for k1 in ks for m1 in range(M) if x[l1][m1, k1]
+                and not (allow_sub == 2 and k1 != r1 and m1 != s)]
 
     memo = {}
 

@@ -132,6 +132,7 @@ extern "C" int ordermoe_route_select(const ordermoe_layer* L, const void* x, int
     if (L->M < 1 || L->M > ORDERMOE_MAX_SERVERS) return fail(ORDERMOE_EINVAL, "route_select: M out of range");
     if (L->gmax < 1 || L->gmax > ORDERMOE_MAX_SUBS) return fail(ORDERMOE_EINVAL, "route_select: gmax out of range");
     if (!(L->Qbar >= 0.0f) || !(L->omega_Q >= 0.0f)) return fail(ORDERMOE_EINVAL, "route_select: Qbar and omega_Q must be >= 0");
+    if (L->allow_sub < 0 || L->allow_sub > 2) return fail(ORDERMOE_EINVAL, "route_select: allow_sub must be 0, 1 or 2");
     if (T < 0) return fail(ORDERMOE_EINVAL, "route_select: T < 0");
     if (T > ((int64_t)1 << 31) / ORDERMOE_MAX_TOPK) return fail(ORDERMOE_EINVAL, "route_select: T too large");
     if (!L->w_router || !L->t1_k || !L->t1_q || !L->t1_n || !L->srvmask || !L->S)

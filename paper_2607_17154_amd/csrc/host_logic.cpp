@@ -246,6 +246,7 @@ extern "C" int ordermoe_build_lookahead(int32_t N, int32_t E, int32_t M, int32_t
     if ((N > 1 && !P) || !x || !sim || !group_of || !theta || !z_bits || !c || !d_ref || !B || !tau ||
         !F || !phi_out)
         return fail(ORDERMOE_EINVAL, "build_lookahead: null pointer");
+    if (allow_sub < 0 || allow_sub > 2) return fail(ORDERMOE_EINVAL, "build_lookahead: allow_sub must be 0, 1 or 2");
     const size_t ME = (size_t)M * E;
     // cost of the best next-layer candidate of target r1 at layer l1 from source s,
     // plus that candidate's own cost-to-go (eq 42's inner minimum)
@@ -271,6 +272,7 @@ extern "C" int ordermoe_build_lookahead(int32_t N, int32_t E, int32_t M, int32_t
             }
             for (int m1 = 0; m1 < M; ++m1) {
                 if (!xl[(size_t)m1 * E + k1]) continue;
+                if (allow_sub == 2 && k1 != r1 && m1 != s) continue;   // local substitutes only
                 double v = g_of(m1, k1);
                 if (!have || v < best) { best = v; have = true; }
             }

@@ -583,7 +583,10 @@ route_select_kernel(const RouteArgs a) {
     }
 #pragma unroll
     for (int slot = 0; slot < ORDERMOE_MAX_TOPK; ++slot)
-        if (slot < k && search[slot] && ke[slot] >= 0) msv[slot] = s_mask[ke[slot]] & mmask;
+        if (slot < k && search[slot] && ke[slot] >= 0) {
+            msv[slot] = s_mask[ke[slot]] & mmask;
+            if (a.allow_sub == 2 && j >= 1) msv[slot] &= 1u << s_loc;   // local substitutes only
+        }
     // servers holding each candidate, one per round for every slot together
     for (;;) {
         uint32_t any = 0;

@@ -272,11 +272,12 @@ def stream_library_tables(sc: StreamCase, gmax: int = 15):
     return theta32, phi, tabs
 
 
-def with_horizon(sc: StreamCase, H: int) -> StreamCase:
-    """The same stack with the look-ahead depth H (eq 42): the oracle's Phi and
-    cost tables recomputed, everything else shared."""
+def with_horizon(sc: StreamCase, H: int, allow_sub: Optional[int] = None) -> StreamCase:
+    """The same stack with the look-ahead depth H (eq 42), and optionally
+    another substitution mode: the oracle's Phi and cost tables recomputed,
+    everything else shared."""
     import dataclasses
-    cfg = dataclasses.replace(sc.cfg, H=H)
+    cfg = dataclasses.replace(sc.cfg, H=H, allow_sub=sc.cfg.allow_sub if allow_sub is None else allow_sub)
     groups = [m["group_of"] for m in sc.models]
     phi = tables.lookahead(H, sc.P, sc.x_dep, sc.sim32, groups, sc.theta, [sc.z_bits] * cfg.N, sc.net.B,
                            sc.net.tau, [sc.c] * cfg.N, sc.net.F, [sc.dref] * cfg.N, cfg.omega_T, cfg.omega_Q,

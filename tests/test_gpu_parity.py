@@ -27,6 +27,8 @@ SMALL = {
     "C2s": wl.C2.with_(T=1000, T_cal=4096),
     "C3s": wl.C3.with_(T=1500, T_cal=4096),
     "C4s": wl.C4.with_(T=1700, T_cal=4096),
+    # the Local Substitute Only baseline: substitutes only on the token's server
+    "C3s_local_sub": wl.C3.with_(T=1500, T_cal=4096, allow_sub=2),
 }
 # decode-sized batches (at most 128 tokens): the thin-GEMM path of the forward
 DECODE = {

@@ -134,12 +134,13 @@ def test_chain_decisions_match_the_oracle(stream_case, chain, oracle_chain):
     assert exhausted_layer is not None and 4 <= exhausted_layer < stream_case.cfg.N - 4
 
 
-@pytest.mark.parametrize("H", [1, 5])
-def test_chain_decisions_match_the_oracle_at_other_horizons(stream_case, H):
+@pytest.mark.parametrize("H,allow_sub", [(1, 1), (5, 1), (3, 2)])
+def test_chain_decisions_match_the_oracle_at_other_horizons(stream_case, H, allow_sub):
     """The look-ahead sweep of Fig. 7: the myopic rule (H = 1) and the deepest
-    horizon swept (H = 5) run the same chain comparison."""
+    horizon swept (H = 5) run the same chain comparison, and so does the Local
+    Substitute Only mode (allow_sub = 2)."""
     from ._pipeline import with_horizon
-    sc = with_horizon(stream_case, H)
+    sc = with_horizon(stream_case, H, allow_sub=allow_sub)
     g = _gpu_chain(sc)
     _compare_chain(sc, g["layers"], _oracle_chain(sc, g["layers"]))
 

@@ -40,6 +40,8 @@ def _brute_select_token(r_list, s, qhat, x, sim, group_of, theta, S, Qbar, omega
                 else:
                     if not (allow and Qbar > 0):
                         continue
+                    if allow == 2 and m != s:      # local substitutes only
+                        continue
                     in_v = group_of[kk] == group_of[r] and np.float32(sim[r, kk]) >= np.float32(theta)
                     if not in_v:
                         continue
@@ -83,7 +85,7 @@ def test_select_matches_exhaustive_enumeration(pin):
     rng = np.random.default_rng(10 + pin)
     for trial in range(40):
         L = _random_layer(rng, 60)
-        allow = int(rng.integers(0, 2))
+        allow = int(rng.integers(0, 3))
         o = layer.select(L["idx"], L["x"], L["sim"], L["group_of"], L["theta"], L["S"],
                          L["Qbar"], 0.5, L["loc"], L["qhat"], pin, allow)
         for t in range(60):

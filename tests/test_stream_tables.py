@@ -122,3 +122,19 @@ def test_library_lookahead_matches_the_oracle_at_every_horizon(stream_case, H):
         assert all(np.all(p == 0) for p in phi)
     else:
         assert any(np.any(p > 0) for p in phi)
+
+
+def test_library_lookahead_matches_the_oracle_with_local_substitutes_only(stream_case):
+    """The Local Substitute Only mode (allow_sub = 2): the future candidate sets
+    keep substitutes on the source server only; library and oracle agree bit
+    for bit."""
+    from tests._pipeline import stream_library_tables, with_horizon
+    sc = with_horizon(stream_case, 3, allow_sub=2)
+    _, phi, tabs = stream_library_tables(sc)
+    for l in range(sc.cfg.N):
+        np.testing.assert_array_equal(phi[l], sc.phi[l])
+        np.testing.assert_array_equal(tabs[l]["S"].view(np.uint32), sc.S[l].view(np.uint32))
+    # fewer future candidates can only raise each minimum
+    ref = with_horizon(stream_case, 3)
+    for l in range(sc.cfg.N):
+        assert np.all(phi[l] >= ref.phi[l])
