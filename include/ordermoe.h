@@ -11,6 +11,7 @@
  *
  *   ordermoe_build_similarity   Section III-B / IV-A, eq (3)-(5), (24)-(28)
  *   ordermoe_place              Section IV-B / IV-C, eq (29)-(35), Algorithm 1
+ *   ordermoe_place_random       Section VI-A, the Random Deployment baseline
  *   ordermoe_build_tables       eq (6)-(8), (18), (37)-(38) (+ eq (42) input)
  *   ordermoe_route_select       router + Section V, eq (36)-(44), Algorithm 2
  *   ordermoe_local_moe_forward  execution of the selected (server, expert)
@@ -151,7 +152,10 @@ int ordermoe_group_experts(int32_t E, const float* sim, const int64_t* counts, f
  * when memory is fragmented, exactly as the algorithm states; used_out shows it.
  * Redundant part (if `redundancy`), over all layers: repeatedly the replica
  * of largest positive benefit pi_m I_j (1 - y_{m,l,g(j)}) / p_j that fits
- * (eq 32-35; ties: lower (layer, server, expert)).
+ * (eq 32-35; ties: lower (layer, server, expert)).  redundancy = 2 drops the
+ * group-coverage factor, B = pi_m w_j / p_j with w the given per-expert
+ * weights: with activation frequencies as w this is the paper's
+ * Popularity-based Replication baseline (Section VI-A).
  *
  *   N layers; E_l host [N] experts per layer; M servers (<= ORDERMOE_MAX_SERVERS)
  *   group_of, importance, p   host, concatenated over layers (sum E_l entries)
@@ -209,6 +213,17 @@ int ordermoe_build_lookahead(int32_t N, int32_t E, int32_t M, int32_t H, const d
                              const double* d_ref, const double* B, const double* tau,
                              const double* F, double omega_T, double omega_Q, float Qbar,
                              int32_t pin_local_exact, int32_t allow_sub, double* phi_out);
+
+/* The paper's Random Deployment baseline (Section VI-A), host only: every
+ * expert once, layer by layer in index order, on a server drawn uniformly
+ * from the memory-feasible ones (none: the server with the most remaining
+ * memory, ties to the lower index); then, if `redundancy`, every (layer,
+ * server, expert) without a copy, in an order shuffled by Fisher-Yates, is
+ * placed when it fits.  The draws come from SplitMix64 seeded with `seed`
+ * (uniform integers below n as next() % n).  Same layouts as ordermoe_place;
+ * ECAPACITY if sum(p) > sum(C), EINVAL for bad sizes or non-positive p, C. */
+int ordermoe_place_random(int32_t N, const int32_t* E_l, int32_t M, const double* p, const double* C,
+                          uint64_t seed, int32_t redundancy, uint8_t* x_out, double* used_out);
 
 /* Transition probabilities between consecutive layers (eq 41), host only:
  * P_l[k][k'] = the share of the calibration tokens with top-1 expert k at

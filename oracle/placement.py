@@ -18,6 +18,18 @@ Redundant placement, over all layers (eq 32-35), greedy:
   * repeatedly deploy the candidate of largest positive benefit (ties: lower
     (l, m, j)), update y and b, until none is left.
 Reading of eq 32: the sum runs over the experts k of group g(j) in layer l.
+
+Baselines of Section VI-A (readings; the paper names them without giving
+their procedure):
+  * Popularity-based Replication (`redundancy=2`): the redundant part above
+    with benefit pi_m w_j / p_j, i.e. without the group-coverage factor;
+    the caller passes activation frequencies as w.
+  * Random Deployment (`place_random`): each expert once, layer by layer in
+    index order, on a server drawn uniformly from the memory-feasible ones
+    (none feasible: the most remaining memory, ties to the lower index);
+    then every (l, m, j) without a copy, in a Fisher-Yates-shuffled order,
+    is placed if it fits.  Draws come from SplitMix64 (Steele, Lea and
+    Flood, OOPSLA 2014), a uniform integer below n being next() % n.
 fp64 throughout.  The benefit of every candidate is evaluated elementwise with
 numpy (same operations and order per candidate as the formula above); the
 layers are padded to a common expert count with zero-importance entries,
@@ -36,8 +48,9 @@ class CapacityError(ValueError):
 
 def place(group_of: Sequence[np.ndarray], importance: Sequence[np.ndarray],
           p: Sequence[np.ndarray], C: np.ndarray, pi: np.ndarray,
-          lambda1: float = 0.5, redundancy: bool = True):
-    """Returns (x: list over layers of [M, E_l] uint8, b [M] used memory)."""
+          lambda1: float = 0.5, redundancy=True):
+    """Returns (x: list over layers of [M, E_l] uint8, b [M] used memory).
+    redundancy: False/0 none, True/1 eq 33, 2 popularity (no (1 - y) factor)."""
     N = len(group_of)
     M = len(C)
     lambda2 = 1.0 - lambda1
@@ -94,7 +107,10 @@ def place(group_of: Sequence[np.ndarray], importance: Sequence[np.ndarray],
                 for kk in np.nonzero(X[l, m])[0]:
                     y[l, m, same[l, kk]] = 1
         while True:
-            Bnf = pim[None, :, None] * I[:, None, :] * (1 - y) / P[:, None, :]
+            if redundancy == 2:
+                Bnf = pim[None, :, None] * I[:, None, :] / P[:, None, :] * np.ones_like(y)
+            else:
+                Bnf = pim[None, :, None] * I[:, None, :] * (1 - y) / P[:, None, :]
             fits = (b[None, :, None] + P[:, None, :]) <= np.asarray(C)[None, :, None]
             cand = (X == 0) & fits & (Bnf > 0)
             if not cand.any():
@@ -106,4 +122,59 @@ def place(group_of: Sequence[np.ndarray], importance: Sequence[np.ndarray],
             y[l, m, same[l, j]] = 1
             x[l][m, j] = 1
             b[m] += p[l][j]
+    return x, b
+
+
+MASK64 = (1 << 64) - 1
+
+
+class SplitMix64:
+    """SplitMix64 from its published definition: add the golden-ratio
+    increment 0x9E3779B97F4A7C15 to the state, then mix the state with
+    xor-shift 30 / multiply 0xBF58476D1CE4E5B9 / xor-shift 27 / multiply
+    0x94D049BB133111EB / xor-shift 31, all modulo 2^64."""
+
+    def __init__(self, seed: int):
+        self.state = seed & MASK64
+
+    def next(self) -> int:
+        self.state = (self.state + 0x9E3779B97F4A7C15) & MASK64
+        z = self.state
+        z = ((z ^ (z >> 30)) * 0xBF58476D1CE4E5B9) & MASK64
+        z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & MASK64
+        return z ^ (z >> 31)
+
+    def below(self, n: int) -> int:
+        return self.next() % n
+
+
+def place_random(p: Sequence[np.ndarray], C: np.ndarray, seed: int, redundancy: bool = True):
+    """Random Deployment baseline (Section VI-A; reading in the module
+    header).  Returns (x: list over layers of [M, E_l] uint8, b [M])."""
+    N = len(p)
+    M = len(C)
+    if sum(float(np.sum(pl)) for pl in p) > float(np.sum(C)):
+        raise CapacityError("total expert memory exceeds the servers' capacity")
+    rng = SplitMix64(seed)
+    b = np.zeros(M)
+    x: List[np.ndarray] = [np.zeros((M, len(pl)), dtype=np.uint8) for pl in p]
+    for l in range(N):
+        for j in range(len(p[l])):
+            feasible = [m for m in range(M) if b[m] + p[l][j] <= C[m]]
+            if feasible:
+                m = feasible[rng.below(len(feasible))]
+            else:
+                m = max(range(M), key=lambda q: (C[q] - b[q], -q))
+            x[l][m, j] = 1
+            b[m] += p[l][j]
+    if redundancy:
+        cand = [(l, m, j) for l in range(N) for m in range(M) for j in range(len(p[l]))
+                if x[l][m, j] == 0]
+        for i in range(len(cand) - 1, 0, -1):        # Fisher-Yates, from the end
+            r = rng.below(i + 1)
+            cand[i], cand[r] = cand[r], cand[i]
+        for (l, m, j) in cand:
+            if b[m] + p[l][j] <= C[m]:
+                x[l][m, j] = 1
+                b[m] += p[l][j]
     return x, b

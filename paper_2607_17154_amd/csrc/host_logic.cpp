@@ -76,6 +76,7 @@ extern "C" int ordermoe_place(int32_t N, const int32_t* E_l, int32_t M, const in
     if (N < 1 || M < 1 || M > ORDERMOE_MAX_SERVERS) return fail(ORDERMOE_EINVAL, "place: N or M out of range");
     if (!E_l || !group_of || !importance || !p || !C || !pi || !x_out || !used_out)
         return fail(ORDERMOE_EINVAL, "place: null pointer");
+    if (redundancy < 0 || redundancy > 2) return fail(ORDERMOE_EINVAL, "place: redundancy must be 0, 1 or 2");
     std::vector<size_t> base(N + 1, 0);
     for (int l = 0; l < N; ++l) {
         if (E_l[l] < 1 || E_l[l] > ORDERMOE_MAX_EXPERTS) return fail(ORDERMOE_EINVAL, "place: E_l out of range");
@@ -149,7 +150,9 @@ extern "C" int ordermoe_place(int32_t N, const int32_t* E_l, int32_t M, const in
                     for (int j = 0; j < E; ++j) {
                         const double pj = p[base[l] + j];
                         if (X(l, m, j) || !(b[m] + pj <= C[m])) continue;             // eq 35
-                        double B = pi[m] * importance[base[l] + j] * (1 - y[g[j]]) / pj;  // eq 33
+                        // eq 33; redundancy = 2 drops the group-coverage factor (popularity replication)
+                        double B = redundancy == 2 ? pi[m] * importance[base[l] + j] / pj
+                                                   : pi[m] * importance[base[l] + j] * (1 - y[g[j]]) / pj;
                         if (!(B > 0.0)) continue;
                         if (bl < 0 || B > bestB) { bestB = B; bl = l; bm = m; bj = j; }
                     }
@@ -351,6 +354,85 @@ extern "C" int ordermoe_adapt_weights(double omega_Q, double kappa, double T_bar
     w = w < 0.0 ? 0.0 : (w > 1.0 ? 1.0 : w);
     *omega_Q_out = w;
     *omega_T_out = 1.0 - w;
+    clear_error();
+    return ORDERMOE_OK;
+}
+
+// SplitMix64 (Steele, Lea and Flood, OOPSLA 2014): the state advances by the
+// golden-ratio constant, the output is a two-multiply mix of the state.
+namespace {
+struct SplitMix64 {
+    uint64_t state;
+    uint64_t next() {
+        uint64_t z = (state += 0x9E3779B97F4A7C15ull);
+        z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+        z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+        return z ^ (z >> 31);
+    }
+    uint64_t below(uint64_t n) { return next() % n; }
+};
+}  // namespace
+
+extern "C" int ordermoe_place_random(int32_t N, const int32_t* E_l, int32_t M, const double* p, const double* C,
+                                     uint64_t seed, int32_t redundancy, uint8_t* x_out, double* used_out) {
+    if (N < 1 || M < 1 || M > ORDERMOE_MAX_SERVERS) return fail(ORDERMOE_EINVAL, "place_random: N or M out of range");
+    if (!E_l || !p || !C || !x_out || !used_out) return fail(ORDERMOE_EINVAL, "place_random: null pointer");
+    std::vector<size_t> base(N + 1, 0);
+    for (int l = 0; l < N; ++l) {
+        if (E_l[l] < 1 || E_l[l] > ORDERMOE_MAX_EXPERTS) return fail(ORDERMOE_EINVAL, "place_random: E_l out of range");
+        base[l + 1] = base[l] + (size_t)E_l[l];
+    }
+    double need = 0.0, have = 0.0;
+    for (size_t i = 0; i < base[N]; ++i) {
+        if (!(p[i] > 0.0)) return fail(ORDERMOE_EINVAL, "place_random: memory demand p must be positive");
+        need += p[i];
+    }
+    for (int m = 0; m < M; ++m) {
+        if (!(C[m] > 0.0)) return fail(ORDERMOE_EINVAL, "place_random: capacity C must be positive");
+        have += C[m];
+    }
+    if (need > have) return fail(ORDERMOE_ECAPACITY, "place_random: total expert memory exceeds total capacity");
+    SplitMix64 rng{seed};
+    std::vector<double> b(M, 0.0);
+    std::vector<uint8_t> x((size_t)M * base[N], 0);
+    auto X = [&](int l, int m, int j) -> uint8_t& { return x[(size_t)M * base[l] + (size_t)m * E_l[l] + j]; };
+    // every expert once, on a uniformly drawn memory-feasible server (none: the
+    // server with the most remaining memory, ties to the lower index)
+    std::vector<int> feas;
+    for (int l = 0; l < N; ++l)
+        for (int j = 0; j < E_l[l]; ++j) {
+            const double pj = p[base[l] + j];
+            feas.clear();
+            for (int m = 0; m < M; ++m)
+                if (b[m] + pj <= C[m]) feas.push_back(m);
+            int m;
+            if (!feas.empty()) {
+                m = feas[(size_t)rng.below(feas.size())];
+            } else {
+                m = 0;
+                for (int q = 1; q < M; ++q)
+                    if (C[q] - b[q] > C[m] - b[m]) m = q;
+            }
+            X(l, m, j) = 1;
+            b[m] += pj;
+        }
+    // replicas: every (layer, server, expert) without a copy, in an order shuffled
+    // by Fisher-Yates, each placed if it fits
+    if (redundancy) {
+        std::vector<uint64_t> cand;
+        for (int l = 0; l < N; ++l)
+            for (int m = 0; m < M; ++m)
+                for (int j = 0; j < E_l[l]; ++j)
+                    if (!X(l, m, j)) cand.push_back(((uint64_t)l << 40) | ((uint64_t)m << 20) | (uint64_t)j);
+        for (size_t i = cand.size(); i > 1; --i) std::swap(cand[i - 1], cand[(size_t)rng.below(i)]);
+        for (uint64_t c : cand) {
+            const int l = (int)(c >> 40), m = (int)((c >> 20) & 0xFFFFF), j = (int)(c & 0xFFFFF);
+            const double pj = p[base[l] + j];
+            if (b[m] + pj <= C[m]) { X(l, m, j) = 1; b[m] += pj; }
+        }
+    }
+    std::copy(x.begin(), x.end(), x_out);
+    std::copy(b.begin(), b.end(), used_out);
     clear_error();
     return ORDERMOE_OK;
 }

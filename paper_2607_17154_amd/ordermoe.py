@@ -30,7 +30,8 @@ EXPORTS = ("ordermoe_last_error", "ordermoe_similarity_workspace_size", "ordermo
            "ordermoe_build_lookahead", "ordermoe_route_workspace_size", "ordermoe_route_select",
            "ordermoe_forward_workspace_size", "ordermoe_local_moe_forward",
            "ordermoe_pack_gate_up", "ordermoe_timing_enable", "ordermoe_timing_read",
-           "ordermoe_estimate_transitions", "ordermoe_theta_layer", "ordermoe_adapt_weights")
+           "ordermoe_estimate_transitions", "ordermoe_theta_layer", "ordermoe_adapt_weights",
+           "ordermoe_place_random")
 TIMING_NAME = 64
 
 
@@ -90,6 +91,8 @@ def lib() -> ctypes.CDLL:
     L.ordermoe_group_experts.argtypes = [_I32, _P, _P, _F32, _F64, _P, _P, _P, _P]
     L.ordermoe_place.restype = ctypes.c_int
     L.ordermoe_place.argtypes = [_I32, _P, _I32, _P, _P, _P, _P, _P, _F64, _I32, _P, _P]
+    L.ordermoe_place_random.restype = ctypes.c_int
+    L.ordermoe_place_random.argtypes = [_I32, _P, _I32, _P, _P, ctypes.c_uint64, _I32, _P, _P]
     L.ordermoe_build_tables.restype = ctypes.c_int
     L.ordermoe_build_tables.argtypes = [_I32, _I32, _P, _P, _F32, _P, _P, _P, _P, _F64, _P, _F64,
                                         _F64, _P, _I32, _P, _P, _P, _P, _P]
@@ -250,6 +253,25 @@ def ordermoe_place(group_of: Sequence[np.ndarray], importance: Sequence[np.ndarr
     used = np.zeros(M, np.float64)
     _check(lib().ordermoe_place(N, E_l.ctypes.data_as(_P), M, gp, ip, ppp, Cp, pip, lambda1,
                                 redundancy, x.ctypes.data_as(_P), used.ctypes.data_as(_P)))
+    out, off = [], 0
+    for e in E_l:
+        out.append(x[off:off + M * e].reshape(M, e).copy())
+        off += M * e
+    return out, used
+
+
+def ordermoe_place_random(p: Sequence[np.ndarray], C, seed: int, redundancy: int = 1):
+    """Random Deployment: returns (list of [M, E_l] uint8 deployments, used memory [M])."""
+    N = len(p)
+    E_l = np.array([len(v) for v in p], dtype=np.int32)
+    M = len(C)
+    pp, ppp = _host(np.concatenate([np.asarray(v) for v in p]), np.float64)
+    Cc, Cp = _host(C, np.float64, M)
+    x = np.zeros(int(M * E_l.sum()), np.uint8)
+    used = np.zeros(M, np.float64)
+    _check(lib().ordermoe_place_random(N, E_l.ctypes.data_as(_P), M, ppp, Cp,
+                                       int(seed) & 0xFFFFFFFFFFFFFFFF, redundancy,
+                                       x.ctypes.data_as(_P), used.ctypes.data_as(_P)))
     out, off = [], 0
     for e in E_l:
         out.append(x[off:off + M * e].reshape(M, e).copy())

@@ -78,12 +78,43 @@ def test_place_matches_oracle_random():
         while C.sum() < need * 1.2:
             C[int(rng.integers(0, M))] += 2
         pi = rng.random(M)
-        red = int(rng.integers(0, 2))
-        x_or, b_or = placement.place(group_of, imp, p, C, pi, 0.5, bool(red))
+        red = int(rng.integers(0, 3))
+        x_or, b_or = placement.place(group_of, imp, p, C, pi, 0.5, red)
         x_lib, b_lib = om.ordermoe_place(group_of, imp, p, C, pi, 0.5, red)
         for l in range(N):
             np.testing.assert_array_equal(x_lib[l], x_or[l])
         np.testing.assert_array_equal(b_lib, b_or)
+
+
+def test_place_random_matches_oracle():
+    rng = np.random.default_rng(12)
+    for trial in range(25):
+        N, M = int(rng.integers(1, 4)), int(rng.integers(2, 9))
+        p = [rng.integers(1, 4, size=int(rng.integers(3, 20))).astype(float) for _ in range(N)]
+        need = sum(v.sum() for v in p)
+        C = rng.integers(2, 9, size=M).astype(float)
+        while C.sum() < need * float(rng.uniform(1.0, 2.5)):
+            C[int(rng.integers(0, M))] += 1
+        seed = int(rng.integers(0, 2 ** 63)) * 2 + 1
+        red = int(rng.integers(0, 2))
+        x_or, b_or = placement.place_random(p, C, seed, bool(red))
+        x_lib, b_lib = om.ordermoe_place_random(p, C, seed, red)
+        for l in range(N):
+            np.testing.assert_array_equal(x_lib[l], x_or[l])
+        np.testing.assert_array_equal(b_lib, b_or)
+
+
+def test_place_random_rejects_bad_input():
+    with pytest.raises(om.OrderMoEError) as ei:
+        om.ordermoe_place_random([np.ones(3)], [1.0, 1.0], 0)
+    assert ei.value.code == om.ECAPACITY
+    with pytest.raises(om.OrderMoEError) as ei:
+        om.ordermoe_place_random([np.array([1.0, 0.0])], [4.0, 4.0], 0)
+    assert ei.value.code == om.EINVAL
+    with pytest.raises(om.OrderMoEError) as ei:
+        om.ordermoe_place([np.array([0, 1])], [np.ones(2)], [np.ones(2)], [4.0, 4.0], [0.5, 0.5],
+                          0.5, 3)
+    assert ei.value.code == om.EINVAL
 
 
 def test_place_capacity_error():
