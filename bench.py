@@ -351,15 +351,15 @@ def _quality_sweep(torch, om):
             "weights": "device draws, N(0, 0.02^2) bf16; routers, tokens and deployment as the layer"}
 
 
-def _stream_model(torch, om, cfg):
-    """The stack's offline model through the library: per layer the similarity
-    build on the GPU (with the top-1 of each calibration token), then the
-    transition estimate (eq 41) and the joint deployment (Algorithm 1) on the
-    host."""
+def _stream_base(torch, om, cfg):
+    """The stack's similarity models through the library: per layer the
+    similarity build on the GPU (with the top-1 of each calibration token),
+    then the transition estimate (eq 41) on the host.  None of it depends on
+    the servers or their memory."""
     import workloads as wl
     dev = "cuda"
     up = lambda a: torch.from_numpy(wl.bf16_bits(a).view(np.int16)).view(torch.bfloat16).to(dev)
-    N, E, M, k = cfg.N, cfg.E, cfg.M, cfg.k
+    N, E, k = cfg.N, cfg.E, cfg.k
     W = wl.stream_routers(cfg)
     theta = [om.ordermoe_theta_layer(l + 1, N, cfg.theta_min, cfg.theta_max) for l in range(N)]
     ws = torch.empty(om.ordermoe_similarity_workspace_size(cfg.T_cal, cfg.d, E), dtype=torch.uint8,
@@ -372,15 +372,57 @@ def _stream_model(torch, om, cfg):
                                                    top1=top1[l]))
     del ws
     P = om.ordermoe_estimate_transitions(top1.cpu().numpy(), E)
-    x_dep, _ = om.ordermoe_place([m["group_of"] for m in models], [m["importance"] for m in models],
-                                 [np.ones(E)] * N, np.array(cfg.capacity), np.full(M, 1.0 / M),
-                                 cfg.lambda1, 1)
-    net = wl.network(cfg)
+    return dict(theta=theta, w_router=w_router, models=models, P=P,
+                X=[up(x) for x in wl.stream_tokens(cfg)])
+
+
+# deployments of the variant study: Algorithm 1 and its ablations, and the two
+# deployment baselines of Section VI-A
+DEPLOYMENTS = ("ordermoe", "no_redundancy", "no_dispersion", "popularity", "random")
+
+
+def _stream_deploy(om, cfg, base, mode="ordermoe", net=None):
+    """A deployment of the stack on cfg.M servers of cfg.capacity (Algorithm 1
+    unless `mode` names a variant) with the network and per-step costs of
+    eq 37-38."""
+    import workloads as wl
+    N, E, M = cfg.N, cfg.E, cfg.M
+    ones, C = [np.ones(E)] * N, np.array(cfg.capacity)
+    if mode == "random":
+        x_dep, _ = om.ordermoe_place_random(ones, C, cfg.seed, 1)
+    else:
+        groups = [m["group_of"] for m in base["models"]]
+        if mode == "popularity":      # replicas by activation frequency (counts over the calibration set)
+            w = [m["counts"] / max(1, int(np.sum(m["counts"]))) for m in base["models"]]
+        else:
+            w = [m["importance"] for m in base["models"]]
+        lam = 1.0 if mode == "no_dispersion" else cfg.lambda1
+        red = {"no_redundancy": 0, "popularity": 2}.get(mode, 1)
+        x_dep, _ = om.ordermoe_place(groups, w, ones, C, np.full(M, 1.0 / M), lam, red)
+    net = wl.network(cfg) if net is None else net
     c = np.full(E, 6.0 * cfg.d * cfg.f)
     dref = float(np.mean(c)) / float(np.mean(net.F))
     z_bits = 8.0 * cfg.d * cfg.bytes_per_el
-    return dict(theta=theta, w_router=w_router, models=models, P=P, x_dep=x_dep, net=net, c=c, dref=dref,
-                z_bits=z_bits, X=[up(x) for x in wl.stream_tokens(cfg)])
+    return dict(base, x_dep=x_dep, net=net, c=c, dref=dref, z_bits=z_bits, deployment=mode)
+
+
+def _stream_model(torch, om, cfg):
+    """The stack's offline model: similarity models, transitions and the joint
+    deployment (Algorithm 1)."""
+    return _stream_deploy(om, cfg, _stream_base(torch, om, cfg))
+
+
+def _group_coverage(cfg, sm):
+    """Local group coverage: over layers and servers, the share of the layer's
+    similarity groups with at least one member on the server (the y of eq 32,
+    averaged)."""
+    cov = []
+    for l, md in enumerate(sm["models"]):
+        g = np.asarray(md["group_of"])
+        ng = len(set(g.tolist()))
+        for m in range(cfg.M):
+            cov.append(len(set(g[sm["x_dep"][l][m] == 1].tolist())) / ng)
+    return float(np.mean(cov))
 
 
 def _stream_lookahead(om, cfg, sm, H, omega_T, omega_Q, allow_sub=None):
@@ -490,6 +532,77 @@ def _horizon_sweep(torch, om):
             points.append(met)
         del sm
     return {"workload": wl.C5_STREAM.name, "points": points}
+
+
+def _run_variant(torch, om, cfg, sm, H, allow_sub):
+    phi = _stream_lookahead(om, cfg, sm, H, cfg.omega_T, cfg.omega_Q, allow_sub=allow_sub)
+    layers = _stream_layers(torch, om, cfg, sm, phi, cfg.omega_T, cfg.omega_Q, allow_sub=allow_sub)
+    met = _trajectory_metrics(cfg, sm, _route_chain(torch, om, cfg, sm, layers))
+    cls = met["classes_LE_LS_RE_RS"]
+    met.update(local_ratio=(cls[0] + cls[1]) / max(1, sum(cls)), group_coverage=_group_coverage(cfg, sm),
+               H=H, allow_sub=allow_sub, deployment=sm["deployment"])
+    return met
+
+
+def _variants(torch, om):
+    """The paper's in-method variants and deployment baselines (Section VI-A,
+    Fig. 4, 5, 9, 10, 12a) on the 32-layer decode stack, every one through the
+    same route/select kernel and host tables: per variant the modeled delay
+    along the realized trajectories (eq 37), cross-server transfers, slot
+    classes, budget used and local group coverage.
+      * variants, at the stack's per-token budget and at one that lasts the
+        stack: full OrderMoE (H = 3); without look-ahead (H = 1); without
+        redundancy; without same-group dispersion (lambda2 = 0); Similarity
+        Deployment without Substitute (exact only); Local Substitute Only;
+        Popularity-based Replication; Random Deployment;
+      * memory ratio 1.0 .. 3.0, Algorithm 1 against popularity replication
+        (Fig. 9: local group coverage and delay);
+      * 4 .. 16 servers at memory ratio 2.0, OrderMoE against exact-only
+        execution on the same deployment (Fig. 12a); servers 0..M-1 are the
+        leading rows of one 16-server network, so adding servers keeps the
+        others' links and speeds."""
+    import workloads as wl
+    cfg = wl.C5_STREAM
+    base = _stream_base(torch, om, cfg)
+    H = cfg.H
+    out = {"workload": cfg.name, "H": H}
+    runs = [("ordermoe", "ordermoe", H, 1), ("without_lookahead", "ordermoe", 1, 1),
+            ("without_redundancy", "no_redundancy", H, 1), ("without_dispersion", "no_dispersion", H, 1),
+            ("without_substitute", "ordermoe", H, 0), ("local_substitute_only", "ordermoe", H, 2),
+            ("popularity_replication", "popularity", H, 1), ("random_deployment", "random", H, 1)]
+    deps, rows = {}, []
+    # the stack's budget (Q-bar = 1.0: used up near layer 16) and one that lasts the stack
+    for qbar in (cfg.Qbar, 2.5):
+        cq = cfg.with_(Qbar=qbar)
+        for name, dep, h, sub in runs:
+            if dep not in deps:
+                deps[dep] = _stream_deploy(om, cfg, base, dep)
+            met = _run_variant(torch, om, cq, deps[dep], h, sub)
+            met.update(variant=name, Qbar=qbar)
+            rows.append(met)
+    out["variants"] = rows
+    out["copies_per_expert_layer0"] = {n: np.bincount(d["x_dep"][0].sum(axis=0)).tolist() for n, d in deps.items()}
+    del deps
+    mem = []
+    for ratio in (1.0, 1.5, 2.0, 2.5, 3.0):
+        c = cfg.with_(memory_ratio=ratio)
+        for dep in ("ordermoe", "popularity"):
+            met = _run_variant(torch, om, c, _stream_deploy(om, c, base, dep), H, 1)
+            met["memory_ratio"] = ratio
+            mem.append(met)
+    out["memory_ratio_sweep"] = mem
+    net16 = wl.network(cfg, M=16)
+    srv = []
+    for M in (4, 8, 12, 16):
+        c = cfg.with_(M=M)
+        net = wl.Network(B=net16.B[:M, :M].copy(), tau=net16.tau[:M, :M].copy(), F=net16.F[:M].copy())
+        sm = _stream_deploy(om, c, base, "ordermoe", net=net)
+        for sub in (1, 0):
+            met = _run_variant(torch, om, c, sm, H, sub)
+            met["servers"] = M
+            srv.append(met)
+    out["server_sweep"] = srv
+    return out
 
 
 def _weight_adaptation(torch, om, windows: int = 14, kappa: float = 0.1):
@@ -658,9 +771,12 @@ def main():
                     help="skip the look-ahead depth sweep H = 1..5 of the decode stack")
     ap.add_argument("--no-adapt", action="store_true",
                     help="skip the eq-45 weight-adaptation loop on the decode stack")
+    ap.add_argument("--no-variants", action="store_true",
+                    help="skip the variant / baseline / memory-ratio / server-count study of the decode stack")
     ap.add_argument("--no-stream", action="store_true",
                     help="skip the 32-layer decode-stream measurement")
-    ap.add_argument("--only", choices=("layer", "simbuild", "stream", "sweep", "horizon", "adapt"),
+    ap.add_argument("--only", choices=("layer", "simbuild", "stream", "sweep", "horizon", "adapt",
+                                       "variants"),
                     help="run one leg alone (for profiling): the layer step without the other "
                          "legs, or only the similarity build / decode stream (prints that leg's "
                          "JSON object)")
@@ -700,9 +816,12 @@ def main():
     if args.only == "adapt":
         print(json.dumps(_weight_adaptation(torch, om)))
         return
+    if args.only == "variants":
+        print(json.dumps(_variants(torch, om)))
+        return
     if args.only == "layer":
         args.no_simbuild = args.no_stream = args.no_cpu_baseline = args.no_other_layers = True
-        args.no_sweep = args.no_horizon = args.no_adapt = True
+        args.no_sweep = args.no_horizon = args.no_adapt = args.no_variants = True
     print("bench: setting up %s" % cfg.name, file=sys.stderr, flush=True)
     st = _setup(cfg, torch, om)
     torch.cuda.synchronize()
@@ -774,6 +893,10 @@ def main():
     if not args.no_adapt:
         print("bench: weight adaptation", file=sys.stderr, flush=True)
         res["weight_adaptation"] = _weight_adaptation(torch, om)
+        torch.cuda.empty_cache()
+    if not args.no_variants:
+        print("bench: variants and baselines", file=sys.stderr, flush=True)
+        res["variants"] = _variants(torch, om)
         torch.cuda.empty_cache()
     if not args.no_stream:
         print("bench: decode stream", file=sys.stderr, flush=True)

@@ -29,12 +29,16 @@ SMALL = {
     "C4s": wl.C4.with_(T=1700, T_cal=4096),
     # the Local Substitute Only baseline: substitutes only on the token's server
     "C3s_local_sub": wl.C3.with_(T=1500, T_cal=4096, allow_sub=2),
+    # 12 and 16 servers (the server-count sweep), tokens starting on every server
+    "C4s_M12": wl.C4.with_(T=1700, T_cal=4096, M=12, capacity=(8.0,) * 12, loc_mode="uniform"),
+    "C4s_M16": wl.C4.with_(T=1700, T_cal=4096, M=16, capacity=(8.0,) * 16, loc_mode="uniform"),
 }
 # decode-sized batches (at most 128 tokens): the thin-GEMM path of the forward
 DECODE = {
     "C2d": wl.C2.with_(T=64, T_cal=4096),
     "C3d": wl.C3.with_(T=128, T_cal=4096),
     "C4d": wl.C4.with_(T=97, T_cal=4096),
+    "C4d_M16": wl.C4.with_(T=97, T_cal=4096, M=16, capacity=(8.0,) * 16, loc_mode="uniform"),
 }
 FULL = {"C2": wl.C2.with_(T_cal=4096), "C3": wl.C3.with_(T_cal=4096), "C4": wl.C4.with_(T_cal=4096),
         # large batches with a ragged last block of the 32-token routing kernels:

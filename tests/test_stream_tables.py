@@ -19,9 +19,9 @@ def test_thresholds_follow_eq6(stream_case):
 
 def test_planted_clusters_are_recovered_at_every_threshold(stream_case):
     # 32 planted clusters of 4 experts; the greedy cover returns them for every theta_l
-    cl = np.arange(wl.C5_STREAM.E) // wl.C5_STREAM.cluster_size
-    for m in stream_case.models:
-        g = m["group_of"]
+    cls = wl.stream_clusters(wl.C5_STREAM)
+    for l, m in enumerate(stream_case.models):
+        g, cl = m["group_of"], cls[l]
         assert len(set(g.tolist())) == 32
         for c in range(32):
             assert len(set(g[cl == c].tolist())) == 1
@@ -44,9 +44,10 @@ def test_deployment_constraints(stream_case):
 
 def test_transitions_are_distributions_with_cluster_persistence(stream_case):
     sc = stream_case
-    cl = np.arange(128) // 4
-    same = cl[:, None] == cl[None, :]
-    for P in sc.P:
+    cls = wl.stream_clusters(wl.C5_STREAM)
+    for l, P in enumerate(sc.P):
+        # P_l maps layer-l experts to layer-(l+1) experts: same planted cluster index
+        same = cls[l][:, None] == cls[l + 1][None, :]
         s = P.sum(axis=1)
         assert np.all((np.abs(s - 1) < 1e-12) | (s == 0))
         assert np.all(P >= 0)

@@ -24,6 +24,7 @@ import numpy as np
 # one expert's weights never depends on having drawn another's.
 _S_CENTRES, _S_NOISE, _S_X, _S_XCAL, _S_WG, _S_WU, _S_WD = 1, 2, 3, 4, 5, 6, 7
 _S_SHARED, _S_LOC, _S_NET, _S_QHAT = 8, 9, 1000, 11
+_S_PERM = 12
 
 
 def _rng(*key: int) -> np.random.Generator:
@@ -267,17 +268,28 @@ def _ar_chain(rng: np.random.Generator, steps: int, shape, rho: float):
         yield z
 
 
+def stream_clusters(cfg: StreamConfig) -> np.ndarray:
+    """Planted cluster of every expert of every layer [N][E]: cluster_size
+    experts per cluster, the members drawn by a seeded permutation per layer
+    (expert numbers carry no similarity, as in a trained model)."""
+    out = np.empty((cfg.N, cfg.E), dtype=np.int64)
+    for l in range(cfg.N):
+        perm = _rng(cfg.seed, _S_PERM, l).permutation(cfg.E)
+        out[l, perm] = np.arange(cfg.E) // cfg.cluster_size
+    return out
+
+
 def stream_routers(cfg: StreamConfig):
-    """W_r of every layer [N][E][d]: row j = centre_l[j // cluster_size] +
+    """W_r of every layer [N][E][d]: row j = centre_l[cluster_l(j)] +
     sigma * N(0,1), times centre_std; the centres follow an AR(1) chain over the
-    layers."""
+    layers, so cluster c of one layer resembles cluster c of the next."""
     cent = _ar_chain(_rng(cfg.seed, _S_CENTRES), cfg.N, (cfg.clusters, cfg.d), cfg.rho_c)
     noise = _rng(cfg.seed, _S_NOISE)
-    cl = np.arange(cfg.E) // cfg.cluster_size
+    cls = stream_clusters(cfg)
     out = np.empty((cfg.N, cfg.E, cfg.d), dtype=np.float32)
     for l, c in enumerate(cent):
         n = noise.standard_normal((cfg.E, cfg.d), dtype=np.float32)
-        out[l] = _store(cfg.centre_std * (c[cl] + np.float32(cfg.sigma) * n), cfg.dtype)
+        out[l] = _store(cfg.centre_std * (c[cls[l]] + np.float32(cfg.sigma) * n), cfg.dtype)
     return out
 
 
