@@ -473,35 +473,39 @@ def _route_chain(torch, om, cfg, sm, layers, qh0=None):
                  counters=o["counters"].cpu().numpy(), qhat_out=o["qhat_out"].cpu().numpy()) for li, o in recs]
 
 
+def _simulate(cfg, sm, recs):
+    """The library's delay simulator (eq 13-17, eq 22) over the realized
+    decisions of the chain: per token the delay of its executed slots along
+    its trajectory (seconds), per server the FLOP it executed, and the
+    transfer and slot counts."""
+    from paper_2607_17154_amd import ordermoe as om
+    em = np.stack([r["exec_m"].reshape(cfg.T, cfg.k) for r in recs])
+    ek = np.stack([r["exec_k"].reshape(cfg.T, cfg.k) for r in recs])
+    net = sm["net"]
+    return om.ordermoe_simulate_delay(recs[0]["loc_in"], em, ek, [sm["c"]] * cfg.N, [sm["z_bits"]] * cfg.N,
+                                      net.B, net.tau, net.F)
+
+
 def _token_delays(cfg, sm, recs):
-    """Per token: the modeled delay of eq 37 summed over its executed slots and
-    the layers, along the realized trajectory (seconds)."""
-    net, c, z = sm["net"], sm["c"], sm["z_bits"]
-    delay = np.zeros(cfg.T)
-    for r in recs:
-        s = r["loc_in"].astype(np.int64)[:, None].repeat(cfg.k, 1)
-        m = r["exec_m"].astype(np.int64)
-        kk = r["exec_k"].astype(np.int64)
-        trans = np.where(s != m, z / net.B[s, m] + net.tau[s, m], 0.0)
-        delay += (trans + c[kk] / net.F[m]).sum(axis=1)
-    return delay
+    return _simulate(cfg, sm, recs)["delay"]
 
 
 def _trajectory_metrics(cfg, sm, recs):
-    """Along the realized trajectories: the modeled delay of every executed slot,
-    d(m, k | s) of eq 37 (transfer from the token's location s when m != s, plus
-    compute c_k / F_m), summed per token over slots and layers; cross-server
-    transfers (distinct token-destination pairs per layer); slot classes; the
-    budget used at the end."""
+    """Along the realized trajectories (the simulator): the mean modeled delay
+    per token, cross-server transfers (distinct token-destination pairs per
+    layer) and their traffic per 1000 tokens, the server workload imbalance
+    (max over mean of eq 22), slot classes, the budget used at the end."""
     T = cfg.T
-    delay = _token_delays(cfg, sm, recs)
+    sim = _simulate(cfg, sm, recs)
     cls = np.zeros(4, np.int64)
-    transfers = 0
     for r in recs:
         cls += r["counters"][:4].astype(np.int64)
-        transfers += int(r["counters"][5])
     slots = cls.sum()
-    return {"delay_ms_per_token": float(delay.mean() * 1e3), "transfers_per_token_layer": transfers / (T * cfg.N),
+    work = sim["work"]
+    return {"delay_ms_per_token": float(sim["delay"].mean() * 1e3),
+            "transfers_per_token_layer": sim["transfers"] / (T * cfg.N),
+            "traffic_MB_per_1000_tokens": sim["traffic_bytes"] / T * 1000 / 1e6,
+            "workload_max_over_mean": float(work.max() / work.mean()),
             "remote_ratio": float(cls[2] + cls[3]) / slots, "classes_LE_LS_RE_RS": [int(v) for v in cls],
             "budget_used": float(np.mean(recs[-1]["qhat_out"]) / cfg.Qbar)}
 

@@ -12,6 +12,7 @@
  *   ordermoe_build_similarity   Section III-B / IV-A, eq (3)-(5), (24)-(28)
  *   ordermoe_place              Section IV-B / IV-C, eq (29)-(35), Algorithm 1
  *   ordermoe_place_random       Section VI-A, the Random Deployment baseline
+ *   ordermoe_simulate_delay     Section III-C/D/F, eq (13)-(17), (22)
  *   ordermoe_build_tables       eq (6)-(8), (18), (37)-(38) (+ eq (42) input)
  *   ordermoe_route_select       router + Section V, eq (36)-(44), Algorithm 2
  *   ordermoe_local_moe_forward  execution of the selected (server, expert)
@@ -251,6 +252,33 @@ int ordermoe_theta_layer(int32_t l, int32_t N, double theta_min, double theta_ma
  *   omega_Q_out, omega_T_out host scalars.  EINVAL otherwise (nothing written). */
 int ordermoe_adapt_weights(double omega_Q, double kappa, double T_bar, double Q_bar, double* omega_Q_out,
                            double* omega_T_out);
+
+/* Delay, server workload and cross-server traffic of realized decisions
+ * (Section III-C/D, eq 13-17; Section III-F, eq 22), host only.  The paper's
+ * model has one execution server per token and layer; with top-k every
+ * executed slot pays eq 15's compute c_k / F_m and, when its server m is not
+ * the token's location s, the transfer z_l / B_{s,m} + tau_{s,m} of eq 13
+ * (first layer, s = the access server) or eq 14.  After a layer the token
+ * resides on slot 0's server (the return path is not modelled).  A token whose
+ * location is >= M, or a slot whose server is >= M, executes nothing there.
+ *   N layers, T tokens, k slots, M servers; E_l [N] experts per layer.
+ *   loc0 [T] u8: access servers; exec_m [N][T][k] u8 and exec_k [N][T][k] i32:
+ *   each layer's decisions (as ordermoe_route_select writes them);
+ *   c [sum E_l] f64 FLOP per expert, layer-major; z_bits [N]; B, tau [M][M]
+ *   row-major (bit/s, s); F [M] FLOP/s.
+ *   Outputs (host, caller-owned): delay_out [T] seconds per token (eq 16-17:
+ *   per-user delays are sums over the user's tokens); work_out [M] FLOP per
+ *   server (eq 22); stats_out [4] = {transfers (distinct token-destination
+ *   pairs per layer), traffic bytes (z_l / 8 per transfer), remote slots,
+ *   executed slots}; loc_out [N][T] u8 (the location entering each layer) or
+ *   null.  Sums run in the order layer, token, slot, in fp64.  EINVAL for
+ *   bad sizes, an executed expert outside [0, E_l), F <= 0 or B <= 0 on a
+ *   used link (nothing written). */
+int ordermoe_simulate_delay(int32_t N, int64_t T, int32_t k, int32_t M, const int32_t* E_l,
+                            const uint8_t* loc0, const uint8_t* exec_m, const int32_t* exec_k,
+                            const double* c, const double* z_bits, const double* B, const double* tau,
+                            const double* F, double* delay_out, double* work_out, double* stats_out,
+                            uint8_t* loc_out);
 
 /* ------------------------------------------------------------------------
  * Routing and server-expert selection of one layer (Section V, the per-layer

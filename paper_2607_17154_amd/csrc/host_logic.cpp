@@ -436,3 +436,82 @@ extern "C" int ordermoe_place_random(int32_t N, const int32_t* E_l, int32_t M, c
     clear_error();
     return ORDERMOE_OK;
 }
+
+// Delay, workload and traffic of realized decisions (eq 13-17, eq 22), one
+// layer at a time: each token's delay grows by its executed slots' transfer
+// (from the location it entered the layer with) and compute terms, then the
+// token moves to slot 0's server.
+extern "C" int ordermoe_simulate_delay(int32_t N, int64_t T, int32_t k, int32_t M, const int32_t* E_l,
+                                       const uint8_t* loc0, const uint8_t* exec_m, const int32_t* exec_k,
+                                       const double* c, const double* z_bits, const double* B,
+                                       const double* tau, const double* F, double* delay_out,
+                                       double* work_out, double* stats_out, uint8_t* loc_out) {
+    if (N < 1 || T < 0 || k < 1 || k > ORDERMOE_MAX_TOPK || M < 1 || M > ORDERMOE_MAX_SERVERS)
+        return fail(ORDERMOE_EINVAL, "simulate_delay: N, T, k or M out of range");
+    if (!E_l || !c || !z_bits || !B || !tau || !F || !delay_out || !work_out || !stats_out ||
+        (T > 0 && (!loc0 || !exec_m || !exec_k)))
+        return fail(ORDERMOE_EINVAL, "simulate_delay: null pointer");
+    std::vector<size_t> cbase(N + 1, 0);
+    for (int l = 0; l < N; ++l) {
+        if (E_l[l] < 1 || E_l[l] > ORDERMOE_MAX_EXPERTS) return fail(ORDERMOE_EINVAL, "simulate_delay: E_l out of range");
+        cbase[l + 1] = cbase[l] + (size_t)E_l[l];
+    }
+    for (int m = 0; m < M; ++m)
+        if (!(F[m] > 0.0)) return fail(ORDERMOE_EINVAL, "simulate_delay: F must be positive");
+    // validate every executed slot before writing anything
+    {
+        std::vector<uint8_t> at(loc0, loc0 + T);
+        for (int l = 0; l < N; ++l)
+            for (int64_t t = 0; t < T; ++t) {
+                if (at[t] >= M) continue;
+                const size_t o = ((size_t)l * T + t) * k;
+                for (int j = 0; j < k; ++j) {
+                    const int m = exec_m[o + j];
+                    if (m >= M) continue;
+                    if (exec_k[o + j] < 0 || exec_k[o + j] >= E_l[l])
+                        return fail(ORDERMOE_EINVAL, "simulate_delay: executed expert out of range");
+                    if (m != at[t] && !(B[(size_t)at[t] * M + m] > 0.0))
+                        return fail(ORDERMOE_EINVAL, "simulate_delay: B must be positive between servers");
+                }
+                if (exec_m[o] < M) at[t] = exec_m[o];
+            }
+    }
+    std::vector<uint8_t> at(loc0, loc0 + T);
+    std::vector<double> delay(T, 0.0), work(M, 0.0);
+    double transfers = 0.0, traffic = 0.0, remote = 0.0, slots = 0.0;
+    for (int l = 0; l < N; ++l) {
+        const double z = z_bits[l];
+        const double* cl = c + cbase[l];
+        for (int64_t t = 0; t < T; ++t) {
+            if (loc_out) loc_out[(size_t)l * T + t] = at[t];
+            const int s = at[t];
+            if (s >= M) continue;
+            const size_t o = ((size_t)l * T + t) * k;
+            uint32_t dest = 0;
+            for (int j = 0; j < k; ++j) {
+                const int m = exec_m[o + j];
+                if (m >= M) continue;
+                if (m != s) {
+                    delay[t] += z / B[(size_t)s * M + m] + tau[(size_t)s * M + m];   // eq 13 / 14
+                    dest |= 1u << m;
+                    remote += 1.0;
+                }
+                delay[t] += cl[exec_k[o + j]] / F[m];                                 // eq 15
+                work[m] += cl[exec_k[o + j]];                                         // eq 22
+                slots += 1.0;
+            }
+            const int nd = __builtin_popcount(dest);
+            transfers += nd;
+            traffic += nd * (z / 8.0);
+            if (exec_m[o] < M) at[t] = exec_m[o];                   // resides on slot 0's server
+        }
+    }
+    std::copy(delay.begin(), delay.end(), delay_out);
+    std::copy(work.begin(), work.end(), work_out);
+    stats_out[0] = transfers;
+    stats_out[1] = traffic;
+    stats_out[2] = remote;
+    stats_out[3] = slots;
+    clear_error();
+    return ORDERMOE_OK;
+}

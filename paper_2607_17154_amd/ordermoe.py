@@ -31,7 +31,7 @@ EXPORTS = ("ordermoe_last_error", "ordermoe_similarity_workspace_size", "ordermo
            "ordermoe_forward_workspace_size", "ordermoe_local_moe_forward",
            "ordermoe_pack_gate_up", "ordermoe_timing_enable", "ordermoe_timing_read",
            "ordermoe_estimate_transitions", "ordermoe_theta_layer", "ordermoe_adapt_weights",
-           "ordermoe_place_random")
+           "ordermoe_place_random", "ordermoe_simulate_delay")
 TIMING_NAME = 64
 
 
@@ -93,6 +93,9 @@ def lib() -> ctypes.CDLL:
     L.ordermoe_place.argtypes = [_I32, _P, _I32, _P, _P, _P, _P, _P, _F64, _I32, _P, _P]
     L.ordermoe_place_random.restype = ctypes.c_int
     L.ordermoe_place_random.argtypes = [_I32, _P, _I32, _P, _P, ctypes.c_uint64, _I32, _P, _P]
+    L.ordermoe_simulate_delay.restype = ctypes.c_int
+    L.ordermoe_simulate_delay.argtypes = [_I32, _I64, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                                          _P, _P]
     L.ordermoe_build_tables.restype = ctypes.c_int
     L.ordermoe_build_tables.argtypes = [_I32, _I32, _P, _P, _F32, _P, _P, _P, _P, _F64, _P, _F64,
                                         _F64, _P, _I32, _P, _P, _P, _P, _P]
@@ -277,6 +280,33 @@ def ordermoe_place_random(p: Sequence[np.ndarray], C, seed: int, redundancy: int
         out.append(x[off:off + M * e].reshape(M, e).copy())
         off += M * e
     return out, used
+
+
+def ordermoe_simulate_delay(loc0, exec_m, exec_k, c: Sequence[np.ndarray], z_bits, B, tau, F):
+    """Delay per token (s), workload per server (FLOP), the location entering
+    each layer [N][T] and the counts: dict(delay, work, loc, transfers,
+    traffic_bytes, remote_slots, slots).  exec_m, exec_k: [N][T][k] host arrays."""
+    em = np.ascontiguousarray(exec_m, dtype=np.uint8)
+    N, T, k = em.shape
+    ek = np.ascontiguousarray(exec_k, dtype=np.int32).reshape(N, T, k)
+    M = len(F)
+    E_l = np.array([len(v) for v in c], dtype=np.int32)
+    l0, l0p = _host(loc0, np.uint8, T)
+    cc, cp = _host(np.concatenate([np.asarray(v, dtype=np.float64) for v in c]), np.float64)
+    zz, zp = _host(z_bits, np.float64, N)
+    Bb, Bp = _host(B, np.float64, M * M)
+    tt, tp = _host(tau, np.float64, M * M)
+    FF, Fp = _host(F, np.float64, M)
+    delay = np.zeros(T, np.float64)
+    work = np.zeros(M, np.float64)
+    stats = np.zeros(4, np.float64)
+    loc = np.zeros((N, T), np.uint8)
+    _check(lib().ordermoe_simulate_delay(N, T, k, M, E_l.ctypes.data_as(_P), l0p, em.ctypes.data_as(_P),
+                                         ek.ctypes.data_as(_P), cp, zp, Bp, tp, Fp, delay.ctypes.data_as(_P),
+                                         work.ctypes.data_as(_P), stats.ctypes.data_as(_P),
+                                         loc.ctypes.data_as(_P)))
+    return dict(delay=delay, work=work, loc=loc, transfers=int(stats[0]), traffic_bytes=float(stats[1]),
+                remote_slots=int(stats[2]), slots=int(stats[3]))
 
 
 def ordermoe_build_tables(sim: np.ndarray, group_of: np.ndarray, theta: float, x: np.ndarray,

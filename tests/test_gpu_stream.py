@@ -134,6 +134,31 @@ def test_chain_decisions_match_the_oracle(stream_case, chain, oracle_chain):
     assert exhausted_layer is not None and 4 <= exhausted_layer < stream_case.cfg.N - 4
 
 
+def test_delay_simulator_follows_the_device_trajectory(stream_case, chain):
+    """The library's delay simulator (eq 13-17, eq 22) over the device's
+    decisions: its trajectory equals the locations the kernels carried from
+    layer to layer, its remote-slot and transfer counts equal the kernels'
+    counters, and its delays equal the oracle's evaluation of the same
+    decisions bit for bit."""
+    from oracle import delay as odelay
+    sc, cfg = stream_case, stream_case.cfg
+    g = chain["layers"]
+    em = np.stack([r["exec_m"].reshape(cfg.T, cfg.k) for r in g])
+    ek = np.stack([r["exec_k"].reshape(cfg.T, cfg.k) for r in g])
+    z = [sc.z_bits] * cfg.N
+    c = [sc.c] * cfg.N
+    sim = om.ordermoe_simulate_delay(g[0]["loc_in"], em, ek, c, z, sc.net.B, sc.net.tau, sc.net.F)
+    for l in range(cfg.N):
+        np.testing.assert_array_equal(sim["loc"][l], g[l]["loc_in"])
+    cnt = np.sum([r["counters"] for r in g], axis=0)
+    assert sim["remote_slots"] == int(cnt[om.CNT_REMOTE_SLOTS])
+    assert sim["transfers"] == int(cnt[om.CNT_TRANSFERS])
+    assert sim["slots"] == int(cnt[:4].sum())
+    want = odelay.simulate(g[0]["loc_in"], em, ek, c, z, sc.net.B, sc.net.tau, sc.net.F)
+    np.testing.assert_array_equal(sim["delay"], want["delay"])
+    np.testing.assert_array_equal(sim["work"], want["work"])
+
+
 @pytest.mark.parametrize("H,allow_sub", [(1, 1), (5, 1), (3, 2)])
 def test_chain_decisions_match_the_oracle_at_other_horizons(stream_case, H, allow_sub):
     """The look-ahead sweep of Fig. 7: the myopic rule (H = 1) and the deepest
