@@ -21,6 +21,16 @@ if not torch.cuda.is_available():  # pragma: no cover
 
 TOL = {"bf16": 2e-2, "f32": 1e-4}
 
+# the library's maximum sizes: 256 experts (16 clusters of 16, so every expert
+# has the full 15 substitutes), top-8, 32 servers, server 0 holding 64 experts
+# (capacities summing to exactly one copy of every expert), a shared expert.
+# Router rows spread by sigma 0.5 at logit scale 4/sqrt(d), so that near-ties
+# among a cluster's 16 members (margin < 1e-4) stay rare
+CMAX = wl.LayerConfig(name="max_T600_d512_E256_f256_top8_M32", dtype="bf16", seed=9, T=600, d=512, E=256,
+                      f=256, k=8, n_shared=1, clusters=16, cluster_size=16, sigma=0.5,
+                      centre_std=4 * 512 ** -0.5, M=32, m0=0, capacity=(64.0,) + (6.0,) * 30 + (12.0,),
+                      loc_mode="uniform", Qbar=0.25, theta=0.7, T_cal=4096)
+
 # reduced shapes that span several tiles with ragged tails; full shapes below
 SMALL = {
     "C1": wl.C1,
@@ -32,6 +42,7 @@ SMALL = {
     # 12 and 16 servers (the server-count sweep), tokens starting on every server
     "C4s_M12": wl.C4.with_(T=1700, T_cal=4096, M=12, capacity=(8.0,) * 12, loc_mode="uniform"),
     "C4s_M16": wl.C4.with_(T=1700, T_cal=4096, M=16, capacity=(8.0,) * 16, loc_mode="uniform"),
+    "Cmax": CMAX,
 }
 # decode-sized batches (at most 128 tokens): the thin-GEMM path of the forward
 DECODE = {
@@ -39,6 +50,7 @@ DECODE = {
     "C3d": wl.C3.with_(T=128, T_cal=4096),
     "C4d": wl.C4.with_(T=97, T_cal=4096),
     "C4d_M16": wl.C4.with_(T=97, T_cal=4096, M=16, capacity=(8.0,) * 16, loc_mode="uniform"),
+    "Cmax_d": CMAX.with_(T=97),
 }
 FULL = {"C2": wl.C2.with_(T_cal=4096), "C3": wl.C3.with_(T_cal=4096), "C4": wl.C4.with_(T_cal=4096),
         # large batches with a ragged last block of the 32-token routing kernels:
