@@ -381,12 +381,15 @@ route_select_kernel(const RouteArgs a) {
     if (a.ksplit > 0) {
         // split router: add the K slices in slice order (the reads of all
         // slices of an element are issued before the additions)
-        // two elements per round; reads past the slices or the batch re-read
-        // the first partial (discarded), so that no branch separates the reads
-        for (int i0 = tid; i0 < TB * Epad; i0 += 2 * RT_THREADS) {
-            float pv[2][RT_SPLIT_MAX_K];
+        // PU elements per round: one round of 16-token blocks up to 128
+        // experts (up to 64 with two, within the 128 registers of those
+        // kernels); reads past the slices or the batch re-read the first
+        // partial (discarded), so that no branch separates the reads
+        constexpr int PU = NBT >= 8 ? 4 : 2;
+        for (int i0 = tid; i0 < TB * Epad; i0 += PU * RT_THREADS) {
+            float pv[PU][RT_SPLIT_MAX_K];
 #pragma unroll
-            for (int u = 0; u < 2; ++u) {
+            for (int u = 0; u < PU; ++u) {
                 const int i = i0 + u * RT_THREADS;
                 const int64_t tok = t0 + i / Epad;
                 const bool ok = i < TB * Epad && tok < a.T;
@@ -395,7 +398,7 @@ route_select_kernel(const RouteArgs a) {
                     pv[u][z] = a.logit_part[(z < a.ksplit && ok) ? ((int64_t)z * a.T + tok) * Epad + i % Epad : 0];
             }
 #pragma unroll
-            for (int u = 0; u < 2; ++u) {
+            for (int u = 0; u < PU; ++u) {
                 const int i = i0 + u * RT_THREADS;
                 float v = 0.f;
 #pragma unroll
@@ -503,9 +506,15 @@ route_select_kernel(const RouteArgs a) {
     // top-(k+1) selection by (logit desc, index asc); this lane's logits (experts
     // j + 16 i) are read once and kept as order-preserving keys
     const int kk1 = (k + 1 < E) ? k + 1 : E;
+    // (reads at clamped addresses and selects instead of branches, so that the
+    // LDS reads issue together and no per-element branch splits the wave)
     uint32_t okey[NBT];
 #pragma unroll
-    for (int i = 0; i < NBT; ++i) okey[i] = (j + 16 * i < E) ? f2ord(lg[j + 16 * i]) : 0u;
+    for (int i = 0; i < NBT; ++i) {
+        const int e = j + 16 * i;
+        const float v = lg[e < E ? e : E - 1];
+        okey[i] = e < E ? f2ord(v) : 0u;
+    }
     uint32_t removed = 0;                    // bit i: local element j + 16 i taken
     int sel_e[ORDERMOE_MAX_TOPK + 1];
     float sel_v[ORDERMOE_MAX_TOPK + 1];
@@ -516,8 +525,8 @@ route_select_kernel(const RouteArgs a) {
 #pragma unroll
             for (int i = 0; i < NBT; ++i) {
                 const int e = j + 16 * i;
-                if (e >= E || (removed & (1u << i))) continue;
-                const uint64_t key = ((uint64_t)okey[i] << 32) | (uint32_t)(0xFFFFu - (uint32_t)e);
+                const bool live = e < E && !((removed >> i) & 1u);
+                const uint64_t key = live ? (((uint64_t)okey[i] << 32) | (uint32_t)(0xFFFFu - (uint32_t)e)) : 0ull;
                 best = key > best ? key : best;
             }
             best = row_max_u64(best);
@@ -565,28 +574,33 @@ route_select_kernel(const RouteArgs a) {
     uint32_t msv[ORDERMOE_MAX_TOPK];
     uint64_t key[ORDERMOE_MAX_TOPK];
     bool search[ORDERMOE_MAX_TOPK];
+    // every slot's table reads are issued (slots past k read slot 0's entries,
+    // discarded), then masked, so that no per-slot branch serialises them
 #pragma unroll
     for (int slot = 0; slot < ORDERMOE_MAX_TOPK; ++slot) {
-        ke[slot] = -1; qe[slot] = 0.f; msv[slot] = 0u; key[slot] = ~0ull; search[slot] = false;
-        if (slot < k) {
-            const int r = sel_e[slot];
-            const uint32_t rmask = s_mask[r];
-            const int nsub = s_t1n[r];
-            const int tk = s_t1k[r * a.gmax + jm1];
-            const float tq = s_t1q[r * a.gmax + jm1];
-            // uniform over the token's row: the reductions below read only lanes of the row
-            search[slot] = loc_ok && !(a.pin && ((rmask >> s_loc) & 1u));
-            if (j == 0) { ke[slot] = r; qe[slot] = 0.f; }
-            else if (subs_on && j - 1 < nsub) { ke[slot] = tk; qe[slot] = tq; }
-            if (ke[slot] < 0 || ke[slot] >= E) ke[slot] = -1;
-        }
+        const bool on = slot < k;
+        const int r = sel_e[on ? slot : 0];
+        const uint32_t rmask = s_mask[r];
+        const int nsub = s_t1n[r];
+        const int tk = s_t1k[r * a.gmax + jm1];
+        const float tq = s_t1q[r * a.gmax + jm1];
+        // uniform over the token's row: the reductions below read only lanes of the row
+        search[slot] = on && loc_ok && !(a.pin && ((rmask >> s_loc) & 1u));
+        const bool sub = j >= 1 && subs_on && j - 1 < nsub;
+        int kc = j == 0 ? r : (sub ? tk : -1);
+        if (!on || kc < 0 || kc >= E) kc = -1;
+        ke[slot] = kc;
+        qe[slot] = on && sub ? tq : 0.f;
+        key[slot] = ~0ull;
     }
+    // the servers holding each candidate (a substitute only on the token's
+    // server in the Local Substitute Only mode)
+    const uint32_t lmask = a.allow_sub == 2 && j >= 1 ? 1u << (s_loc & 31) : ~0u;
 #pragma unroll
-    for (int slot = 0; slot < ORDERMOE_MAX_TOPK; ++slot)
-        if (slot < k && search[slot] && ke[slot] >= 0) {
-            msv[slot] = s_mask[ke[slot]] & mmask;
-            if (a.allow_sub == 2 && j >= 1) msv[slot] &= 1u << s_loc;   // local substitutes only
-        }
+    for (int slot = 0; slot < ORDERMOE_MAX_TOPK; ++slot) {
+        const uint32_t hm = s_mask[ke[slot] >= 0 ? ke[slot] : 0];
+        msv[slot] = search[slot] && ke[slot] >= 0 ? hm & mmask & lmask : 0u;
+    }
     // servers holding each candidate, one per round for every slot together
     for (;;) {
         uint32_t any = 0;
