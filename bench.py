@@ -184,6 +184,8 @@ def _cpu_baseline(cfg, st, target_s: float):
     loc = wl.token_locations(cfg)
     qh = wl.accumulated_loss(cfg)
 
+    split = [0.0, 0.0]                 # decisions, outputs: seconds over the timed passes
+
     def run(n):
         X = st["X"][:n]
         t0 = time.perf_counter()
@@ -192,9 +194,13 @@ def _cpu_baseline(cfg, st, target_s: float):
                             cfg.theta, S, cfg.Qbar, cfg.omega_Q, loc[:n], qh[:n],
                             cfg.pin_local_exact, cfg.allow_sub)
         olayer.dispatch(sel["exec_m"], loc[:n], cfg.M)
+        t1 = time.perf_counter()
         olayer.server_output(X, w, sel["exec_k"], sel["exec_m"], loc[:n], cfg.m0, ew, (),
                              np.arange(n))
-        return time.perf_counter() - t0
+        t2 = time.perf_counter()
+        split[0] += t1 - t0
+        split[1] += t2 - t1
+        return t2 - t0
 
     for j in st["local"]:
         ew(j)
@@ -202,15 +208,32 @@ def _cpu_baseline(cfg, st, target_s: float):
     dt = run(n)
     while dt < target_s / 4 and n < cfg.T:
         n = min(cfg.T, int(n * max(2.0, target_s / max(dt, 1e-3) * 0.8)))
+        split[:] = [0.0, 0.0]
         dt = run(n)
     reps = 1
     if dt < target_s / 2:
         # the whole batch is quick: repeat it to a bounded sample of about target_s seconds
         reps = max(1, int(target_s / max(dt, 1e-3)))
+        split[:] = [0.0, 0.0]
         dt = sum(run(n) for _ in range(reps))
-    return {"value": reps * n / dt, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
-            "sample": "%d pass(es) over the first %d of the %d tokens (route fp64, selection, "
-                      "dispatch, fp64 FFN of server %d); %.1f s" % (reps, n, cfg.T, cfg.m0, dt)}
+    dec_s, out_s = split
+    res = {"value": reps * n / dt, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+           "sample": "%d pass(es) over the first %d of the %d tokens (route fp64, selection, "
+                     "dispatch, fp64 FFN of server %d); %.1f s" % (reps, n, cfg.T, cfg.m0, dt),
+           "decisions_tokens_per_s": reps * n / dec_s, "outputs_tokens_per_s": reps * n / out_s}
+    # the same path on one host thread, on a smaller sample of about a quarter of target_s
+    try:
+        from threadpoolctl import threadpool_limits
+        n1 = int(max(16, min(cfg.T, target_s / 4 / max(dt / (reps * n) * cores, 1e-9))))
+        split[:] = [0.0, 0.0]
+        with threadpool_limits(limits=1):
+            d1 = run(n1)
+        res["one_core"] = {"value": n1 / d1, "decisions_tokens_per_s": n1 / split[0],
+                           "outputs_tokens_per_s": n1 / split[1],
+                           "sample": "the first %d tokens, %.1f s" % (n1, d1)}
+    except ImportError:  # pragma: no cover
+        pass
+    return res
 
 
 def _simbuild(torch, om, reps: int = 5):
