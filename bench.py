@@ -459,6 +459,34 @@ def _stream_lookahead(om, cfg, sm, H, omega_T, omega_Q, allow_sub=None):
                                       cfg.pin_local_exact, cfg.allow_sub if allow_sub is None else allow_sub)
 
 
+def _device_lookahead_inputs(torch, cfg, sm):
+    """The look-ahead inputs of the stack as device tensors (for the device build)."""
+    N = cfg.N
+    d = lambda a, t: torch.from_numpy(np.ascontiguousarray(np.asarray(a, dtype=t))).cuda()
+    return dict(P=d(sm["P"], np.float64), x=d(np.stack(sm["x_dep"]), np.uint8),
+                sim=d(np.stack([m["sim"] for m in sm["models"]]), np.float32),
+                group_of=d(np.stack([m["group_of"] for m in sm["models"]]), np.int32),
+                theta=d(np.array(sm["theta"], np.float32), np.float32), z_bits=d(np.full(N, sm["z_bits"]), np.float64),
+                c=d(np.tile(sm["c"], (N, 1)), np.float64), d_ref=d(np.full(N, sm["dref"]), np.float64),
+                B=d(sm["net"].B, np.float64), tau=d(sm["net"].tau, np.float64), F=d(sm["net"].F, np.float64))
+
+
+def _device_lookahead(torch, om, cfg, inputs, H, omega_T, omega_Q, reps=5):
+    """Phi^(H-1) built on the device (eq 41-42): the result and the average time
+    of one build (HIP events around `reps` builds)."""
+    phi = om.ordermoe_build_lookahead_device(H, omega_T=omega_T, omega_Q=omega_Q, Qbar=cfg.Qbar,
+                                             pin_local_exact=cfg.pin_local_exact, allow_sub=cfg.allow_sub, **inputs)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        om.ordermoe_build_lookahead_device(H, omega_T=omega_T, omega_Q=omega_Q, Qbar=cfg.Qbar,
+                                           pin_local_exact=cfg.pin_local_exact, allow_sub=cfg.allow_sub,
+                                           phi=phi, **inputs)
+    e1.record()
+    torch.cuda.synchronize()
+    return phi.cpu().numpy(), e0.elapsed_time(e1) / reps * 1e3
+
+
 def _stream_layers(torch, om, cfg, sm, phi, omega_T, omega_Q, allow_sub=None):
     """Per layer: the decision tables (eq 7, 18, 37-38 with Phi) on the device
     and the layer struct."""
@@ -539,9 +567,10 @@ def _horizon_sweep(torch, om):
     (eq 42) on the host, then the
     route/select chain runs through the 32 layers for the 64-token batch.
     Reports the modeled delay and cross-server transfers of the realized
-    trajectories, slot classes, budget used, and the host time of the Phi
-    build (the per-token decision cost on the GPU does not depend on H: Phi is
-    a table lookup)."""
+    trajectories, slot classes, budget used, and the time of the Phi build on
+    the host and on the device (the device build checked equal to the host's;
+    the per-token decision cost on the GPU does not depend on H: Phi is a
+    table lookup)."""
     import workloads as wl
     points = []
     # memory ratio 2.0 (the paper's default: every server then holds a member of
@@ -549,13 +578,16 @@ def _horizon_sweep(torch, om):
     for ratio in (2.0, 1.0):
         cfg = wl.C5_STREAM.with_(memory_ratio=ratio)
         sm = _stream_model(torch, om, cfg)
+        dev_in = _device_lookahead_inputs(torch, cfg, sm)
         for H in (1, 2, 3, 4, 5):
             t0 = time.perf_counter()
             phi = _stream_lookahead(om, cfg, sm, H, cfg.omega_T, cfg.omega_Q)
             t_phi = time.perf_counter() - t0
+            phi_d, us_d = _device_lookahead(torch, om, cfg, dev_in, H, cfg.omega_T, cfg.omega_Q)
             layers = _stream_layers(torch, om, cfg, sm, phi, cfg.omega_T, cfg.omega_Q)
             met = _trajectory_metrics(cfg, sm, _route_chain(torch, om, cfg, sm, layers))
-            met.update(memory_ratio=ratio, H=H, phi_build_ms=t_phi * 1e3)
+            met.update(memory_ratio=ratio, H=H, phi_build_ms=t_phi * 1e3, phi_build_device_us=us_d,
+                       phi_device_equals_host=bool(np.array_equal(phi_d, np.stack(phi))))
             points.append(met)
         del sm
     return {"workload": wl.C5_STREAM.name, "points": points}
@@ -630,6 +662,33 @@ def _variants(torch, om):
             srv.append(met)
     out["server_sweep"] = srv
     return out
+
+
+def _property3(torch, om, T: int = 1024, H: int = 3):
+    """Statistical check of Property 3 (the look-ahead selection is no worse
+    than the myopic one in expectation when the calibration transitions match
+    the runtime routing): the 32-layer stack at memory ratio 1.0 (each server
+    holds half of the groups, so the choice between servers matters), T
+    independent decode tokens drawn by the same generator as the calibration
+    tokens, each run through the chain with H = 1 and with H; the per-token
+    modeled delays (eq 13-17 along the realized trajectories) are compared
+    in pairs."""
+    import workloads as wl
+    cfg = wl.C5_STREAM.with_(memory_ratio=1.0, T=T)
+    sm = _stream_deploy(om, cfg, _stream_base(torch, om, cfg))
+    dl = {}
+    for h in (1, H):
+        phi = _stream_lookahead(om, cfg, sm, h, cfg.omega_T, cfg.omega_Q)
+        recs = _route_chain(torch, om, cfg, sm, _stream_layers(torch, om, cfg, sm, phi, cfg.omega_T, cfg.omega_Q))
+        dl[h] = _simulate(cfg, sm, recs)["delay"]
+    diff = (dl[H] - dl[1]) * 1e3
+    se = float(diff.std(ddof=1) / np.sqrt(T))
+    return {"workload": cfg.name, "memory_ratio": 1.0, "tokens": T, "H": H,
+            "delay_ms_per_token_H1": float(dl[1].mean() * 1e3), "delay_ms_per_token_H": float(dl[H].mean() * 1e3),
+            "paired_diff_ms_mean": float(diff.mean()), "paired_diff_ms_stderr": se,
+            "paired_diff_ms_ci95": [float(diff.mean() - 1.96 * se), float(diff.mean() + 1.96 * se)],
+            "tokens_better": int((diff < 0).sum()), "tokens_worse": int((diff > 0).sum()),
+            "tokens_equal": int((diff == 0).sum())}
 
 
 def _weight_adaptation(torch, om, windows: int = 14, kappa: float = 0.1):
@@ -798,12 +857,14 @@ def main():
                     help="skip the look-ahead depth sweep H = 1..5 of the decode stack")
     ap.add_argument("--no-adapt", action="store_true",
                     help="skip the eq-45 weight-adaptation loop on the decode stack")
+    ap.add_argument("--no-property3", action="store_true",
+                    help="skip the paired look-ahead / myopic check of Property 3 on 1024 decode tokens")
     ap.add_argument("--no-variants", action="store_true",
                     help="skip the variant / baseline / memory-ratio / server-count study of the decode stack")
     ap.add_argument("--no-stream", action="store_true",
                     help="skip the 32-layer decode-stream measurement")
     ap.add_argument("--only", choices=("layer", "simbuild", "stream", "sweep", "horizon", "adapt",
-                                       "variants"),
+                                       "variants", "property3"),
                     help="run one leg alone (for profiling): the layer step without the other "
                          "legs, or only the similarity build / decode stream (prints that leg's "
                          "JSON object)")
@@ -846,9 +907,12 @@ def main():
     if args.only == "variants":
         print(json.dumps(_variants(torch, om)))
         return
+    if args.only == "property3":
+        print(json.dumps(_property3(torch, om)))
+        return
     if args.only == "layer":
         args.no_simbuild = args.no_stream = args.no_cpu_baseline = args.no_other_layers = True
-        args.no_sweep = args.no_horizon = args.no_adapt = args.no_variants = True
+        args.no_sweep = args.no_horizon = args.no_adapt = args.no_variants = args.no_property3 = True
     print("bench: setting up %s" % cfg.name, file=sys.stderr, flush=True)
     st = _setup(cfg, torch, om)
     torch.cuda.synchronize()
@@ -920,6 +984,10 @@ def main():
     if not args.no_adapt:
         print("bench: weight adaptation", file=sys.stderr, flush=True)
         res["weight_adaptation"] = _weight_adaptation(torch, om)
+        torch.cuda.empty_cache()
+    if not args.no_property3:
+        print("bench: Property 3 check", file=sys.stderr, flush=True)
+        res["property3"] = _property3(torch, om)
         torch.cuda.empty_cache()
     if not args.no_variants:
         print("bench: variants and baselines", file=sys.stderr, flush=True)

@@ -215,6 +215,23 @@ int ordermoe_build_lookahead(int32_t N, int32_t E, int32_t M, int32_t H, const d
                              const double* F, double omega_T, double omega_Q, float Qbar,
                              int32_t pin_local_exact, int32_t allow_sub, double* phi_out);
 
+/* The same Phi on the device (eq 41-42): every array is device memory with
+ * the layout of ordermoe_build_lookahead, and the result equals that host
+ * routine's bit for bit (the candidate costs are formed in the same fp64
+ * operations and order, each Phi entry is summed in target order).
+ *   ws: device workspace of ordermoe_lookahead_device_workspace_size(N, E, M)
+ *   bytes; phi_out and ws are written, all inputs are only read.  The work
+ *   is ordered on `stream` (a hipStream_t); the call does not synchronise.
+ *   EINVAL for bad sizes or null pointers, EWORKSPACE for a short workspace. */
+size_t ordermoe_lookahead_device_workspace_size(int32_t N, int32_t E, int32_t M);
+int ordermoe_build_lookahead_device(int32_t N, int32_t E, int32_t M, int32_t H, const double* P,
+                                    const uint8_t* x, const float* sim, const int32_t* group_of,
+                                    const float* theta, const double* z_bits, const double* c,
+                                    const double* d_ref, const double* B, const double* tau,
+                                    const double* F, double omega_T, double omega_Q, float Qbar,
+                                    int32_t pin_local_exact, int32_t allow_sub, double* phi_out,
+                                    void* ws, size_t ws_bytes, void* stream);
+
 /* The paper's Random Deployment baseline (Section VI-A), host only: every
  * expert once, layer by layer in index order, on a server drawn uniformly
  * from the memory-feasible ones (none: the server with the most remaining
@@ -235,6 +252,17 @@ int ordermoe_place_random(int32_t N, const int32_t* E_l, int32_t M, const double
  *   P_out host [N-1][E][E] double (nothing is written when N = 1). */
 int ordermoe_estimate_transitions(int32_t N, int32_t E, int64_t T_cal, const int32_t* top1,
                                   double* P_out);
+
+/* The same transition probabilities on the device (eq 41): top1 device
+ * [N][T_cal] int32 (entries outside [0, E) are not counted), P device
+ * [N-1][E][E] double, equal to ordermoe_estimate_transitions' bit for bit
+ * (integer counts, one fp64 division per entry).  ws: device workspace of
+ * ordermoe_transitions_device_workspace_size(N, E) bytes.  Ordered on
+ * `stream`; no synchronisation.  EINVAL for bad sizes or null pointers,
+ * EWORKSPACE for a short workspace; nothing is written when N = 1. */
+size_t ordermoe_transitions_device_workspace_size(int32_t N, int32_t E);
+int ordermoe_estimate_transitions_device(int32_t N, int32_t E, int64_t T_cal, const int32_t* top1, double* P,
+                                         void* ws, size_t ws_bytes, void* stream);
 
 /* Similarity threshold of layer l (1-based) of an N-layer stack (eq 6):
  * theta_l = theta_min + (theta_max - theta_min) (N - l) / (N - 1), in double,

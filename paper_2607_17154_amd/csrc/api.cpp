@@ -278,3 +278,55 @@ extern "C" int ordermoe_pack_gate_up(int32_t dtype, int32_t n, int32_t f, int32_
     clear_error();
     return ORDERMOE_OK;
 }
+
+extern "C" size_t ordermoe_transitions_device_workspace_size(int32_t N, int32_t E) {
+    if (N < 1 || E < 1 || E > ORDERMOE_MAX_EXPERTS) return 0;
+    return transitions_device_workspace(N, E);
+}
+
+extern "C" int ordermoe_estimate_transitions_device(int32_t N, int32_t E, int64_t T_cal, const int32_t* top1,
+                                                    double* P, void* ws, size_t ws_bytes, void* stream) {
+    if (N < 1 || E < 1 || E > ORDERMOE_MAX_EXPERTS || T_cal < 0)
+        return fail(ORDERMOE_EINVAL, "estimate_transitions_device: size out of range");
+    if (N == 1) { clear_error(); return ORDERMOE_OK; }
+    if (!P || !ws || (T_cal > 0 && !top1)) return fail(ORDERMOE_EINVAL, "estimate_transitions_device: null pointer");
+    const size_t need = transitions_device_workspace(N, E);
+    if (ws_bytes < need)
+        return fail(ORDERMOE_EWORKSPACE, "estimate_transitions_device: workspace needs " + std::to_string(need) + " bytes");
+    const int e = launch_transitions_device(N, E, T_cal, top1, P, ws, stream);
+    if (e) return hip_fail(e, "estimate_transitions_device launch");
+    clear_error();
+    return ORDERMOE_OK;
+}
+
+extern "C" size_t ordermoe_lookahead_device_workspace_size(int32_t N, int32_t E, int32_t M) {
+    if (N < 1 || E < 1 || E > ORDERMOE_MAX_EXPERTS || M < 1 || M > ORDERMOE_MAX_SERVERS) return 0;
+    return lookahead_device_workspace(N, E, M);
+}
+
+extern "C" int ordermoe_build_lookahead_device(int32_t N, int32_t E, int32_t M, int32_t H, const double* P,
+                                               const uint8_t* x, const float* sim, const int32_t* group_of,
+                                               const float* theta, const double* z_bits, const double* c,
+                                               const double* d_ref, const double* B, const double* tau,
+                                               const double* F, double omega_T, double omega_Q, float Qbar,
+                                               int32_t pin_local_exact, int32_t allow_sub, double* phi_out,
+                                               void* ws, size_t ws_bytes, void* stream) {
+    if (N < 1 || E < 1 || E > ORDERMOE_MAX_EXPERTS || M < 1 || M > ORDERMOE_MAX_SERVERS || H < 1)
+        return fail(ORDERMOE_EINVAL, "build_lookahead_device: size out of range");
+    if (allow_sub < 0 || allow_sub > 2) return fail(ORDERMOE_EINVAL, "build_lookahead_device: allow_sub must be 0, 1 or 2");
+    if (!phi_out || !ws) return fail(ORDERMOE_EINVAL, "build_lookahead_device: null pointer");
+    if (H > 1 && N > 1 && (!P || !x || !sim || !group_of || !theta || !z_bits || !c || !d_ref || !B || !tau || !F))
+        return fail(ORDERMOE_EINVAL, "build_lookahead_device: null pointer");
+    const size_t need = lookahead_device_workspace(N, E, M);
+    if (ws_bytes < need)
+        return fail(ORDERMOE_EWORKSPACE, "build_lookahead_device: workspace needs " + std::to_string(need) + " bytes");
+    LookaheadDeviceArgs d;
+    d.N = N; d.E = E; d.M = M; d.H = H; d.P = P; d.x = x; d.sim = sim; d.group_of = group_of; d.theta = theta;
+    d.z_bits = z_bits; d.c = c; d.d_ref = d_ref; d.B = B; d.tau = tau; d.F = F; d.omega_T = omega_T;
+    d.omega_Q = omega_Q; d.Qbar = Qbar; d.pin = pin_local_exact; d.allow_sub = allow_sub; d.phi = phi_out;
+    d.ws = ws;
+    const int e = launch_lookahead_device(d, stream);
+    if (e) return hip_fail(e, "build_lookahead_device launch");
+    clear_error();
+    return ORDERMOE_OK;
+}

@@ -127,6 +127,32 @@ int launch_similarity(const SimArgs& a, void* stream);
 int64_t similarity_tokens_per_chunk(int E);
 int similarity_max_experts();
 
+// transition statistics and look-ahead tables on the device (lookahead.hip)
+struct LookaheadDeviceArgs {
+    int32_t N, E, M, H;
+    const double* P;
+    const uint8_t* x;
+    const float* sim;
+    const int32_t* group_of;
+    const float* theta;
+    const double* z_bits;
+    const double* c;
+    const double* d_ref;
+    const double* B;
+    const double* tau;
+    const double* F;
+    double omega_T, omega_Q;
+    float Qbar;
+    int32_t pin, allow_sub;
+    double* phi;
+    void* ws;
+};
+size_t transitions_device_workspace(int32_t N, int32_t E);
+size_t lookahead_device_workspace(int32_t N, int32_t E, int32_t M);
+int launch_transitions_device(int32_t N, int32_t E, int64_t T_cal, const int32_t* top1, double* P, void* ws,
+                              void* stream);
+int launch_lookahead_device(const LookaheadDeviceArgs& d, void* stream);
+
 int launch_pack_gate_up(int dtype, int n, int f, int d, const void* g, const void* u, void* out,
                         void* stream);
 

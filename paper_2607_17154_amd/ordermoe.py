@@ -31,7 +31,9 @@ EXPORTS = ("ordermoe_last_error", "ordermoe_similarity_workspace_size", "ordermo
            "ordermoe_forward_workspace_size", "ordermoe_local_moe_forward",
            "ordermoe_pack_gate_up", "ordermoe_timing_enable", "ordermoe_timing_read",
            "ordermoe_estimate_transitions", "ordermoe_theta_layer", "ordermoe_adapt_weights",
-           "ordermoe_place_random", "ordermoe_simulate_delay")
+           "ordermoe_place_random", "ordermoe_simulate_delay", "ordermoe_lookahead_device_workspace_size",
+           "ordermoe_build_lookahead_device", "ordermoe_transitions_device_workspace_size",
+           "ordermoe_estimate_transitions_device")
 TIMING_NAME = 64
 
 
@@ -93,6 +95,15 @@ def lib() -> ctypes.CDLL:
     L.ordermoe_place.argtypes = [_I32, _P, _I32, _P, _P, _P, _P, _P, _F64, _I32, _P, _P]
     L.ordermoe_place_random.restype = ctypes.c_int
     L.ordermoe_place_random.argtypes = [_I32, _P, _I32, _P, _P, ctypes.c_uint64, _I32, _P, _P]
+    L.ordermoe_lookahead_device_workspace_size.restype = _SZ
+    L.ordermoe_lookahead_device_workspace_size.argtypes = [_I32, _I32, _I32]
+    L.ordermoe_build_lookahead_device.restype = ctypes.c_int
+    L.ordermoe_build_lookahead_device.argtypes = [_I32, _I32, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                                                  _P, _F64, _F64, _F32, _I32, _I32, _P, _P, _SZ, _P]
+    L.ordermoe_transitions_device_workspace_size.restype = _SZ
+    L.ordermoe_transitions_device_workspace_size.argtypes = [_I32, _I32]
+    L.ordermoe_estimate_transitions_device.restype = ctypes.c_int
+    L.ordermoe_estimate_transitions_device.argtypes = [_I32, _I32, _I64, _P, _P, _P, _SZ, _P]
     L.ordermoe_simulate_delay.restype = ctypes.c_int
     L.ordermoe_simulate_delay.argtypes = [_I32, _I64, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
                                           _P, _P]
@@ -349,6 +360,48 @@ def ordermoe_build_lookahead(H: int, P: np.ndarray, x: np.ndarray, sim: np.ndarr
     _check(lib().ordermoe_build_lookahead(N, E, M, H, *(p for _, p in arrs), omega_T, omega_Q, Qbar,
                                           pin_local_exact, allow_sub, phi.ctypes.data_as(_P)))
     return phi
+
+
+def ordermoe_build_lookahead_device(H: int, P, x, sim, group_of, theta, z_bits, c, d_ref, B, tau, F,
+                                    omega_T: float, omega_Q: float, Qbar: float, pin_local_exact: int = 1,
+                                    allow_sub: int = 1, phi=None, ws=None, stream=None):
+    """Phi [N, M, E] float64 on the device (eq 41-42), equal to
+    ordermoe_build_lookahead's.  Every argument array is a contiguous device
+    tensor: P float64 [N-1, E, E] (None when N = 1), x uint8 [N, M, E], sim
+    float32 [N, E, E], group_of int32 [N, E], theta float32 [N], z_bits, d_ref
+    float64 [N], c float64 [N, E], B, tau float64 [M, M], F float64 [M]."""
+    import torch
+    N, M, E = x.shape
+    if phi is None:
+        phi = torch.empty((N, M, E), dtype=torch.float64, device=x.device)
+    need = int(lib().ordermoe_lookahead_device_workspace_size(N, E, M))
+    if ws is None:
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
+    f64 = torch.float64
+    args = [_dev(P, f64, (N - 1) * E * E) if N > 1 else 0, _dev(x, torch.uint8, N * M * E),
+            _dev(sim, torch.float32, N * E * E), _dev(group_of, torch.int32, N * E), _dev(theta, torch.float32, N),
+            _dev(z_bits, f64, N), _dev(c, f64, N * E), _dev(d_ref, f64, N), _dev(B, f64, M * M),
+            _dev(tau, f64, M * M), _dev(F, f64, M)]
+    _check(lib().ordermoe_build_lookahead_device(N, E, M, H, *args, omega_T, omega_Q, Qbar, pin_local_exact,
+                                                 allow_sub, _dev(phi, f64, N * M * E), _dev(ws), ws.numel(),
+                                                 _stream(stream)))
+    return phi
+
+
+def ordermoe_estimate_transitions_device(top1, E: int, P=None, ws=None, stream=None):
+    """P [N-1, E, E] float64 on the device (eq 41) from the device top-1
+    experts top1 int32 [N, T_cal]; equal to ordermoe_estimate_transitions'."""
+    import torch
+    N, T_cal = top1.shape
+    if P is None:
+        P = torch.empty((max(N - 1, 0), E, E), dtype=torch.float64, device=top1.device)
+    need = int(lib().ordermoe_transitions_device_workspace_size(N, E))
+    if ws is None:
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=top1.device)
+    _check(lib().ordermoe_estimate_transitions_device(N, E, T_cal, _dev(top1, torch.int32, N * T_cal),
+                                                      _dev(P, torch.float64, (N - 1) * E * E) if N > 1 else 0,
+                                                      _dev(ws), ws.numel(), _stream(stream)))
+    return P
 
 
 def ordermoe_route_workspace_size(T: int, k: int, M: int) -> int:
