@@ -220,6 +220,23 @@ def test_device_entry_points_validate_before_launch():
                                             None, 0, None)
     assert rc == om.EINVAL
     assert om.lib().ordermoe_pack_gate_up(om.BF16, 1, 10, 64, None, None, None, None) == om.EINVAL
+    # the device builds of eq 41-42: sizes, pointers and workspace checked before any launch
+    L = om.lib()
+    assert L.ordermoe_estimate_transitions_device(4, 300, 10, None, None, None, 0, None) == om.EINVAL
+    assert L.ordermoe_estimate_transitions_device(4, 8, 10, None, None, None, 0, None) == om.EINVAL
+    assert L.ordermoe_estimate_transitions_device(1, 8, 10, None, None, None, 0, None) == om.OK   # nothing to do
+    need = L.ordermoe_transitions_device_workspace_size(4, 8)
+    assert need == 3 * 8 * 8 * 4
+    rc = L.ordermoe_estimate_transitions_device(4, 8, 10, ctypes.c_void_p(16), ctypes.c_void_p(16),
+                                                ctypes.c_void_p(16), need - 1, None)
+    assert rc == om.EWORKSPACE
+    assert L.ordermoe_lookahead_device_workspace_size(4, 8, 33) == 0
+    args = [None] * 11 + [0.5, 0.5, 1.0, 1, 1]
+    assert L.ordermoe_build_lookahead_device(4, 8, 2, 0, *args, None, None, 0, None) == om.EINVAL    # H < 1
+    assert L.ordermoe_build_lookahead_device(4, 8, 2, 2, *args[:15], 3, None, None, 0, None) == om.EINVAL
+    rc = L.ordermoe_build_lookahead_device(4, 8, 2, 3, *args, ctypes.c_void_p(16), ctypes.c_void_p(16),
+                                           1 << 20, None)
+    assert rc == om.EINVAL and "null pointer" in om.last_error()          # H > 1 needs every input
 
 
 def test_workspace_sizes_are_monotone():
