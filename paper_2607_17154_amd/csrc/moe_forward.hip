@@ -386,6 +386,7 @@ __device__ inline float silu_f(float g) { return g / (1.0f + __expf(-g)); }
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void* lds_ptr;
 
 constexpr int BUF_DWORD3 = 0x00020000;   // raw buffer resource word 3 on gfx9-class GPUs
 
@@ -428,19 +429,17 @@ __device__ inline void sched_interleave() {
 // filled round of big tiles runs as a round of half tiles on all CUs.
 template <int BM, int BN, int MODE, int PART>
 __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
-    constexpr int BK = 64, LDK = BK + 8;
+    constexpr int BK = 64;
     constexpr int WM = BM / 2, WN = BN / 2;
     constexpr int FM = WM / 32, FN = WN / 32;
-    constexpr int AV = BM * BK / 8 / 256;
-    constexpr int BV = BN * BK / 8 / 256;
+    constexpr int AV = BM / 32;                     // 8-row load instructions per wave and K tile
+    constexpr int BV = BN / 32;
     static_assert(FN % 2 == 0, "gate/up pairs need an even number of 32-column blocks");
-    extern __shared__ __attribute__((aligned(16))) char lds_raw[];
-    __bf16* sA = (__bf16*)lds_raw;                  // [2][BM][LDK]
-    __bf16* sB = sA + 2 * BM * LDK;                 // [2][BN][LDK]
+    // two buffers of the A and B tiles, [rows][64] bf16 each
+    __shared__ __attribute__((aligned(16))) __bf16 sA0[BM * 64], sA1[BM * 64], sB0[BN * 64], sB1[BN * 64];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
-    const int lrow = tid >> 3, lch = (tid & 7) * 8;  // this thread's load slot
     const int total = *p.ntiles;
     const int per_xcd = gridDim.x >> 3;
     const int vid = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
@@ -469,26 +468,28 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
         const __bf16* Bw = shared ? (const __bf16*)p.Ws
                                   : (const __bf16*)p.Wr + (size_t)L.g * L.N * K;
         const __amdgpu_buffer_rsrc_t rb_rs = make_rsrc(Bw, (uint32_t)((size_t)L.N * K * 2));
-        __amdgpu_buffer_rsrc_t ra_rs;
+        // LDS rows of 64 K values (128 bytes, unpadded); 16-byte chunk q of
+        // row r holds the operand's chunk q ^ (r & 7), so that the 8 rows a
+        // fragment read takes per group of lanes fall on distinct banks.  Load
+        // instruction v of wave w covers rows (w AV + v) 8 .. +7 of the tile:
+        // lane l takes row + l / 8 and fetches its chunk (l & 7) ^ (l / 8),
+        // which the direct-to-LDS load writes at position l & 7.
+        const int gc = (lane & 7) ^ (lane >> 3);
+        const int rsub = lane >> 3;
+        // A: the gathered token rows of X (gate/up) or the group's activation rows (down)
+        const __bf16* Ab = MODE == 0 ? (const __bf16*)p.X
+                                     : (shared ? (const __bf16*)p.As : (const __bf16*)p.Ar + (size_t)L.rowbase * K);
+        const __amdgpu_buffer_rsrc_t ra_rs =
+            make_rsrc(Ab, MODE == 0 ? p.x_bytes : (uint32_t)((size_t)L.R * K * 2));
         uint32_t aoff[AV];
-        if (MODE == 0) {
-            ra_rs = make_rsrc(p.X, p.x_bytes);
 #pragma unroll
-            for (int v = 0; v < AV; ++v) {
-                const int row = L.m0 + lrow + 32 * v;
-                aoff[v] = row < L.R ? ((uint32_t)p.row_tok[L.rowbase + row] * (uint32_t)p.ldx + lch) * 2u : OOR;
-            }
-        } else {
-            const __bf16* Ab = shared ? (const __bf16*)p.As : (const __bf16*)p.Ar + (size_t)L.rowbase * K;
-            ra_rs = make_rsrc(Ab, (uint32_t)((size_t)L.R * K * 2));
-#pragma unroll
-            for (int v = 0; v < AV; ++v) {
-                const int row = L.m0 + lrow + 32 * v;
-                aoff[v] = row < L.R ? ((uint32_t)row * (uint32_t)K + lch) * 2u : OOR;
-            }
+        for (int v = 0; v < AV; ++v) {
+            const int row = L.m0 + (wave * AV + v) * 8 + rsub;
+            const uint32_t src = MODE == 0 ? (row < L.R ? (uint32_t)p.row_tok[L.rowbase + row] : 0u) : (uint32_t)row;
+            aoff[v] = row < L.R ? (src * (uint32_t)(MODE == 0 ? p.ldx : K) + gc * 8) * 2u : OOR;
         }
-        const uint32_t boff0 = ((uint32_t)(L.n0 + lrow) * (uint32_t)K + lch) * 2u;
-        const uint32_t bstride = 64u * (uint32_t)K;       // 32 rows, in bytes
+        const uint32_t boff0 = ((uint32_t)(L.n0 + wave * BV * 8 + rsub) * (uint32_t)K + gc * 8) * 2u;
+        const uint32_t bstride = 16u * (uint32_t)K;       // 8 rows, in bytes
 
         f32x16 acc[FM][FN];
 #pragma unroll
@@ -498,36 +499,34 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
 #pragma unroll
                 for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-        bf16x8 ra[AV], rb[BV];
-        auto gloadA = [&](int k0) {
+        // the loads of a K tile go from memory straight into LDS buffer b
+        auto dmaA = [&](__bf16* sa, int k0) {
 #pragma unroll
-            for (int v = 0; v < AV; ++v) ra[v] = buf_load16(ra_rs, aoff[v], (uint32_t)k0 * 2u);
+            for (int v = 0; v < AV; ++v) {
+                // (a local copy: the host pass drops the kernel when an array
+                // element captured by reference is the builtin's operand)
+                const uint32_t vo = aoff[v];
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(ra_rs, (lds_ptr)(sa + (wave * AV + v) * 8 * 64), 16, vo,
+                                                         (uint32_t)k0 * 2u, 0, 0);
+            }
         };
-        auto gloadB = [&](int k0) {
+        auto dmaB = [&](__bf16* sb, int k0) {
 #pragma unroll
-            for (int v = 0; v < BV; ++v) rb[v] = buf_load16(rb_rs, boff0 + v * bstride, (uint32_t)k0 * 2u);
+            for (int v = 0; v < BV; ++v)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rb_rs, (lds_ptr)(sb + (wave * BV + v) * 8 * 64), 16,
+                                                         boff0 + v * bstride, (uint32_t)k0 * 2u, 0, 0);
         };
-        auto sstoreA = [&](int buf) {
-            __bf16* a = sA + buf * BM * LDK + lrow * LDK + lch;
-#pragma unroll
-            for (int v = 0; v < AV; ++v) *(bf16x8*)(a + v * 32 * LDK) = ra[v];
-        };
-        auto sstoreB = [&](int buf) {
-            __bf16* b = sB + buf * BN * LDK + lrow * LDK + lch;
-#pragma unroll
-            for (int v = 0; v < BV; ++v) *(bf16x8*)(b + v * 32 * LDK) = rb[v];
-        };
-        const int KT = K / BK;
-        const int arow_off = (wm * WM + (lane & 31)) * LDK + (lane >> 5) * 8;
-        const int brow_off = (wn * WN + (lane & 31)) * LDK + (lane >> 5) * 8;
+        const int KT = K / BK;                            // even: K is a multiple of 128
+        // fragment of row (lane & 31) of each 32-row block, K chunk 2 ks + lane / 32
+        const int arow = (wm * WM + (lane & 31)) * 64;
+        const int brow = (wn * WN + (lane & 31)) * 64;
         bf16x8 af[2][FM], bfm[2][FN];
-        auto fload = [&](int buf, int ks, int slot) {
-            const __bf16* a = sA + buf * BM * LDK + arow_off + ks * 16;
-            const __bf16* b = sB + buf * BN * LDK + brow_off + ks * 16;
+        auto fload = [&](const __bf16* sa, const __bf16* sb, int ks, int slot) {
+            const int pos = ((2 * ks + (lane >> 5)) ^ (lane & 7)) * 8;
 #pragma unroll
-            for (int i = 0; i < FM; ++i) af[slot][i] = *(const bf16x8*)(a + i * 32 * LDK);
+            for (int i = 0; i < FM; ++i) af[slot][i] = *(const bf16x8*)(sa + arow + i * 32 * 64 + pos);
 #pragma unroll
-            for (int j = 0; j < FN; ++j) bfm[slot][j] = *(const bf16x8*)(b + j * 32 * LDK);
+            for (int j = 0; j < FN; ++j) bfm[slot][j] = *(const bf16x8*)(sb + brow + j * 32 * 64 + pos);
         };
         auto mfmas = [&](int slot) {
 #pragma unroll
@@ -536,47 +535,48 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
                 for (int j = 0; j < FN; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[slot][i], bfm[slot][j], acc[i][j], 0, 0, 0);
         };
-        // Each K tile of 64 is four MFMA sub-steps of 16.  The memory traffic
-        // of the next K tile is spread over them so the MFMA pipe never waits
-        // behind a burst of memory instructions: sub-step 0 issues the B
-        // (weight) reads, 1 the A reads, 2 stores B to the idle LDS buffer, 3
-        // stores A, so each store waits only for reads issued two sub-steps
-        // earlier; every sub-step also reads the fragments of the next one.
-        // Scheduling groups interleave MFMAs with these instructions, fences
-        // keep the sub-steps in order.  The body is branch-free: after the last
-        // tile the last K tile is re-read into the idle buffer, never used.
+        // Each K tile of 64 is four MFMA sub-steps of 16.  The next K tile's
+        // loads are issued into the idle buffer during the first two sub-steps
+        // (B, then A), a whole K tile ahead of their use; every sub-step also
+        // reads the fragments of the next one.  A K tile ends with the wait
+        // for this wave's loads and the barrier for everyone's.  The two
+        // buffers are separate LDS arrays and the loop is unrolled by two, so
+        // that the loads into one buffer are never taken to alias the reads of
+        // the other.  After the last tile the last K tile is re-read into the
+        // idle buffer, never used.
         constexpr int NM = FM * FN, NR = FM + FN;
-        constexpr int VMEM_READ = 0x020, LDS_WRITE = 0x200;
-        gloadA(0);
-        gloadB(0);
-        sstoreA(0);
-        sstoreB(0);
-        __syncthreads();
-        fload(0, 0, 0);
-        for (int kt = 0; kt < KT; ++kt) {
-            const int cur = kt & 1;
-            const int kn = (kt + 1 < KT ? kt + 1 : kt) * BK;
-            fload(cur, 1, 1);
-            gloadB(kn);
+        constexpr int VMEM_READ = 0x020;
+        auto ktile = [&](__bf16* ca, __bf16* cb, __bf16* na, __bf16* nb, int kn) {
+            dmaB(nb, kn);
+            fload(ca, cb, 1, 1);
             mfmas(0);
             sched_interleave<0, NM, NR, BV, VMEM_READ>();
             __builtin_amdgcn_sched_barrier(0);
-            fload(cur, 2, 0);
-            gloadA(kn);
+            dmaA(na, kn);
+            fload(ca, cb, 2, 0);
             mfmas(1);
             sched_interleave<0, NM, NR, AV, VMEM_READ>();
             __builtin_amdgcn_sched_barrier(0);
-            fload(cur, 3, 1);
-            sstoreB(cur ^ 1);
+            fload(ca, cb, 3, 1);
             mfmas(0);
-            sched_interleave<0, NM, NR, BV, LDS_WRITE>();
+            sched_interleave<0, NM, NR, 0, VMEM_READ>();
             __builtin_amdgcn_sched_barrier(0);
-            sstoreA(cur ^ 1);
             mfmas(1);
-            sched_interleave<0, NM, 0, AV, LDS_WRITE>();
             __builtin_amdgcn_sched_barrier(0);
+            __builtin_amdgcn_s_waitcnt(0x0F70);          // vmcnt(0): this wave's loads are in LDS
             __syncthreads();
-            fload(cur ^ 1, 0, 0);
+            fload(na, nb, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+        };
+        dmaA(sA0, 0);
+        dmaB(sB0, 0);
+        __builtin_amdgcn_s_waitcnt(0x0F70);
+        __syncthreads();
+        fload(sA0, sB0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        for (int kt = 0; kt < KT; kt += 2) {
+            ktile(sA0, sB0, sA1, sB1, (kt + 1) * BK);
+            ktile(sA1, sB1, sA0, sB0, (kt + 2 < KT ? kt + 2 : kt + 1) * BK);
         }
 
         // epilogue: element e of a 32x32 block is row (e/4)*8 + (lane/32)*4 + e%4,
@@ -899,7 +899,7 @@ constexpr int64_t THIN_MAX_T = 128;
 constexpr int THIN_PER_CU = 3;
 
 template <int BM, int BN>
-constexpr size_t bf16_gemm_lds() { return (size_t)2 * (BM + BN) * (64 + 8) * 2; }
+constexpr size_t bf16_gemm_lds() { return 0; }   // the tiles live in the kernel's static LDS (2 (BM + BN) 128 B)
 
 template <typename K>
 int set_lds(K kernel, size_t bytes) {
