@@ -435,6 +435,7 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
     constexpr int AV = BM / 32;                     // 8-row load instructions per wave and K tile
     constexpr int BV = BN / 32;
     static_assert(FN % 2 == 0, "gate/up pairs need an even number of 32-column blocks");
+    static_assert(BM % 64 == 0 && BN % 64 == 0, "an even number of load instructions per wave");
     // two buffers of the A and B tiles, [rows][64] bf16 each
     __shared__ __attribute__((aligned(16))) __bf16 sA0[BM * 64], sA1[BM * 64], sB0[BN * 64], sB1[BN * 64];
 
@@ -469,12 +470,15 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
                                   : (const __bf16*)p.Wr + (size_t)L.g * L.N * K;
         const __amdgpu_buffer_rsrc_t rb_rs = make_rsrc(Bw, (uint32_t)((size_t)L.N * K * 2));
         // LDS rows of 64 K values (128 bytes, unpadded); 16-byte chunk q of
-        // row r holds the operand's chunk q ^ (r & 7), so that the 8 rows a
-        // fragment read takes per group of lanes fall on distinct banks.  Load
-        // instruction v of wave w covers rows (w AV + v) 8 .. +7 of the tile:
-        // lane l takes row + l / 8 and fetches its chunk (l & 7) ^ (l / 8),
-        // which the direct-to-LDS load writes at position l & 7.
-        const int gc = (lane & 7) ^ (lane >> 3);
+        // row r holds the operand's chunk q ^ ((r >> 1) & 7), so that the 16
+        // rows a fragment read serves per LDS cycle (16 lanes of 16 bytes over
+        // the 64 banks) fall on distinct banks.  Load instruction v of wave w
+        // covers rows (w AV + v) 8 .. +7 of the tile: lane l takes row + l / 8
+        // and fetches the chunk that the direct-to-LDS load writes at position
+        // l & 7 of that row, (l & 7) ^ ((r >> 1) & 7); with AV, BV even that is
+        // gc0 for even v and gc1 for odd v.
+        const int gc0 = (lane & 7) ^ (lane >> 4);
+        const int gc1 = (lane & 7) ^ (4 | (lane >> 4));
         const int rsub = lane >> 3;
         // A: the gathered token rows of X (gate/up) or the group's activation rows (down)
         const __bf16* Ab = MODE == 0 ? (const __bf16*)p.X
@@ -486,9 +490,10 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
         for (int v = 0; v < AV; ++v) {
             const int row = L.m0 + (wave * AV + v) * 8 + rsub;
             const uint32_t src = MODE == 0 ? (row < L.R ? (uint32_t)p.row_tok[L.rowbase + row] : 0u) : (uint32_t)row;
-            aoff[v] = row < L.R ? (src * (uint32_t)(MODE == 0 ? p.ldx : K) + gc * 8) * 2u : OOR;
+            aoff[v] = row < L.R ? (src * (uint32_t)(MODE == 0 ? p.ldx : K) + ((v & 1) ? gc1 : gc0) * 8) * 2u : OOR;
         }
-        const uint32_t boff0 = ((uint32_t)(L.n0 + wave * BV * 8 + rsub) * (uint32_t)K + gc * 8) * 2u;
+        const uint32_t brow0 = (uint32_t)(L.n0 + wave * BV * 8 + rsub) * (uint32_t)K;
+        const uint32_t boffe = (brow0 + gc0 * 8) * 2u, boffo = (brow0 + gc1 * 8) * 2u;
         const uint32_t bstride = 16u * (uint32_t)K;       // 8 rows, in bytes
 
         f32x16 acc[FM][FN];
@@ -514,7 +519,8 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
 #pragma unroll
             for (int v = 0; v < BV; ++v)
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(rb_rs, (lds_ptr)(sb + (wave * BV + v) * 8 * 64), 16,
-                                                         boff0 + v * bstride, (uint32_t)k0 * 2u, 0, 0);
+                                                         ((v & 1) ? boffo : boffe) + v * bstride, (uint32_t)k0 * 2u,
+                                                         0, 0);
         };
         const int KT = K / BK;                            // even: K is a multiple of 128
         // fragment of row (lane & 31) of each 32-row block, K chunk 2 ks + lane / 32
@@ -522,7 +528,7 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
         const int brow = (wn * WN + (lane & 31)) * 64;
         bf16x8 af[2][FM], bfm[2][FN];
         auto fload = [&](const __bf16* sa, const __bf16* sb, int ks, int slot) {
-            const int pos = ((2 * ks + (lane >> 5)) ^ (lane & 7)) * 8;
+            const int pos = ((2 * ks + (lane >> 5)) ^ ((lane >> 1) & 7)) * 8;   // row & 31 = lane & 31
 #pragma unroll
             for (int i = 0; i < FM; ++i) af[slot][i] = *(const bf16x8*)(sa + arow + i * 32 * 64 + pos);
 #pragma unroll
