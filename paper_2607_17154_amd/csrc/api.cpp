@@ -186,9 +186,12 @@ static size_t fwd_ws(const ordermoe_experts* W, int64_t T, int32_t k, Carver& c,
     char* ar = c.take<char>((size_t)rr * W->f * esz);
     char* as = c.take<char>((size_t)rs * W->n_shared * W->f * esz);
     char* ob = c.take<char>((size_t)(rr + rs) * W->d * esz);
+    int32_t* sc = c.take<int32_t>(forward_split_counters());
+    float* sp = c.take<float>(forward_split_floats(W->dtype, T));
     if (a) {
         a->blk_rows = br; a->blk_base = bb; a->row_tok = rt; a->row_w = rw; a->tok_rows = tr;
         a->tile_info = ti; a->act_r = ar; a->act_s = as; a->obuf = ob; a->rmax_routed = rr;
+        a->sk_cnt = sc; a->sk_part = sp;
         a->nblk = nblk;
     }
     return c.size();

@@ -102,6 +102,8 @@ struct ForwardArgs {
     void* act_r;           // [rmax_routed][f] routed activations
     void* act_s;           // [T][n_shared * f] shared activations
     void* obuf;            // [rmax][d] per-row outputs
+    float* sk_part;        // bf16 GEMMs: partial tiles of split tiles
+    int32_t* sk_cnt;       // [forward_split_counters()] arrival counters of split tiles
     int64_t rmax_routed;
     int nblk;
 };
@@ -109,6 +111,8 @@ int launch_local_forward(const ForwardArgs& a, void* stream);
 int forward_tokens_per_block();
 bool forward_uses_thin(int dtype, int64_t T);
 void forward_tile_shape(int dtype, int64_t T, int* bm_gu, int* bn_gu, int* bm_dn, int* bn_dn);
+size_t forward_split_counters();
+size_t forward_split_floats(int dtype, int64_t T);
 
 struct SimArgs {
     int dtype, d, E, k;

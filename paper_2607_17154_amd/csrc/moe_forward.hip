@@ -20,7 +20,12 @@
 // is read from device memory, so no host synchronisation is needed.  Tiles of
 // one expert are ordered m-fastest so consecutive tiles share a weight tile,
 // and workgroup ids are remapped so that each XCD (and its L2) works on a
-// contiguous range of tiles.
+// contiguous range of tiles.  The bf16 GEMMs run whole rounds of tiles (one
+// tile per workgroup per round); the tiles left over, fewer than the grid, are
+// cut along K into pieces at the same positions in every tile when that keeps
+// at least two workgroups per tile busy, and the last workgroup to finish a
+// piece of a split tile adds the pieces in a fixed order and runs the
+// epilogue.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -36,6 +41,13 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 constexpr int FT_TB = 256;        // tokens per block in the row kernels
 constexpr int MAXG = ORDERMOE_MAX_LOCAL + 1;
 constexpr int MAXR = ORDERMOE_MAX_TOPK + 1;   // rows per token (routed + shared)
+// bf16 GEMM launches: at most SK_MAX_GRID workgroups.  Split tiles use one
+// partial tile per workgroup (its slot) and one arrival counter per split
+// tile, in one array of SK_MAX_GRID counters per GEMM (gate/up, down), zeroed
+// by the row kernels before every forward.  A tile is cut into at most
+// SK_SPLIT pieces (the last arrival reads them all).
+constexpr int SK_MAX_GRID = 256;
+constexpr int SK_SPLIT = 4;
 
 struct RowsArgs {
     int64_t T;
@@ -52,6 +64,7 @@ struct RowsArgs {
     float* row_w;
     int32_t* tok_rows;        // [T][k+1]
     int32_t* tile_info;       // [4]
+    int32_t* sk_cnt;          // [2][SK_MAX_GRID] split-tile arrival counters, zeroed here
     int nblk;
     // tile geometry for the tile counts
     int bm_gu, bn_gu, bm_dn, bn_dn;
@@ -159,6 +172,7 @@ __global__ void __launch_bounds__(SCAN_THREADS) rows_scan_kernel(const RowsArgs 
     __shared__ int32_t s_tot[MAXG];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int G = a.n_local + a.has_shared;
+    for (int i = tid; i < 2 * SK_MAX_GRID; i += SCAN_THREADS) a.sk_cnt[i] = 0;
     for (int g = wave; g < G; g += SCAN_WAVES) {
         int32_t carry = 0;
         for (int b0 = 0; b0 < a.nblk; b0 += 64) {
@@ -264,6 +278,7 @@ __global__ void __launch_bounds__(SCAN_THREADS) rows_small_kernel(const RowsArgs
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int G = a.n_local + a.has_shared;
     for (int i = tid; i < a.E; i += SCAN_THREADS) s_lidx[i] = a.lidx[i];
+    for (int i = tid; i < 2 * SK_MAX_GRID; i += SCAN_THREADS) a.sk_cnt[i] = 0;
     __syncthreads();
     const int64_t t = tid;
     int grp[MAXR], rank[MAXR];
@@ -349,7 +364,8 @@ struct GemmArgs {
     void* Or;                 // mode 0: routed activations out; mode 1: row outputs [*][Nr]
     void* Os;                 // mode 0: shared activations out; mode 1: unused
     const float* row_w;       // mode 1
-    int head_grid;            // PART 1 and 2: grid of the whole-round launch
+    float* sk_part;           // bf16: [SK_MAX_GRID][BM * BN] partial tiles of split tiles
+    int32_t* sk_cnt;          // bf16: [2][SK_MAX_GRID] arrival counters (zero at launch)
 };
 
 struct TileLoc {
@@ -389,6 +405,7 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void* lds_ptr;
 
 constexpr int BUF_DWORD3 = 0x00020000;   // raw buffer resource word 3 on gfx9-class GPUs
+constexpr int SC1 = 16;                  // buffer load/store cache bit sc1: coherent at agent scope
 
 __device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, BUF_DWORD3);
@@ -416,18 +433,20 @@ __device__ inline void sched_interleave() {
 
 // bf16 grouped GEMM C = A B^T per tile of BM x BN, K step 64, 4 waves (2 x 2),
 // each wave a (BM/2) x (BN/2) block of v_mfma_f32_32x32x16_bf16 tiles.
-// Operands are staged global -> registers -> LDS, double buffered, with rows
-// padded by 16 bytes so that 16-byte fragment reads of 8 consecutive rows hit
-// distinct banks.  Global reads are raw buffer loads: the K position travels in
-// the scalar offset, and rows past the end of a group read as zeros through
-// the buffer range check (their offset is set past the buffer).  Byte offsets
-// inside one operand fit in 31 bits (checked by the host).
+// Operands go from memory straight into LDS (buffer loads to LDS), two
+// buffers; the layout is described at the K loop.  The K position travels in
+// the buffer load's scalar offset, and rows past the end of a group read as
+// zeros through the buffer range check (their offset is set past the buffer).
+// Byte offsets inside one operand fit in 31 bits (checked by the host).
 //
-// PART selects the tiles: 0 all tiles; 1 the whole rounds of tiles, the first
-// head_grid * floor(tiles / head_grid); 2 the remaining tiles of a BM x 2BN
-// tiling, each cut into two BM x BN halves along N, so that the last, partly
-// filled round of big tiles runs as a round of half tiles on all CUs.
-template <int BM, int BN, int MODE, int PART>
+// Work: rounds of whole tiles while a round fills the grid; the tiles left
+// over are cut along K into equal pieces when that puts at least two
+// workgroups on each (split-K), else they run whole as a last, partial round.
+// A piece stores its fp32 partial tile in its slot, and the workgroup whose
+// arrival completes the tile's counter sums the tile's pieces in K order (so
+// the result does not depend on who is last) and runs the epilogue.  No
+// workgroup waits for another.
+template <int BM, int BN, int MODE>
 __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
     constexpr int BK = 64;
     constexpr int WM = BM / 2, WN = BN / 2;
@@ -438,31 +457,54 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
     static_assert(BM % 64 == 0 && BN % 64 == 0, "an even number of load instructions per wave");
     // two buffers of the A and B tiles, [rows][64] bf16 each
     __shared__ __attribute__((aligned(16))) __bf16 sA0[BM * 64], sA1[BM * 64], sB0[BN * 64], sB1[BN * 64];
+    __shared__ int s_last;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
     const int total = *p.ntiles;
-    const int per_xcd = gridDim.x >> 3;
-    const int vid = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+    const int grid = (int)gridDim.x;                // a multiple of 8, at most SK_MAX_GRID
+    const int vid = (blockIdx.x & 7) * (grid >> 3) + (blockIdx.x >> 3);
     constexpr uint32_t OOR = 0x80000000u;           // offset past every buffer: reads zero
-    const int head = PART == 0 ? total : (total / p.head_grid) * p.head_grid;
-    const int ntile = PART == 2 ? 2 * (total - head) : head;
+    const int rounds = total / grid, head = rounds * grid;
 
-    // rounds of G tiles in snake order (odd rounds reversed), so that the
-    // workgroups that took the long tiles at the head of the list take the last
-    // tiles of the next round
-    for (int r = 0;; ++r) {
-        const int tile = r * (int)gridDim.x + ((r & 1) ? (int)gridDim.x - 1 - vid : vid);
-        if (tile >= ntile) {
-            if (r & 1) continue;     // a partial odd round: the high tiles are missing
-            break;
-        }
+    // the tiles left after the whole rounds: when at least two workgroups per
+    // tile are free, each tile is cut along K into `split` pieces at the same
+    // positions in every tile (piece j of the tile at head + i goes to
+    // position j * left + i of the round), so that the workgroups of an XCD
+    // read the same K range of neighbouring tiles together, as in a whole
+    // round.  Positions follow the snake order of the rounds.  Only when all
+    // tiles have the same K: then every workgroup finishes its rounds at about
+    // the same time (a shared group with a longer K keeps some workgroups busy
+    // while the pieces would go out).
+    const int left = total - head;
+    int split = left > 0 ? grid / left : 0;
+    if (split > SK_SPLIT) split = SK_SPLIT;
+    if (split > p.Kr / (2 * BK)) split = p.Kr / (2 * BK);
+    if (p.G > p.n_routed && p.Ks != p.Kr) split = 1;
+
+    for (int r = 0; r <= rounds; ++r) {
         TileLoc L;
-        if (PART == 2) {
-            if (!decode_tile<BM, 2 * BN>(p, head + (tile >> 1), L)) break;
-            L.n0 += (tile & 1) * BN;
-        } else if (!decode_tile<BM, BN>(p, tile, L)) {
-            break;
+        int kt_lo = 0, kt_hi = 0;       // K tiles of 64 of this piece
+        int nseg = 1, ctr = 0, pslot = 0;
+        if (r < rounds || split < 2) {
+            // whole tiles in rounds of `grid`, in snake order (odd rounds
+            // reversed), so that the workgroups that took the long tiles at the
+            // head of the list take the last tiles of the next round; the last
+            // round may be partial
+            const int tile = r * grid + ((r & 1) ? grid - 1 - vid : vid);
+            if (tile >= total || !decode_tile<BM, BN>(p, tile, L)) break;
+            kt_hi = L.K / BK;
+        } else {
+            const int pos = (rounds & 1) ? grid - 1 - vid : vid;
+            if (pos >= split * left) break;
+            const int j = pos / left;
+            ctr = pos - j * left;
+            pslot = pos;
+            if (!decode_tile<BM, BN>(p, head + ctr, L)) break;
+            const int units = L.K / (2 * BK);
+            kt_lo = 2 * (j * units / split);
+            kt_hi = 2 * ((j + 1) * units / split);
+            nseg = split;
         }
         const bool shared = L.g >= p.n_routed;
         const int K = L.K;
@@ -522,7 +564,6 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
                                                          ((v & 1) ? boffo : boffe) + v * bstride, (uint32_t)k0 * 2u,
                                                          0, 0);
         };
-        const int KT = K / BK;                            // even: K is a multiple of 128
         // fragment of row (lane & 31) of each 32-row block, K chunk 2 ks + lane / 32
         const int arow = (wm * WM + (lane & 31)) * 64;
         const int brow = (wn * WN + (lane & 31)) * 64;
@@ -574,15 +615,84 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
             fload(na, nb, 0, 0);
             __builtin_amdgcn_sched_barrier(0);
         };
-        dmaA(sA0, 0);
-        dmaB(sB0, 0);
+        // the piece's K tiles [kt_lo, kt_hi): an even number (K units of 128)
+        dmaA(sA0, kt_lo * BK);
+        dmaB(sB0, kt_lo * BK);
         __builtin_amdgcn_s_waitcnt(0x0F70);
         __syncthreads();
         fload(sA0, sB0, 0, 0);
         __builtin_amdgcn_sched_barrier(0);
-        for (int kt = 0; kt < KT; kt += 2) {
+        for (int kt = kt_lo; kt < kt_hi; kt += 2) {
             ktile(sA0, sB0, sA1, sB1, (kt + 1) * BK);
-            ktile(sA1, sB1, sA0, sB0, (kt + 2 < KT ? kt + 2 : kt + 1) * BK);
+            ktile(sA1, sB1, sA0, sB0, (kt + 2 < kt_hi ? kt + 2 : kt + 1) * BK);
+        }
+
+        if (nseg > 1) {
+            // a piece of a split tile: its partial sums go to slot j left + ctr
+            // (its position in the round), thread
+            // tid's 16-byte group h of block (i, j) at byte
+            // (((i FN + j) 4 + h) 256 + tid) 16 (each store instruction writes
+            // 4 KB in a row).  Buffer stores and loads keep the lane's offset in
+            // one register and the slot and group in the scalar offset.  They
+            // carry the sc1 cache bit (the bit of agent-scope atomic loads and
+            // stores), so each location is coherent across the XCDs' L2 caches
+            // without a whole-cache write-back or invalidate, which would also
+            // evict the tiles of every other workgroup on the XCD.  The stores
+            // complete (vmcnt 0) before the arrival is counted, and the last
+            // arrival's loads are issued after the count is read.
+            constexpr uint32_t TILE_BYTES = (uint32_t)BM * BN * 4u;
+            const __amdgpu_buffer_rsrc_t rp = make_rsrc(p.sk_part, (uint32_t)SK_MAX_GRID * TILE_BYTES);
+            const uint32_t lo = (uint32_t)tid * 16u;
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+#pragma unroll
+                    for (int h = 0; h < 4; ++h) {
+                        const f32x4 v{acc[i][j][4 * h], acc[i][j][4 * h + 1], acc[i][j][4 * h + 2], acc[i][j][4 * h + 3]};
+                        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), rp, (int)lo,
+                                                               (int)((uint32_t)pslot * TILE_BYTES +
+                                                                     (uint32_t)((i * FN + j) * 4 + h) * 4096u), SC1);
+                    }
+            __builtin_amdgcn_s_waitcnt(0x0F70);          // vmcnt(0): this wave's stores are done
+            __syncthreads();
+            if (tid == 0) s_last = atomicAdd(p.sk_cnt + MODE * SK_MAX_GRID + ctr, 1) == nseg - 1;
+            __syncthreads();
+            if (!s_last) continue;
+            // the last arrival: the tile is the sum of its pieces in K order
+            // (piece j in slot j * left + ctr).  Every group reads SK_SPLIT
+            // pieces without a branch, so that the loads of many groups are in
+            // flight together: the pieces past nseg have a lane offset past the
+            // buffer (the range check covers the lane offset) and read as
+            // zeros, and adding them leaves the sum as it is.
+            uint32_t pbase[SK_SPLIT], plo[SK_SPLIT];
+#pragma unroll
+            for (int sg = 0; sg < SK_SPLIT; ++sg) {
+                pbase[sg] = sg < nseg ? (uint32_t)(ctr + sg * left) * TILE_BYTES : 0u;
+                plo[sg] = sg < nseg ? lo : OOR;
+            }
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+#pragma unroll
+                    for (int h = 0; h < 4; ++h) {
+                        const uint32_t go = (uint32_t)((i * FN + j) * 4 + h) * 4096u;
+                        f32x4 pv[SK_SPLIT];
+#pragma unroll
+                        for (int sg = 0; sg < SK_SPLIT; ++sg) {
+                            const uint32_t vo = plo[sg];
+                            pv[sg] = __builtin_bit_cast(
+                                f32x4, __builtin_amdgcn_raw_buffer_load_b128(rp, (int)vo, (int)(pbase[sg] + go), SC1));
+                        }
+                        f32x4 v = pv[0];
+#pragma unroll
+                        for (int sg = 1; sg < SK_SPLIT; ++sg) v += pv[sg];
+                        acc[i][j][4 * h] = v[0];
+                        acc[i][j][4 * h + 1] = v[1];
+                        acc[i][j][4 * h + 2] = v[2];
+                        acc[i][j][4 * h + 3] = v[3];
+                    }
         }
 
         // epilogue: element e of a 32x32 block is row (e/4)*8 + (lane/32)*4 + e%4,
@@ -904,15 +1014,6 @@ constexpr int F32_BM = 64, F32_BN = 64;
 constexpr int64_t THIN_MAX_T = 128;
 constexpr int THIN_PER_CU = 3;
 
-template <int BM, int BN>
-constexpr size_t bf16_gemm_lds() { return 0; }   // the tiles live in the kernel's static LDS (2 (BM + BN) 128 B)
-
-template <typename K>
-int set_lds(K kernel, size_t bytes) {
-    return (int)hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                    (int)bytes);
-}
-
 int persistent_grid(int64_t upper_tiles, int per_cu) {
     int dev = 0, cus = 256;
     if (hipGetDevice(&dev) == hipSuccess) {
@@ -925,7 +1026,22 @@ int persistent_grid(int64_t upper_tiles, int per_cu) {
     return (int)(g < 8 ? 8 : g);
 }
 
+// grid of a bf16 GEMM launch: up to SK_SPLIT workgroups per tile (the split
+// tiles are shared out over them), at most SK_MAX_GRID
+int bf16_grid(int64_t upper_tiles) {
+    const int g = persistent_grid((int64_t)SK_SPLIT * upper_tiles, 1);
+    return g < SK_MAX_GRID ? g : SK_MAX_GRID;
+}
+
 }  // namespace
+
+size_t forward_split_counters() { return 2 * SK_MAX_GRID; }
+
+size_t forward_split_floats(int dtype, int64_t T) {
+    if (dtype != ORDERMOE_BF16 || forward_uses_thin(dtype, T)) return 0;
+    const size_t tile = (size_t)GU_BM * GU_BN > (size_t)DN_BM * DN_BN ? (size_t)GU_BM * GU_BN : (size_t)DN_BM * DN_BN;
+    return (size_t)SK_MAX_GRID * tile;
+}
 
 int forward_tokens_per_block() { return FT_TB; }
 
@@ -951,7 +1067,7 @@ int launch_local_forward(const ForwardArgs& f, void* stream) {
     for (int i = 0; i < ORDERMOE_MAX_EXPERTS; ++i) r.lidx[i] = f.lidx[i];
     r.blk_rows = f.blk_rows; r.blk_base = f.blk_base; r.row_offsets = f.row_offsets;
     r.row_tok = f.row_tok; r.row_w = f.row_w; r.tok_rows = f.tok_rows; r.tile_info = f.tile_info;
-    r.nblk = f.nblk;
+    r.sk_cnt = f.sk_cnt; r.nblk = f.nblk;
     r.bm_gu = bm_gu; r.bn_gu = bn_gu; r.bm_dn = bm_dn; r.bn_dn = bn_dn;
     r.n_gu_r = 2 * f.f; r.n_gu_s = 2 * f.n_shared * f.f; r.n_dn = f.d;
 
@@ -985,6 +1101,7 @@ int launch_local_forward(const ForwardArgs& f, void* stream) {
     g.offsets = f.row_offsets; g.G = G; g.n_routed = f.n_local;
     g.X = f.x; g.row_tok = f.row_tok; g.ldx = f.d; g.row_w = f.row_w;
     g.x_bytes = (uint32_t)((size_t)f.T * f.d * (f.dtype == ORDERMOE_BF16 ? 2 : 4));
+    g.sk_part = f.sk_part; g.sk_cnt = f.sk_cnt;
 
     // gate/up: [rows][d] x [2f][d]^T -> activations [rows][f]
     g.ntiles = f.tile_info + 0;
@@ -1002,26 +1119,9 @@ int launch_local_forward(const ForwardArgs& f, void* stream) {
         }
         if ((e = hipGetLastError()) != hipSuccess) return (int)e;
     } else if (f.dtype == ORDERMOE_BF16) {
-        static int lds_ok = -1;
-        if (lds_ok < 0) {
-            lds_ok = set_lds(ggemm_bf16<GU_BM, GU_BN, 0, 1>, bf16_gemm_lds<GU_BM, GU_BN>()) |
-                     set_lds(ggemm_bf16<GU_BM, GU_BN / 2, 0, 2>, bf16_gemm_lds<GU_BM, GU_BN / 2>()) |
-                     set_lds(ggemm_bf16<DN_BM, DN_BN, 1, 0>, bf16_gemm_lds<DN_BM, DN_BN>());
-        }
-        if (lds_ok) return lds_ok;
-        // whole rounds of 256 x 256 tiles, then the rest as 256 x 128 halves
-        const int grid_gu = persistent_grid(ub_gu, 1);
-        g.head_grid = grid_gu;
         {
         KernelTimer kt_("gemm_gate_up", st);
-        ggemm_bf16<GU_BM, GU_BN, 0, 1>
-            <<<dim3(grid_gu), dim3(256), bf16_gemm_lds<GU_BM, GU_BN>(), st>>>(g);
-        }
-        if ((e = hipGetLastError()) != hipSuccess) return (int)e;
-        {
-        KernelTimer kt_("gemm_gate_up_tail", st);
-        ggemm_bf16<GU_BM, GU_BN / 2, 0, 2>
-            <<<dim3(persistent_grid(2 * (int64_t)grid_gu, 1)), dim3(256), bf16_gemm_lds<GU_BM, GU_BN / 2>(), st>>>(g);
+        ggemm_bf16<GU_BM, GU_BN, 0><<<dim3(bf16_grid(ub_gu)), dim3(256), 0, st>>>(g);
         }
         if ((e = hipGetLastError()) != hipSuccess) return (int)e;
     } else {
@@ -1044,8 +1144,7 @@ int launch_local_forward(const ForwardArgs& f, void* stream) {
     } else if (f.dtype == ORDERMOE_BF16) {
         {
         KernelTimer kt_("gemm_down", st);
-        ggemm_bf16<DN_BM, DN_BN, 1, 0>
-            <<<dim3(persistent_grid(ub_dn, 1)), dim3(256), bf16_gemm_lds<DN_BM, DN_BN>(), st>>>(g);
+        ggemm_bf16<DN_BM, DN_BN, 1><<<dim3(bf16_grid(ub_dn)), dim3(256), 0, st>>>(g);
         }
     } else {
         {
