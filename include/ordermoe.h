@@ -401,10 +401,18 @@ typedef struct {
     const void* w_shared_down;   /* dev [d][n_shared*f] (the n_shared W_down side by side) */
 } ordermoe_experts;
 
-/* Requirements: d % 128 == 0, f % 64 == 0; T >= 0; 1 <= k <= ORDERMOE_MAX_TOPK.
+/* Requirements: bf16 d % 256 == 0 and f % 128 == 0, fp32 d % 64 == 0 and
+ * f % 32 == 0 (else ORDERMOE_EINVAL); weights, x and y 16-byte aligned;
+ * T >= 0; 1 <= k <= ORDERMOE_MAX_TOPK.
  * w, exec_k, exec_m: dev [T][k] as written by ordermoe_route_select.
  * y: dev [T][d].  row_offsets: dev [n_local + 2] int32, out: start row of
- * each local expert, then of the shared rows, then the total row count. */
+ * each local expert, then of the shared rows, then the total row count.
+ * ws: dev, at least ordermoe_forward_workspace_size(W, T, k) bytes (else
+ * ORDERMOE_EWORKSPACE): row tables, the activations, the per-row outputs and,
+ * for bf16 batches above 128 tokens, 64 MiB of fp32 partial tiles for GEMM
+ * tiles split along K (summed in K order, so results are deterministic).  The
+ * call uses it until the stream passes the call; calls in flight at the same
+ * time need workspaces of their own. */
 size_t ordermoe_forward_workspace_size(const ordermoe_experts* W, int64_t T, int32_t k);
 int ordermoe_local_moe_forward(const ordermoe_experts* W, const void* x, int64_t T, int32_t k,
                                const float* w, const int32_t* exec_k, const uint8_t* exec_m,
