@@ -629,10 +629,9 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
 
         if (nseg > 1) {
             // a piece of a split tile: its partial sums go to slot j left + ctr
-            // (its position in the round), thread
-            // tid's 16-byte group h of block (i, j) at byte
-            // (((i FN + j) 4 + h) 256 + tid) 16 (each store instruction writes
-            // 4 KB in a row).  Buffer stores and loads keep the lane's offset in
+            // (its position in the round), thread tid's 16-byte group h of
+            // block (i, j) at byte (((i FN + j) 4 + h) 256 + tid) 16 of the slot
+            // (each store instruction writes 4 KB in a row).  Buffer stores and loads keep the lane's offset in
             // one register and the slot and group in the scalar offset.  They
             // carry the sc1 cache bit (the bit of agent-scope atomic loads and
             // stores), so each location is coherent across the XCDs' L2 caches
@@ -664,7 +663,8 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
             // pieces without a branch, so that the loads of many groups are in
             // flight together: the pieces past nseg have a lane offset past the
             // buffer (the range check covers the lane offset) and read as
-            // zeros, and adding them leaves the sum as it is.
+            // zeros, and adding them leaves the sum as it is (up to the sign of
+            // a zero).
             uint32_t pbase[SK_SPLIT], plo[SK_SPLIT];
 #pragma unroll
             for (int sg = 0; sg < SK_SPLIT; ++sg) {
