@@ -919,8 +919,7 @@ def main():
     for _ in range(args.warmup):
         _step(cfg, st, om)
     torch.cuda.synchronize()
-    om.ordermoe_timing_read(reset=True)
-    om.ordermoe_timing_enable(True)
+    # the timed steps, as a caller runs them (no per-kernel events)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     e0.record()
@@ -928,10 +927,26 @@ def main():
         _step(cfg, st, om)
     e1.record()
     torch.cuda.synchronize()
-    om.ordermoe_timing_enable(False)
     ms = e0.elapsed_time(e1)
-    kt = om.ordermoe_timing_read(reset=True)
     print("bench: %d steps in %.3f ms" % (args.steps, ms), file=sys.stderr, flush=True)
+    # the same number of steps again with the library's HIP events around every
+    # kernel launch (on the launch stream), for the per-kernel durations; the
+    # events themselves add time between the kernels, so this pass is not the
+    # step time
+    om.ordermoe_timing_read(reset=True)
+    om.ordermoe_timing_enable(True)
+    e2, e3 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e2.record()
+    for _ in range(args.steps):
+        _step(cfg, st, om)
+    e3.record()
+    torch.cuda.synchronize()
+    om.ordermoe_timing_enable(False)
+    ms_events = e2.elapsed_time(e3)
+    kt = om.ordermoe_timing_read(reset=True)
+    print("bench: %d steps with per-kernel events in %.3f ms" % (args.steps, ms_events), file=sys.stderr,
+          flush=True)
 
     rows = st["ro"].cpu().numpy()
     R = int(rows[-1])
@@ -965,6 +980,7 @@ def main():
                      "traffic": _measured_traffic(), "flop_per_launch": gu_flops,
                      "avg_launch_us": gu_avg_s * 1e6},
         "kernels_avg_us": {k: v[0] / v[1] * 1e3 for k, v in sorted(kt.items())},
+        "ms_per_step_with_kernel_events": ms_events / args.steps,
         "mfma_frac_ffn": (2.0 * R * cfg.d * 3 * cfg.f) / (ms_step / 1e3) / 1e12 / PEAK_BF16_TFLOPS,
     }
     if not args.no_simbuild:
