@@ -8,10 +8,13 @@ the local grouped SwiGLU FFN with the weighted combine
 servers holding 2 experts each -- bf16, synthetic seeded inputs, inputs
 resident in HBM before the timed region.
 
-Prints one JSON line (rank 0).  Besides tokens/s it reports the roofline of
-the dominant kernel (the grouped gate/up GEMM) from its average launch time
-measured with HIP events over the timed region, and the CPU oracle timed on a
-bounded sample of the same workload.
+Prints one compact JSON line (rank 0).  Besides tokens/s it reports the
+roofline of the dominant kernel (the grouped gate/up GEMM) from its average
+launch time measured with HIP events on the launch stream, and the CPU oracle
+timed on a bounded sample of the same workload.  The other legs (the Qwen- and
+DeepSeek-shaped layers, the similarity build, the sweeps, the decode stream)
+go to a JSON file (--out, by default gpurun_out/bench_full.json); the line
+carries one figure of each.
 """
 from __future__ import annotations
 
@@ -868,6 +871,8 @@ def main():
                     help="run one leg alone (for profiling): the layer step without the other "
                          "legs, or only the similarity build / decode stream (prints that leg's "
                          "JSON object)")
+    ap.add_argument("--out", default=os.path.join(ROOT, "gpurun_out", "bench_full.json"),
+                    help="file that receives every leg's results (stdout gets one compact line)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a 1 GiB device copy (to scale rocprofv3 byte counters)")
     args = ap.parse_args()
@@ -957,8 +962,21 @@ def main():
     gu_flops = 2.0 * R * cfg.d * (2 * cfg.f)          # gate and up projections of R rows
     achieved = gu_flops / gu_avg_s / 1e12
     ms_step = ms / args.steps
+    metric = "MoE-layer tokens/s on 1 MI355X (route+substitute+grouped FFN); % MFMA peak"
+    roofline = {"bound": "mfma", "kernel": "gemm_gate_up", "achieved": achieved,
+                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
+                "traffic": _measured_traffic(), "flop_per_launch": gu_flops,
+                "avg_launch_us": gu_avg_s * 1e6}
+    config = {"workload": cfg.name,
+              "why": "the Mixtral-8x7B-shaped layer: the paper's headline model (its latency, "
+                     "traffic and throughput results are on Mixtral-8x7B); the DeepSeek-shaped "
+                     "layer carries more FLOPs but is not a model the paper evaluates",
+              "tokens": cfg.T, "hidden": cfg.d, "experts": cfg.E, "ffn": cfg.f, "top_k": cfg.k,
+              "servers": cfg.M, "server": cfg.m0, "local_experts": st["local"], "local_rows": R,
+              "classes_LE_LS_RE_RS": [int(v) for v in counters[:4]],
+              "flagged_tokens": int(counters[4]), "remote_transfers": int(counters[5])}
     res = {
-        "metric": "MoE-layer tokens/s on 1 MI355X (route+substitute+grouped FFN); % MFMA peak",
+        "metric": metric,
         "value": cfg.T * args.steps / (ms / 1e3),
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -970,15 +988,8 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded; random-init expert and router weights of the layer shape)",
-        "config": {"workload": cfg.name, "tokens": cfg.T, "hidden": cfg.d, "experts": cfg.E,
-                   "ffn": cfg.f, "top_k": cfg.k, "servers": cfg.M, "server": cfg.m0,
-                   "local_experts": st["local"], "local_rows": R,
-                   "classes_LE_LS_RE_RS": [int(v) for v in counters[:4]],
-                   "flagged_tokens": int(counters[4]), "remote_transfers": int(counters[5])},
-        "roofline": {"bound": "mfma", "kernel": "gemm_gate_up", "achieved": achieved,
-                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
-                     "traffic": _measured_traffic(), "flop_per_launch": gu_flops,
-                     "avg_launch_us": gu_avg_s * 1e6},
+        "config": config,
+        "roofline": roofline,
         "kernels_avg_us": {k: v[0] / v[1] * 1e3 for k, v in sorted(kt.items())},
         "ms_per_step_with_kernel_events": ms_events / args.steps,
         "mfma_frac_ffn": (2.0 * R * cfg.d * 3 * cfg.f) / (ms_step / 1e3) / 1e12 / PEAK_BF16_TFLOPS,
@@ -1017,7 +1028,49 @@ def main():
     if not args.no_cpu_baseline:
         print("bench: timing the CPU oracle", file=sys.stderr, flush=True)
         res["cpu_baseline"] = _cpu_baseline(cfg, st, args.cpu_seconds)
-    print(json.dumps(res))
+    # every leg goes to the results file; stdout gets one compact line
+    out_path = args.out
+    os.makedirs(os.path.dirname(os.path.abspath(out_path)), exist_ok=True)
+    with open(out_path, "w") as fh:
+        json.dump(res, fh, indent=1)
+    print("bench: all legs written to %s" % out_path, file=sys.stderr, flush=True)
+    print(json.dumps(_compact(res, out_path)))
+
+
+def _compact(res: dict, out_path: str) -> dict:
+    """The headline line: the metric on the Mixtral-shaped layer, the gate/up
+    GEMM's roofline, the CPU oracle, and one figure per other leg."""
+    line = {k: res[k] for k in ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step",
+                                "higher_is_better", "scaling", "vs_baseline", "dtype", "data")}
+    cfgd = res["config"]
+    line["config"] = {k: cfgd[k] for k in ("workload", "why", "local_rows", "classes_LE_LS_RE_RS",
+                                           "flagged_tokens")}
+    rf = res["roofline"]
+    line["roofline"] = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in rf.items()}
+    ka = res["kernels_avg_us"]
+    line["kernels_avg_us"] = {k: round(v, 1) for k, v in ka.items()}
+    if "cpu_baseline" in res:
+        cb = res["cpu_baseline"]
+        line["cpu_baseline"] = {k: cb[k] for k in ("value", "unit", "cores", "kind", "sample")}
+        line["cpu_baseline"]["os_cpu_count"] = os.cpu_count()
+        line["cpu_baseline"]["OMP_NUM_THREADS"] = os.environ.get("OMP_NUM_THREADS")
+    other = {}
+    for key, v in res.get("other_layers", {}).items():
+        other[key] = {"ms_per_step": round(v["ms_per_step"], 4), "tokens_per_s": round(v["tokens_per_s"]),
+                      "gate_up_frac": round(v["gemm_gate_up_frac"], 3),
+                      "down_frac": round(v["gemm_down_frac"], 3),
+                      "route_hbm_frac": round(v["route_hbm_frac"], 3)}
+    if "similarity_build" in res:
+        sb = res["similarity_build"]
+        other["C5_build"] = {"device_us": round(sb["device_us"], 1), "hbm_frac": round(sb["hbm_frac"], 3)}
+    if "decode_stream" in res:
+        ds = res["decode_stream"]
+        other["C5_stream"] = {"us_per_layer": round(ds["us_per_layer"], 1),
+                              "hbm_frac_ffn_gemms": round(ds["hbm_frac_ffn_gemms"], 3)}
+    if other:
+        line["other"] = other
+    line["details"] = os.path.relpath(out_path, ROOT) if out_path.startswith(ROOT) else out_path
+    return line
 
 
 if __name__ == "__main__":

@@ -403,7 +403,11 @@ typedef struct {
 
 /* Requirements: bf16 d % 256 == 0 and f % 128 == 0, fp32 d % 64 == 0 and
  * f % 32 == 0 (else ORDERMOE_EINVAL); weights, x and y 16-byte aligned;
- * T >= 0; 1 <= k <= ORDERMOE_MAX_TOPK.
+ * T >= 0; 1 <= k <= ORDERMOE_MAX_TOPK.  Each operand the GEMMs read must span
+ * fewer than 2^31 bytes (else ORDERMOE_EINVAL, and the workspace size is 0):
+ * T*d, 2*f*d, 2*max(n_shared,1)*f*d and T*max(n_shared,1)*f elements times the
+ * element size (bf16: T*d < 2^30 and T*f < 2^30, so at d = 4096 and
+ * f = 14336 at most 74898 tokens per call).
  * w, exec_k, exec_m: dev [T][k] as written by ordermoe_route_select.
  * y: dev [T][d].  row_offsets: dev [n_local + 2] int32, out: start row of
  * each local expert, then of the shared rows, then the total row count.

@@ -23,7 +23,11 @@ Pins (tests/test_oracle_*.py): brute-force cosine and textbook top-k;
 a cosine limit for Gaussian calibration inputs; exact MoE when substitution is
 off; all-local deployments giving no remote slots; Properties 1 and 2 of the
 paper; hand-traced placements; exhaustive enumeration of eq 43 on tiny layers;
-H = 1 giving Phi = 0 and a closed form of Phi for all-local deployments.
+H = 1 giving Phi = 0 and a closed form of Phi for all-local deployments;
+hand-traced look-ahead values where a budget-free substitute or an unpinned
+remote copy is the future minimum; a literal path expansion of eq 42 and the
+expected realized cost of the trajectory it induces (Property 3) on tiny
+random stacks with every selection mode.
 Parity unpinned: the paper prints no worked numeric example (no Sim values,
 groups, placements or per-token decisions), so no value here is checked
 against a number printed in the paper.

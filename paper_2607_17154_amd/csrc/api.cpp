@@ -226,8 +226,24 @@ static int check_experts(const ordermoe_experts* W) {
     return ORDERMOE_OK;
 }
 
+// The GEMMs address each operand through a buffer resource with 32-bit byte
+// offsets and mark rows past a group's end with offset 2^31, so every operand
+// they read must span fewer than 2^31 bytes: the token rows (T x d), one
+// expert's packed gate/up weights (2f x d) and down weights (d x f), the shared
+// experts' concatenated weights (2 n_shared f x d, d x n_shared f), and one
+// group's activation rows (at most T rows of f, or of n_shared f).
+static bool operands_fit_31_bits(const ordermoe_experts* W, int64_t T) {
+    const int64_t lim = ((int64_t)1 << 31) - 1;
+    const int64_t esz = W->dtype == ORDERMOE_BF16 ? 2 : 4;
+    const int64_t ns = W->n_shared > 0 ? W->n_shared : 1;
+    const int64_t d = W->d, f = W->f;
+    return T * d * esz <= lim && 2 * f * d * esz <= lim && 2 * ns * f * d * esz <= lim &&
+           T * ns * f * esz <= lim;
+}
+
 extern "C" size_t ordermoe_forward_workspace_size(const ordermoe_experts* W, int64_t T, int32_t k) {
     if (check_experts(W) != ORDERMOE_OK || T < 0 || k < 1 || k > ORDERMOE_MAX_TOPK) return 0;
+    if (!operands_fit_31_bits(W, T)) return 0;
     Carver c(nullptr);
     return fwd_ws(W, T, k, c, nullptr);
 }
@@ -242,6 +258,9 @@ extern "C" int ordermoe_local_moe_forward(const ordermoe_experts* W, const void*
     if (k < 1 || k > ORDERMOE_MAX_TOPK) return fail(ORDERMOE_EINVAL, "local_moe_forward: k out of range");
     if (T < 0 || T > ((int64_t)1 << 31) / (ORDERMOE_MAX_TOPK + 1))
         return fail(ORDERMOE_EINVAL, "local_moe_forward: T out of range");
+    if (!operands_fit_31_bits(W, T))
+        return fail(ORDERMOE_EINVAL, "local_moe_forward: T*d, 2*f*d, 2*n_shared*f*d and T*n_shared*f elements "
+                                     "must each span fewer than 2^31 bytes");
     if (server < 0 || server >= ORDERMOE_MAX_SERVERS) return fail(ORDERMOE_EINVAL, "local_moe_forward: server out of range");
     if (!row_offsets) return fail(ORDERMOE_EINVAL, "local_moe_forward: null row_offsets");
     if (T > 0 && (!x || !w || !exec_k || !exec_m || !loc_in || !y))

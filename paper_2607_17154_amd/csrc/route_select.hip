@@ -613,7 +613,8 @@ route_select_kernel(const RouteArgs a) {
                 const int m = __builtin_ctz(msv[slot]);
                 msv[slot] &= msv[slot] - 1;
                 const float J = fmaf(a.cq, qe[slot], Stab[((int64_t)s_loc * M + m) * E + ke[slot]]);
-                const uint64_t cand = ((uint64_t)__float_as_uint(J) << 32) | ((uint32_t)j << 16) |
+                // J's order as a float (negative costs included; -0 counts as +0)
+                const uint64_t cand = ((uint64_t)f2ord(J == 0.f ? 0.f : J) << 32) | ((uint32_t)j << 16) |
                                       ((uint32_t)(m != s_loc) << 15) | ((uint32_t)m << 8) |
                                       (uint32_t)ke[slot];
                 key[slot] = cand < key[slot] ? cand : key[slot];

@@ -253,6 +253,43 @@ def test_workspace_sizes_are_monotone():
     assert 0 < s1 < s2
 
 
+def test_forward_rejects_operands_past_31_bit_offsets():
+    """The GEMMs address operands with 32-bit byte offsets: T*d*esz, 2*f*d*esz,
+    2*n_shared*f*d*esz and T*n_shared*f*esz must stay below 2^31 (no launch)."""
+    ids = np.array([0, 4], np.int32)
+
+    def experts(d, f, n_shared=0):
+        ex = om.Experts(dtype=om.BF16, d=d, f=f, E=8, n_local=2, n_shared=n_shared)
+        ex.local_experts = ids.ctypes.data_as(ctypes.c_void_p)
+        ex.w_gate_up = ex.w_down = 16
+        if n_shared:
+            ex.w_shared_gate_up = ex.w_shared_down = 16
+        return ex
+
+    L = om.lib()
+    ex = experts(4096, 1024)
+    assert L.ordermoe_forward_workspace_size(ctypes.byref(ex), (1 << 18) - 1, 2) > 0   # T*d*2 < 2^31
+    assert L.ordermoe_forward_workspace_size(ctypes.byref(ex), 1 << 18, 2) == 0        # T*d*2 = 2^31
+    p = ctypes.c_void_p(16)
+    rc = L.ordermoe_local_moe_forward(ctypes.byref(ex), p, 1 << 18, 2, p, p, p, p, 0, p, p, p, 1 << 40, None)
+    assert rc == om.EINVAL and "2^31" in om.last_error()
+    # one expert's activation rows (at most T of them): T f 2 bytes
+    ex = experts(256, 14336)
+    assert L.ordermoe_forward_workspace_size(ctypes.byref(ex), 74898, 2) > 0
+    assert L.ordermoe_forward_workspace_size(ctypes.byref(ex), 74899, 2) == 0
+    # one expert's packed gate/up weights: 2 f d 2 bytes
+    ex = experts(32768, 16384)                                 # 2^31 bytes exactly
+    assert L.ordermoe_forward_workspace_size(ctypes.byref(ex), 16, 2) == 0
+    ex = experts(32768, 16384 - 128)
+    assert L.ordermoe_forward_workspace_size(ctypes.byref(ex), 16, 2) > 0
+    # the shared experts side by side, and their activation rows
+    ex = experts(4096, 14336, n_shared=16)                     # 2 * 16 * f * d * 2 > 2^31
+    assert L.ordermoe_forward_workspace_size(ctypes.byref(ex), 16, 2) == 0
+    ex = experts(256, 16384, n_shared=4)                       # 2 n f d 2 = 2^26; T n f 2 >= 2^31 at T = 2^14
+    assert L.ordermoe_forward_workspace_size(ctypes.byref(ex), (1 << 14) - 1, 2) > 0
+    assert L.ordermoe_forward_workspace_size(ctypes.byref(ex), 1 << 14, 2) == 0
+
+
 def test_weight_adaptation_oracle_pins():
     """eq 45: a step of kappa (Q_bar - T_bar) on omega_Q, projected onto [0, 1],
     with omega_T = 1 - omega_Q."""
