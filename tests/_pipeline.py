@@ -285,3 +285,42 @@ def with_horizon(sc: StreamCase, H: int, allow_sub: Optional[int] = None) -> Str
     S = [tables.static_cost(cfg.M, cfg.E, sc.z_bits, sc.net.B, sc.net.tau, sc.c, sc.net.F, sc.dref,
                             cfg.omega_T, phi[l]) for l in range(cfg.N)]
     return dataclasses.replace(sc, cfg=cfg, phi=phi, S=S)
+
+
+# ------------------------------------------------------------ GEMM work plan (host mirror)
+# The bf16 grouped GEMMs of the local forward (batches above 128 tokens) run
+# 256 x 256 gate/up tiles and 192 x 256 down tiles over a persistent grid of at
+# most 256 workgroups (one per CU on MI355X, at most four per tile); the tiles
+# left after whole rounds are cut along K into up to 4 pieces when at least two
+# workgroups per tile are free and every group has the same K.  Tests use this
+# mirror to know which of their shapes exercise the split.
+def gemm_plan(cfg, rows, n_local: int, cus: int = 256):
+    """rows: the forward's row_offsets output [n_local + 2].  Returns
+    {"gate_up": (tiles, grid, rounds, left, split), "down": (...)}."""
+    R = np.diff(np.asarray(rows, dtype=np.int64))       # rows per group, shared last
+    has_sh = cfg.n_shared > 0
+    T, k, d, f, ns = cfg.T, cfg.k, cfg.d, cfg.f, cfg.n_shared
+    rr = T * min(k, n_local)
+    rs = T if has_sh else 0
+
+    def grid_of(ub):
+        g = min(cus, 4 * ub)
+        g = (g + 7) & ~7
+        return min(max(g, 8), 256)
+
+    def plan(bm, bn, Nr, Ns, Kr, Ks, ub):
+        tiles = sum(-(-int(R[g]) // bm) * (Nr // bn) for g in range(n_local))
+        if has_sh:
+            tiles += -(-int(R[n_local]) // bm) * (Ns // bn)
+        grid = grid_of(ub)
+        rounds = tiles // grid
+        left = tiles - rounds * grid
+        split = min(grid // left, 4, Kr // 128) if left else 0
+        if has_sh and Ks != Kr:
+            split = 1
+        return tiles, grid, rounds, left, split
+
+    ub_gu = (-(-rr // 256) + n_local) * (2 * f // 256) + ((-(-rs // 256) + 1) * (2 * ns * f // 256) if has_sh else 0)
+    ub_dn = (-(-(rr + rs) // 192) + n_local + int(has_sh)) * (d // 256)
+    return {"gate_up": plan(256, 256, 2 * f, 2 * ns * f, d, d, ub_gu),
+            "down": plan(192, 256, d, d, f, ns * f, ub_dn)}

@@ -1,6 +1,6 @@
 """Transition statistics (eq 41) and the look-ahead cost-to-go (eq 42) built on
-the device, through the C ABI, against the host library's bit for bit (the
-host routines equal the oracle's, tests/test_stream_tables.py)."""
+the device, through the C ABI: against the oracle's transitions and Phi
+(exact / within 1e-12 relative), and against the host library's bit for bit."""
 import numpy as np
 import pytest
 
@@ -33,6 +33,11 @@ def test_device_transitions_equal_the_host_estimate(N, E, T):
         return
     want = om.ordermoe_estimate_transitions(top1, E)
     np.testing.assert_array_equal(got.cpu().numpy(), want)
+    # the oracle's estimate (eq 41): counts over the same tokens, row-normalised
+    from oracle import tables
+    P_or = tables.transitions([top1[l] for l in range(N)], [E] * N)
+    for l in range(N - 1):
+        np.testing.assert_allclose(got.cpu().numpy()[l], P_or[l], rtol=1e-15, atol=0, err_msg="layer %d" % l)
 
 
 def _device_phi(sc, H, allow_sub, pin):
@@ -57,11 +62,18 @@ def _device_phi(sc, H, allow_sub, pin):
 def test_device_lookahead_equals_the_host_tables(stream_case, H, allow_sub, pin):
     """The 32-layer stack (128 experts, 8 servers): Phi^(H-1) of every layer."""
     import dataclasses
+    from oracle import tables
     sc = with_horizon(stream_case, H, allow_sub=allow_sub)
     sc = dataclasses.replace(sc, cfg=dataclasses.replace(sc.cfg, pin_local_exact=pin))
+    cfg = sc.cfg
     _, phi_host, _ = stream_library_tables(sc)
     got = _device_phi(sc, H, allow_sub, pin)
+    # the oracle's Phi^(H-1) of the same stack and mode
+    phi_or = tables.lookahead(H, sc.P, sc.x_dep, sc.sim32, [m["group_of"] for m in sc.models], sc.theta,
+                              [sc.z_bits] * cfg.N, sc.net.B, sc.net.tau, [sc.c] * cfg.N, sc.net.F,
+                              [sc.dref] * cfg.N, cfg.omega_T, cfg.omega_Q, cfg.Qbar, pin, allow_sub)
     for l in range(sc.cfg.N):
+        np.testing.assert_allclose(got[l], phi_or[l], rtol=1e-12, atol=0, err_msg="oracle, layer %d" % l)
         np.testing.assert_array_equal(got[l], phi_host[l], err_msg="layer %d" % l)
     if H == 1:
         assert np.all(got == 0)

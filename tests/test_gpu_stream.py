@@ -4,9 +4,11 @@ Each layer's route/select reads the locations and accumulated losses the
 previous layer wrote on the device (Algorithm 2's loop over layers), with the
 layer's threshold (eq 6) and look-ahead tables (eq 41-42, H = 3).  The oracle
 runs the same chain from its own outputs.  A token whose router margin falls
-below 1e-4 on either side at some layer is flagged there; its decisions are
-compared up to that layer and it is left out afterwards (its later state may
-legitimately differ), and the number of such tokens is reported.  Property 2
+below 1e-4 on either side at some layer is flagged there and its decisions at
+that layer are not compared; the oracle then takes the GPU's recorded location
+and accumulated loss for it, so every token enters every layer in the same
+state on both sides and every unflagged (token, layer) pair is compared (the
+count is asserted).  Property 2
 (the accumulated loss never exceeds the budget) is checked on every token at
 every layer.  The local expert FFN of server 0 is checked at the first and
 the last layer against the oracle's output."""
@@ -63,18 +65,20 @@ def _gpu_chain(sc, keep_layers=()):
 
 def _oracle_chain(sc, gpu_layers):
     """The oracle's own chain: per layer its decisions, the locations it started
-    from, and the tokens not flagged (on either side) up to that layer."""
+    from, and the tokens not flagged (on either side) at that layer.  After a
+    layer, a flagged token's location and accumulated loss are re-synced to the
+    values the GPU recorded for it (its decision may legitimately differ)."""
     cfg = sc.cfg
     loc = np.zeros(cfg.T, np.uint8)
     qh = np.zeros(cfg.T, np.float32)
-    live = np.ones(cfg.T, bool)
     res = []
     for l in range(cfg.N):
         dec = stream_oracle_layer(sc, l, loc, qh)
-        flag = (dec["margin"] < 1e-4) | (gpu_layers[l]["margin"] < 1e-4)
-        live = live & ~flag
-        res.append(dict(dec=dec, loc_in=loc, live=live, flag=flag))
-        loc, qh = dec["loc_out"], dec["qhat_out"]
+        g = gpu_layers[l]
+        flag = (dec["margin"] < 1e-4) | (g["margin"] < 1e-4)
+        res.append(dict(dec=dec, loc_in=loc, qhat_in=qh, live=~flag, flag=flag))
+        loc = np.where(flag, g["loc_out"], dec["loc_out"]).astype(np.uint8)
+        qh = np.where(flag, g["qhat_out"], dec["qhat_out"]).astype(np.float32)
     return res
 
 
@@ -85,12 +89,18 @@ def _compare_chain(sc, gpu_layers, oracle_chain):
     cfg = sc.cfg
     T, k = cfg.T, cfg.k
     exhausted_layer = None
+    compared = flagged = 0
     for l in range(cfg.N):
         g = gpu_layers[l]
         dec, loc, live, flag = (oracle_chain[l][n] for n in ("dec", "loc_in", "live", "flag"))
         if l > 0:
             np.testing.assert_array_equal(g["loc_in"], gpu_layers[l - 1]["loc_out"])
+            # both sides start the layer in the same state, every token
+            np.testing.assert_array_equal(oracle_chain[l]["qhat_in"], gpu_layers[l - 1]["qhat_out"])
+        np.testing.assert_array_equal(g["loc_in"], loc, err_msg="H %d layer %d loc_in" % (cfg.H, l))
         ok = live
+        compared += int(ok.sum())
+        flagged += int(flag.sum())
         for n in ("idx", "exec_k", "exec_m", "cls", "qhat_out", "loc_out"):
             np.testing.assert_array_equal(g[n][ok], dec[n][ok], err_msg="H %d layer %d %s" % (cfg.H, l, n))
         # Property 2 on every token, flagged or not
@@ -111,10 +121,10 @@ def _compare_chain(sc, gpu_layers, oracle_chain):
             exhausted_layer = l
         print("H %d layer %2d: LE/LS/RE/RS %s  flagged %d  compared %d  max Qhat %.4f" % (
             cfg.H, l, list(c[:4]), int(flag.sum()), int(ok.sum()), float(g["qhat_out"].max())), flush=True)
-    live = oracle_chain[-1]["live"]
-    print("H %d: live tokens after %d layers: %d of %d; substitution stops at layer %s"
-          % (cfg.H, cfg.N, int(live.sum()), T, exhausted_layer), flush=True)
-    assert live.sum() >= T // 2
+    print("H %d: %d of %d (token, layer) pairs compared, %d flagged; substitution stops at layer %s"
+          % (cfg.H, compared, T * cfg.N, flagged, exhausted_layer), flush=True)
+    assert compared == T * cfg.N - flagged
+    assert flagged <= 0.02 * T * cfg.N
     return exhausted_layer
 
 
@@ -168,6 +178,31 @@ def test_chain_decisions_match_the_oracle_at_other_horizons(stream_case, H, allo
     sc = with_horizon(stream_case, H, allow_sub=allow_sub)
     g = _gpu_chain(sc)
     _compare_chain(sc, g["layers"], _oracle_chain(sc, g["layers"]))
+
+
+@pytest.fixture(scope="module")
+def stream_case_ratio1():
+    """The 32-layer stack at memory ratio 1.0 (one copy of every expert): the
+    look-ahead (eq 42-43) changes decisions here."""
+    from ._pipeline import build_stream
+    return build_stream(wl.C5_STREAM.with_(memory_ratio=1.0))
+
+
+def test_lookahead_decides_at_memory_ratio_one(stream_case_ratio1):
+    """At H = 3 and H = 1 the chains both match the oracle slot for slot, and
+    the look-ahead term moves at least one slot to another (server, expert)
+    than the myopic rule picks (eq 43 with Phi != 0)."""
+    from ._pipeline import with_horizon
+    runs = {}
+    for H in (1, 3):
+        sc = stream_case_ratio1 if H == stream_case_ratio1.cfg.H else with_horizon(stream_case_ratio1, H)
+        g = _gpu_chain(sc)
+        _compare_chain(sc, g["layers"], _oracle_chain(sc, g["layers"]))
+        runs[H] = g["layers"]
+    differ = sum(int(np.sum((a["exec_m"] != b["exec_m"]) | (a["exec_k"] != b["exec_k"])))
+                 for a, b in zip(runs[1], runs[3]))
+    print("memory ratio 1.0: %d slots decided differently at H = 3 than at H = 1" % differ, flush=True)
+    assert differ > 0
 
 
 @pytest.mark.parametrize("layer", FORWARD_LAYERS)
