@@ -374,6 +374,22 @@ int ordermoe_route_select(const ordermoe_layer* L, const void* x, int64_t T,
                           const uint8_t* loc_in, const float* qhat_in,
                           const ordermoe_route_out* out, void* ws, size_t ws_bytes, void* stream);
 
+/* ordermoe_route_select for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same kernels and results, with the workspace taken from a
+ * fixed scratch array of ORDERMOE_NOALLOC_SCRATCH_BYTES in device memory that
+ * the library holds on each GPU it runs on until the process ends.  The call
+ * allocates and frees nothing.  Batches whose
+ * ordermoe_route_workspace_size(T, k, M) exceeds the scratch return
+ * ORDERMOE_EWORKSPACE before any launch.  Every call on one GPU uses that GPU's
+ * one scratch array: calls whose device work overlaps (other streams, other
+ * threads) race and must be ordered by the caller.  The scratch is rewritten
+ * before it is read on every call, so nothing needs clearing between calls. */
+#define ORDERMOE_NOALLOC_SCRATCH_BYTES (8u << 20)
+int ordermoe_route_select_noalloc(const ordermoe_layer* L, const void* x, int64_t T,
+                                  const uint8_t* loc_in, const float* qhat_in,
+                                  const ordermoe_route_out* out, void* stream);
+
 /* ------------------------------------------------------------------------
  * Local MoE execution on one server.
  *

@@ -4,6 +4,7 @@
 
 #include <algorithm>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -120,10 +121,12 @@ extern "C" size_t ordermoe_route_workspace_size(int64_t T, int32_t k, int32_t M)
     return route_ws(T, k, M, c, nullptr);
 }
 
-extern "C" int ordermoe_route_select(const ordermoe_layer* L, const void* x, int64_t T,
-                                     const uint8_t* loc_in, const float* qhat_in,
-                                     const ordermoe_route_out* out, void* ws, size_t ws_bytes,
-                                     void* stream) {
+static int run_route(const ordermoe_layer* L, const void* x, int64_t T, const uint8_t* loc_in,
+                     const float* qhat_in, const ordermoe_route_out* out, void* ws, void* stream,
+                     const char* who);
+
+static int check_route_args(const ordermoe_layer* L, const void* x, int64_t T, const uint8_t* loc_in,
+                            const float* qhat_in, const ordermoe_route_out* out) {
     if (!L || !out) return fail(ORDERMOE_EINVAL, "route_select: null layer or output struct");
     if (L->dtype != ORDERMOE_F32 && L->dtype != ORDERMOE_BF16) return fail(ORDERMOE_EDTYPE, "route_select: dtype");
     if (L->d < 64 || L->d % 64 != 0) return fail(ORDERMOE_EINVAL, "route_select: d must be a positive multiple of 64");
@@ -144,10 +147,67 @@ extern "C" int ordermoe_route_select(const ordermoe_layer* L, const void* x, int
         return fail(ORDERMOE_EINVAL, "route_select: null pointer");
     if ((T > 0 && !aligned16(x)) || !aligned16(L->w_router))
         return fail(ORDERMOE_EINVAL, "route_select: x and w_router must be 16-byte aligned");
+    return ORDERMOE_OK;
+}
+
+extern "C" int ordermoe_route_select(const ordermoe_layer* L, const void* x, int64_t T,
+                                     const uint8_t* loc_in, const float* qhat_in,
+                                     const ordermoe_route_out* out, void* ws, size_t ws_bytes,
+                                     void* stream) {
+    const int rc = check_route_args(L, x, T, loc_in, qhat_in, out);
+    if (rc) return rc;
     const size_t need = ordermoe_route_workspace_size(T, L->k, L->M);
     if (!ws || ws_bytes < need)
         return fail(ORDERMOE_EWORKSPACE, "route_select: workspace needs " + std::to_string(need) + " bytes");
+    return run_route(L, x, T, loc_in, qhat_in, out, ws, stream, "route_select launch");
+}
 
+// scratch of ordermoe_route_select_noalloc: one copy per GPU, held for the life
+// of the process; host code addresses it only through the device address that
+// hipGetSymbolAddress returns for the current device (never by this name)
+static __device__ __align__(256) char scratch[ORDERMOE_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mu;
+static void* g_scratch_dev[kMaxDevices] = {};
+
+// the current device's copy of `scratch`, looked up once per device
+static int scratch_address(void** ptr) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail((int)e, "route_select_noalloc: hipGetDevice");
+    if (dev < 0 || dev >= kMaxDevices)
+        return fail(ORDERMOE_EINVAL, "route_select_noalloc: device id beyond " + std::to_string(kMaxDevices));
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_dev[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p) return hip_fail((int)e, "route_select_noalloc: hipGetSymbolAddress(scratch)");
+        g_scratch_dev[dev] = p;
+    }
+    *ptr = g_scratch_dev[dev];
+    return ORDERMOE_OK;
+}
+
+extern "C" int ordermoe_route_select_noalloc(const ordermoe_layer* L, const void* x, int64_t T,
+                                             const uint8_t* loc_in, const float* qhat_in,
+                                             const ordermoe_route_out* out, void* stream) {
+    const int rc = check_route_args(L, x, T, loc_in, qhat_in, out);
+    if (rc) return rc;
+    const size_t need = ordermoe_route_workspace_size(T, L->k, L->M);
+    if (need > (size_t)ORDERMOE_NOALLOC_SCRATCH_BYTES)
+        return fail(ORDERMOE_EWORKSPACE, "route_select_noalloc: this batch needs " + std::to_string(need) +
+                                            " bytes of scratch, above the fixed " +
+                                            std::to_string((size_t)ORDERMOE_NOALLOC_SCRATCH_BYTES));
+    void* ws = nullptr;
+    const int r2 = scratch_address(&ws);
+    if (r2) return r2;
+    return run_route(L, x, T, loc_in, qhat_in, out, ws, stream, "route_select_noalloc launch");
+}
+
+static int run_route(const ordermoe_layer* L, const void* x, int64_t T, const uint8_t* loc_in,
+                     const float* qhat_in, const ordermoe_route_out* out, void* ws, void* stream,
+                     const char* who) {
     RouteArgs a{};
     a.dtype = L->dtype; a.d = L->d; a.E = L->E; a.k = L->k; a.M = L->M; a.gmax = L->gmax;
     a.pin = L->pin_local_exact; a.allow_sub = L->allow_sub; a.renorm = L->renorm;
@@ -159,7 +219,7 @@ extern "C" int ordermoe_route_select(const ordermoe_layer* L, const void* x, int
     Carver c(ws);
     route_ws(T, L->k, L->M, c, &a);
     int e = launch_route_select(a, stream);
-    if (e) return hip_fail(e, "route_select launch");
+    if (e) return hip_fail(e, who);
     clear_error();
     return ORDERMOE_OK;
 }

@@ -20,6 +20,7 @@ LIB_PATH = os.path.join(_HERE, "libordermoe.so")
 OK, EINVAL, EDTYPE, ECAPACITY, EHIP, EWORKSPACE = 0, -1, -2, -3, -4, -5
 F32, BF16 = 0, 1
 MAX_SERVERS, MAX_EXPERTS, MAX_TOPK, MAX_SUBS, MAX_LOCAL = 32, 256, 8, 15, 64
+NOALLOC_SCRATCH_BYTES = 8 << 20
 MARGIN_FLAG = 1.0e-4
 CNT_LOCAL_EXACT, CNT_LOCAL_SUB, CNT_REMOTE_EXACT, CNT_REMOTE_SUB = 0, 1, 2, 3
 CNT_FLAGGED, CNT_TRANSFERS, CNT_REMOTE_SLOTS, CNT_INVALID, NUM_COUNTERS = 4, 5, 6, 7, 8
@@ -33,7 +34,7 @@ EXPORTS = ("ordermoe_last_error", "ordermoe_similarity_workspace_size", "ordermo
            "ordermoe_estimate_transitions", "ordermoe_theta_layer", "ordermoe_adapt_weights",
            "ordermoe_place_random", "ordermoe_simulate_delay", "ordermoe_lookahead_device_workspace_size",
            "ordermoe_build_lookahead_device", "ordermoe_transitions_device_workspace_size",
-           "ordermoe_estimate_transitions_device")
+           "ordermoe_estimate_transitions_device", "ordermoe_route_select_noalloc")
 TIMING_NAME = 64
 
 
@@ -118,6 +119,9 @@ def lib() -> ctypes.CDLL:
     L.ordermoe_route_select.restype = ctypes.c_int
     L.ordermoe_route_select.argtypes = [ctypes.POINTER(Layer), _P, _I64, _P, _P,
                                         ctypes.POINTER(RouteOut), _P, _SZ, _P]
+    L.ordermoe_route_select_noalloc.restype = ctypes.c_int
+    L.ordermoe_route_select_noalloc.argtypes = [ctypes.POINTER(Layer), _P, _I64, _P, _P,
+                                                ctypes.POINTER(RouteOut), _P]
     L.ordermoe_forward_workspace_size.restype = _SZ
     L.ordermoe_forward_workspace_size.argtypes = [ctypes.POINTER(Experts), _I64, _I32]
     L.ordermoe_local_moe_forward.restype = ctypes.c_int
@@ -456,6 +460,22 @@ def ordermoe_route_select(layer: Layer, x, T: int, loc_in, qhat_in, out: Dict, w
                                        loc_in.data_ptr() if T > 0 else 0,
                                        qhat_in.data_ptr() if T > 0 else 0, ctypes.byref(s),
                                        _dev(workspace), workspace.numel(), _stream(stream)))
+
+
+def ordermoe_route_select_noalloc(layer: Layer, x, T: int, loc_in, qhat_in, out: Dict, stream=None,
+                                  out_struct: Optional[RouteOut] = None):
+    """ordermoe_route_select with the library's fixed per-GPU scratch instead
+    of a caller workspace (allocates nothing)."""
+    import torch
+    if T > 0:
+        _dev(x, _torch_dtype(layer.dtype), T * layer.d)
+        _dev(loc_in, torch.uint8, T)
+        _dev(qhat_in, torch.float32, T)
+    s = out_struct if out_struct is not None else route_out_struct(out)
+    _check(lib().ordermoe_route_select_noalloc(ctypes.byref(layer), x.data_ptr() if T > 0 else 0, T,
+                                               loc_in.data_ptr() if T > 0 else 0,
+                                               qhat_in.data_ptr() if T > 0 else 0, ctypes.byref(s),
+                                               _stream(stream)))
 
 
 def make_experts(dtype: int, d: int, f: int, E: int, local_experts: Sequence[int], w_gate_up,

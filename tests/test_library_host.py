@@ -290,6 +290,27 @@ def test_forward_rejects_operands_past_31_bit_offsets():
     assert L.ordermoe_forward_workspace_size(ctypes.byref(ex), 1 << 14, 2) == 0
 
 
+def test_noalloc_route_select_rejects_batches_beyond_its_scratch():
+    """The allocation-free routing call checks the batch's workspace against its
+    fixed scratch on the host and returns ORDERMOE_EWORKSPACE before any launch."""
+    L = om.lib()
+    T, k, M = 300000, 8, 32
+    assert L.ordermoe_route_workspace_size(T, k, M) > om.NOALLOC_SCRATCH_BYTES
+    assert L.ordermoe_route_workspace_size(65536, k, M) <= om.NOALLOC_SCRATCH_BYTES
+    lay = om.Layer(dtype=om.BF16, d=512, E=64, k=k, M=M, gmax=3)
+    for n in ("w_router", "t1_k", "t1_q", "t1_n", "srvmask", "S"):
+        setattr(lay, n, 256)
+    out = om.RouteOut()
+    for n, _ in om.RouteOut._fields_:
+        setattr(out, n, 256)
+    p = ctypes.c_void_p(256)
+    rc = L.ordermoe_route_select_noalloc(ctypes.byref(lay), p, T, p, p, ctypes.byref(out), None)
+    assert rc == om.EWORKSPACE and "scratch" in om.last_error()
+    # argument checks come first, as in ordermoe_route_select
+    lay.k = 9
+    assert L.ordermoe_route_select_noalloc(ctypes.byref(lay), p, T, p, p, ctypes.byref(out), None) == om.EINVAL
+
+
 def test_weight_adaptation_oracle_pins():
     """eq 45: a step of kappa (Q_bar - T_bar) on omega_Q, projected onto [0, 1],
     with omega_T = 1 - omega_Q."""
