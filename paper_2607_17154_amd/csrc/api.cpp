@@ -108,10 +108,9 @@ static size_t route_ws(int64_t T, int32_t k, int32_t M, Carver& c, RouteArgs* a)
     const int nblk = (int)((T + tb - 1) / tb);
     int32_t* bd = c.take<int32_t>((size_t)std::max(nblk, 1) * M);
     int64_t* bc = c.take<int64_t>((size_t)std::max(nblk, 1) * 8);
-    int32_t* db = c.take<int32_t>((size_t)std::max(nblk, 1) * M);
     // small batches split the router over K slices: room for their partial logits
     float* lp = c.take<float>(route_split_buffer_floats(T));
-    if (a) { a->blk_dst = bd; a->blk_cnt = bc; a->dst_base = db; a->logit_part = lp; a->nblk = nblk; }
+    if (a) { a->blk_dst = bd; a->blk_cnt = bc; a->logit_part = lp; a->nblk = nblk; }
     return c.size();
 }
 
@@ -238,7 +237,6 @@ static size_t fwd_ws(const ordermoe_experts* W, int64_t T, int32_t k, Carver& c,
     const int64_t rs = has_sh ? T : 0;
     const size_t esz = W->dtype == ORDERMOE_BF16 ? 2 : 4;
     int32_t* br = c.take<int32_t>((size_t)std::max(nblk, 1) * std::max(G, 1));
-    int32_t* bb = c.take<int32_t>((size_t)std::max(nblk, 1) * std::max(G, 1));
     int32_t* rt = c.take<int32_t>((size_t)std::max<int64_t>(rr + rs, 1));
     float* rw = c.take<float>((size_t)std::max<int64_t>(rr + rs, 1));
     int32_t* tr = c.take<int32_t>((size_t)std::max<int64_t>(T * (k + 1), 1));
@@ -249,7 +247,7 @@ static size_t fwd_ws(const ordermoe_experts* W, int64_t T, int32_t k, Carver& c,
     int32_t* sc = c.take<int32_t>(forward_split_counters());
     float* sp = c.take<float>(forward_split_floats(W->dtype, T));
     if (a) {
-        a->blk_rows = br; a->blk_base = bb; a->row_tok = rt; a->row_w = rw; a->tok_rows = tr;
+        a->blk_rows = br; a->row_tok = rt; a->row_w = rw; a->tok_rows = tr;
         a->tile_info = ti; a->act_r = ar; a->act_s = as; a->obuf = ob; a->rmax_routed = rr;
         a->sk_cnt = sc; a->sk_part = sp;
         a->nblk = nblk;

@@ -65,7 +65,6 @@ struct RouteArgs {
     // workspace
     int32_t* blk_dst;      // [nblk][M] remote slots per destination per block
     int64_t* blk_cnt;      // [nblk][8] per-block counters
-    int32_t* dst_base;     // [nblk][M] first position of each block inside the destination segment
     float* logit_part;     // [ksplit][T][Epad] router partial logits of small batches
     int nblk;
     int S_in_lds;          // set by the launcher: stage the cost table in LDS
@@ -94,7 +93,6 @@ struct ForwardArgs {
     int32_t* row_offsets;
     // workspace
     int32_t* blk_rows;     // [nblk][G] rows per group per block (G = n_local + has_shared)
-    int32_t* blk_base;     // [nblk][G] first row of each block inside its group
     int32_t* row_tok;      // [rmax] token of each row
     float* row_w;          // [rmax] merged gate weight of each row
     int32_t* tok_rows;     // [T][k + 1] rows of each token, -1 padded

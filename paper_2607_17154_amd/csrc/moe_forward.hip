@@ -5,12 +5,13 @@
 //   rows_count_kernel    per-block row counts per group (local experts, then
 //                        the shared pseudo-expert), duplicates of one token
 //                        merged
-//   rows_scan_kernel     one block: exclusive scans over blocks, group row
-//                        offsets, tile counts of the two GEMMs
-//   rows_scatter_kernel  stable placement of every row (token order inside a
-//                        group), merged gate weight, token -> rows map
-//   rows_small_kernel    the three row kernels as one block (batches of at
-//                        most 1024 tokens)
+//   rows_scatter_kernel  each block totals the count table itself (group
+//                        offsets, its position in each group, tile counts of
+//                        the two GEMMs), then places its rows stably (token
+//                        order inside a group) with the merged gate weight
+//                        and the token -> rows map
+//   rows_small_kernel    both row kernels as one block (batches of at most
+//                        1024 tokens)
 //   ggemm_bf16<.., 0>    gate/up projection, X rows gathered through row_tok,
 //                        packed [2f][d] weights, epilogue silu(g) * u -> bf16
 //   ggemm_bf16<.., 1>    down projection of the activations, epilogue scales
@@ -58,7 +59,6 @@ struct RowsArgs {
     const uint8_t* loc_in;
     int32_t lidx[ORDERMOE_MAX_EXPERTS];   // expert -> local slot (kernel argument)
     int32_t* blk_rows;        // [nblk][G]
-    int32_t* blk_base;        // [nblk][G] first row of each block inside its group
     int32_t* row_offsets;     // [n_local + 2]
     int32_t* row_tok;
     float* row_w;
@@ -164,79 +164,82 @@ __global__ void __launch_bounds__(FT_TB) rows_count_kernel(const RowsArgs a) {
 constexpr int SCAN_THREADS = 1024;
 constexpr int SCAN_WAVES = SCAN_THREADS / 64;
 
-// One block.  Wave w scans groups w, w + 16, ... over the token blocks on its
-// own (64 blocks per step, a wave-level inclusive scan plus a carry), so the
-// groups proceed in parallel without block-wide barriers; then wave 0 lays
-// out the group offsets and the tile counts of the two GEMMs.
-__global__ void __launch_bounds__(SCAN_THREADS) rows_scan_kernel(const RowsArgs a) {
-    __shared__ int32_t s_tot[MAXG];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+// One wave: the group offsets (exclusive scan of the group totals tot[0..G),
+// local experts then the shared group) into first[], and, when `publish`, the
+// row offsets and the tile counts of the two GEMMs into device memory.
+__device__ inline void group_layout(const RowsArgs& a, const int32_t* tot, int32_t* first, int lane, bool publish) {
     const int G = a.n_local + a.has_shared;
-    for (int i = tid; i < 2 * SK_MAX_GRID; i += SCAN_THREADS) a.sk_cnt[i] = 0;
-    for (int g = wave; g < G; g += SCAN_WAVES) {
-        int32_t carry = 0;
-        for (int b0 = 0; b0 < a.nblk; b0 += 64) {
-            const int b = b0 + lane;
-            const int32_t v = b < a.nblk ? a.blk_rows[(int64_t)b * G + g] : 0;
-            int32_t inc = v;
-            for (int off = 1; off < 64; off <<= 1) {
-                const int32_t o = __shfl_up(inc, off);
-                if (lane >= off) inc += o;
-            }
-            if (b < a.nblk) a.blk_base[(int64_t)b * G + g] = carry + inc - v;   // within-group offset
-            carry += __shfl(inc, 63);
+    int32_t base = 0;
+    int64_t tiles_gu = 0, tiles_dn = 0;
+    for (int g0 = 0; g0 <= a.n_local; g0 += 64) {
+        const int g = g0 + lane;
+        const int32_t R = g < G ? tot[g] : 0;
+        int32_t inc = R;
+        for (int off = 1; off < 64; off <<= 1) {
+            const int32_t o = __shfl_up(inc, off);
+            if (lane >= off) inc += o;
         }
-        if (lane == 0) s_tot[g] = carry;
+        if (g <= a.n_local) {
+            first[g] = base + inc - R;
+            if (publish) a.row_offsets[g] = base + inc - R;
+        }
+        int64_t tg = 0, td = 0;
+        if (g < G) {
+            const bool sh = g == a.n_local;
+            tg = (int64_t)((R + a.bm_gu - 1) / a.bm_gu) * ((sh ? a.n_gu_s : a.n_gu_r) / a.bn_gu);
+            td = (int64_t)((R + a.bm_dn - 1) / a.bm_dn) * (a.n_dn / a.bn_dn);
+        }
+        for (int off = 32; off >= 1; off >>= 1) {
+            tg += __shfl_xor(tg, off);
+            td += __shfl_xor(td, off);
+        }
+        tiles_gu += tg;
+        tiles_dn += td;
+        base += __shfl(inc, 63);
     }
-    __syncthreads();
-    // group offsets (exclusive scan of the totals) and tile counts, wave 0
-    if (wave == 0) {
-        int32_t base = 0;
-        int64_t tiles_gu = 0, tiles_dn = 0;
-        for (int g0 = 0; g0 <= a.n_local; g0 += 64) {
-            const int g = g0 + lane;
-            const int32_t R = g < G ? s_tot[g] : 0;
-            int32_t inc = R;
-            for (int off = 1; off < 64; off <<= 1) {
-                const int32_t o = __shfl_up(inc, off);
-                if (lane >= off) inc += o;
-            }
-            if (g <= a.n_local) a.row_offsets[g] = base + inc - R;
-            int64_t tg = 0, td = 0;
-            if (g < G) {
-                const bool sh = g == a.n_local;
-                tg = (int64_t)((R + a.bm_gu - 1) / a.bm_gu) * ((sh ? a.n_gu_s : a.n_gu_r) / a.bn_gu);
-                td = (int64_t)((R + a.bm_dn - 1) / a.bm_dn) * (a.n_dn / a.bn_dn);
-            }
-            for (int off = 32; off >= 1; off >>= 1) {
-                tg += __shfl_xor(tg, off);
-                td += __shfl_xor(td, off);
-            }
-            tiles_gu += tg;
-            tiles_dn += td;
-            base += __shfl(inc, 63);
-        }
-        if (lane == 0) {
-            a.row_offsets[a.n_local + 1] = base;
-            a.tile_info[0] = (int32_t)tiles_gu;
-            a.tile_info[1] = (int32_t)tiles_dn;
-            a.tile_info[2] = base;
-            a.tile_info[3] = 0;
-        }
+    if (publish && lane == 0) {
+        a.row_offsets[a.n_local + 1] = base;
+        a.tile_info[0] = (int32_t)tiles_gu;
+        a.tile_info[1] = (int32_t)tiles_dn;
+        a.tile_info[2] = base;
+        a.tile_info[3] = 0;
     }
 }
 
+// Placement of every row, one block per block of rows_count_kernel.  Each
+// block first totals the count table on its own (groups x blocks integers):
+// its first row inside each group (the counts of the blocks before it) and the
+// group totals, whose exclusive scan gives the group offsets; block 0 also
+// publishes the row offsets and tile counts and clears the split-tile arrival
+// counters of the GEMMs.  Then every row goes to its group offset + block
+// position + its rank in token order.
 __global__ void __launch_bounds__(FT_TB) rows_scatter_kernel(const RowsArgs a) {
     __shared__ int32_t s_lidx[ORDERMOE_MAX_EXPERTS];
     __shared__ int32_t s_wcnt[FT_TB / 64][MAXG];
     __shared__ unsigned long long s_msk[FT_TB / 64][MAXG];
+    __shared__ int32_t s_lo[MAXG], s_tot[MAXG];
     __shared__ int32_t s_first[MAXG];        // first row of this block in each group
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int G = a.n_local + a.has_shared;
+    const int b = (int)blockIdx.x;
     for (int i = tid; i < a.E; i += FT_TB) s_lidx[i] = a.lidx[i];
-    for (int g = tid; g < G; g += FT_TB) s_first[g] = a.row_offsets[g] + a.blk_base[(int64_t)blockIdx.x * G + g];
+    if (b == 0)
+        for (int i = tid; i < 2 * SK_MAX_GRID; i += FT_TB) a.sk_cnt[i] = 0;
+    for (int g = wave; g < G; g += FT_TB / 64) {
+        int32_t lo = 0, tot = 0;
+        for (int i = lane; i < a.nblk; i += 64) {
+            const int32_t v = a.blk_rows[(int64_t)i * G + g];
+            tot += v;
+            lo += i < b ? v : 0;
+        }
+        for (int off = 32; off >= 1; off >>= 1) {
+            lo += __shfl_xor(lo, off);
+            tot += __shfl_xor(tot, off);
+        }
+        if (lane == 0) { s_lo[g] = lo; s_tot[g] = tot; }
+    }
     __syncthreads();
-    const int64_t t = (int64_t)blockIdx.x * FT_TB + tid;
+    const int64_t t = (int64_t)b * FT_TB + tid;
     int grp[MAXR], rank[MAXR];
     float ws[MAXR];
     int n = 0;
@@ -247,6 +250,10 @@ __global__ void __launch_bounds__(FT_TB) rows_scatter_kernel(const RowsArgs a) {
         for (int q = 0; q < MAXR; ++q) { grp[q] = -1; ws[q] = 0.f; }
     }
     wave_group_ranks(s_msk[wave], G, lane, grp, n, rank, s_wcnt[wave]);
+    if (wave == 0) {
+        group_layout(a, s_tot, s_first, lane, b == 0);
+        for (int g = lane; g < G; g += 64) s_first[g] += s_lo[g];
+    }
     __syncthreads();
     if (t < a.T) {
         const int stride = a.k + 1;
@@ -266,15 +273,14 @@ __global__ void __launch_bounds__(FT_TB) rows_scatter_kernel(const RowsArgs a) {
     }
 }
 
-// Batches of at most SCAN_THREADS tokens (decode): the three row kernels as one
+// Batches of at most SCAN_THREADS tokens (decode): the row kernels as one
 // block, one token per thread -- group ranks by wave lane masks, group totals,
-// row offsets and tile counts (as rows_scan_kernel), then the placement (as
-// rows_scatter_kernel).
+// row offsets and tile counts, then the placement (as rows_scatter_kernel).
 __global__ void __launch_bounds__(SCAN_THREADS) rows_small_kernel(const RowsArgs a) {
     __shared__ int32_t s_lidx[ORDERMOE_MAX_EXPERTS];
     __shared__ int32_t s_wcnt[SCAN_WAVES][MAXG];
     __shared__ unsigned long long s_msk[SCAN_WAVES][MAXG];
-    __shared__ int32_t s_first[MAXG];
+    __shared__ int32_t s_first[MAXG], s_tot[MAXG];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int G = a.n_local + a.has_shared;
     for (int i = tid; i < a.E; i += SCAN_THREADS) s_lidx[i] = a.lidx[i];
@@ -293,40 +299,12 @@ __global__ void __launch_bounds__(SCAN_THREADS) rows_small_kernel(const RowsArgs
     wave_group_ranks(s_msk[wave], G, lane, grp, n, rank, s_wcnt[wave]);
     __syncthreads();
     if (wave == 0) {
-        int32_t base = 0;
-        int64_t tiles_gu = 0, tiles_dn = 0;
-        for (int g0 = 0; g0 <= a.n_local; g0 += 64) {
-            const int g = g0 + lane;
+        for (int g = lane; g < G; g += 64) {
             int32_t R = 0;
-            if (g < G)
-                for (int w = 0; w < SCAN_WAVES; ++w) R += s_wcnt[w][g];
-            int32_t inc = R;
-            for (int off = 1; off < 64; off <<= 1) {
-                const int32_t o = __shfl_up(inc, off);
-                if (lane >= off) inc += o;
-            }
-            if (g <= a.n_local) { a.row_offsets[g] = base + inc - R; s_first[g] = base + inc - R; }
-            int64_t tg = 0, td = 0;
-            if (g < G) {
-                const bool sh = g == a.n_local;
-                tg = (int64_t)((R + a.bm_gu - 1) / a.bm_gu) * ((sh ? a.n_gu_s : a.n_gu_r) / a.bn_gu);
-                td = (int64_t)((R + a.bm_dn - 1) / a.bm_dn) * (a.n_dn / a.bn_dn);
-            }
-            for (int off = 32; off >= 1; off >>= 1) {
-                tg += __shfl_xor(tg, off);
-                td += __shfl_xor(td, off);
-            }
-            tiles_gu += tg;
-            tiles_dn += td;
-            base += __shfl(inc, 63);
+            for (int w = 0; w < SCAN_WAVES; ++w) R += s_wcnt[w][g];
+            s_tot[g] = R;
         }
-        if (lane == 0) {
-            a.row_offsets[a.n_local + 1] = base;
-            a.tile_info[0] = (int32_t)tiles_gu;
-            a.tile_info[1] = (int32_t)tiles_dn;
-            a.tile_info[2] = base;
-            a.tile_info[3] = 0;
-        }
+        group_layout(a, s_tot, s_first, lane, true);
     }
     __syncthreads();
     if (t < a.T) {
@@ -1065,7 +1043,7 @@ int launch_local_forward(const ForwardArgs& f, void* stream) {
     r.T = f.T; r.k = f.k; r.E = f.E; r.n_local = f.n_local; r.has_shared = has_sh; r.server = f.server;
     r.w = f.w; r.exec_k = f.exec_k; r.exec_m = f.exec_m; r.loc_in = f.loc_in;
     for (int i = 0; i < ORDERMOE_MAX_EXPERTS; ++i) r.lidx[i] = f.lidx[i];
-    r.blk_rows = f.blk_rows; r.blk_base = f.blk_base; r.row_offsets = f.row_offsets;
+    r.blk_rows = f.blk_rows; r.row_offsets = f.row_offsets;
     r.row_tok = f.row_tok; r.row_w = f.row_w; r.tok_rows = f.tok_rows; r.tile_info = f.tile_info;
     r.sk_cnt = f.sk_cnt; r.nblk = f.nblk;
     r.bm_gu = bm_gu; r.bn_gu = bn_gu; r.bm_dn = bm_dn; r.bn_dn = bn_dn;
@@ -1083,11 +1061,6 @@ int launch_local_forward(const ForwardArgs& f, void* stream) {
         {
             KernelTimer kt_("rows_count", st);
             hipLaunchKernelGGL(rows_count_kernel, dim3(f.nblk), dim3(FT_TB), 0, st, r);
-        }
-        if ((e = hipGetLastError()) != hipSuccess) return (int)e;
-        {
-            KernelTimer kt_("rows_scan", st);
-            hipLaunchKernelGGL(rows_scan_kernel, dim3(1), dim3(SCAN_THREADS), 0, st, r);
         }
         if ((e = hipGetLastError()) != hipSuccess) return (int)e;
         {

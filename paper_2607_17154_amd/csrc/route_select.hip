@@ -681,48 +681,43 @@ route_select_kernel(const RouteArgs a) {
     if (tid < M) a.blk_dst[(int64_t)blockIdx.x * M + tid] = s_cnt[8 + tid];
 }
 
-constexpr int SCAN_THREADS = 1024;
-constexpr int SCAN_WAVES = SCAN_THREADS / 64;
-
-// One block, every wave on its own (no block-wide barriers): waves 0-7 total
-// the eight counters over the token blocks; wave w (and w + 16) scans the
-// per-block counts of destination w over the blocks, giving each block's
-// first position inside that destination's segment and the destination's
-// total.  The segments follow in server order (dispatch_scatter_kernel adds
-// the segment start).
-__global__ void __launch_bounds__(SCAN_THREADS)
-dispatch_scan_kernel(const int32_t* blk_dst, const int64_t* blk_cnt, int nblk, int M,
-                     int32_t* dst_base, int32_t* dst_count, int64_t* counters) {
+// The dispatch list, one block per routing block.  Each block first totals
+// the routing blocks' per-destination counts on its own (a few thousand
+// integers at most): its first position inside each destination's segment
+// (the counts of the blocks before it) and every destination's total, from
+// which the segment starts follow in server order; block 0 also writes the
+// per-destination totals and the eight counters.  Then each remote slot of the
+// block goes to segment start + block position + its rank among the block's
+// earlier slots to the same destination (slot order), so the list is sorted by
+// (destination, token, slot).
+__global__ void __launch_bounds__(RT_THREADS)
+dispatch_kernel(const int32_t* blk_dst, const int64_t* blk_cnt, int nblk, const uint8_t* exec_m,
+                const uint8_t* loc_in, int64_t T, int k, int M, int tb, int32_t* dst_count, int64_t* counters,
+                int32_t* dispatch) {
+    __shared__ int8_t s_dst[RT_TB2 * ORDERMOE_MAX_TOPK];
+    __shared__ int32_t s_base[ORDERMOE_MAX_SERVERS], s_tot[ORDERMOE_MAX_SERVERS], s_start[ORDERMOE_MAX_SERVERS];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    if (wave < 8) {
+    const int b = (int)blockIdx.x;
+    for (int m = wave; m < M; m += RT_WAVES) {
+        int32_t lo = 0, tot = 0;
+        for (int i = lane; i < nblk; i += 64) {
+            const int32_t v = blk_dst[(int64_t)i * M + m];
+            tot += v;
+            lo += i < b ? v : 0;
+        }
+        for (int off = 32; off >= 1; off >>= 1) {
+            lo += __shfl_xor(lo, off);
+            tot += __shfl_xor(tot, off);
+        }
+        if (lane == 0) { s_base[m] = lo; s_tot[m] = tot; }
+    }
+    if (b == 0 && wave < 8) {
         int64_t v = 0;
-        for (int b = lane; b < nblk; b += 64) v += blk_cnt[(int64_t)b * 8 + wave];
+        for (int i = lane; i < nblk; i += 64) v += blk_cnt[(int64_t)i * 8 + wave];
         for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
         if (lane == 0) counters[wave] = v;
     }
-    for (int m = wave; m < M; m += SCAN_WAVES) {
-        int32_t carry = 0;
-        for (int b0 = 0; b0 < nblk; b0 += 64) {
-            const int b = b0 + lane;
-            const int32_t v = b < nblk ? blk_dst[(int64_t)b * M + m] : 0;
-            int32_t inc = v;
-            for (int off = 1; off < 64; off <<= 1) {
-                const int32_t o = __shfl_up(inc, off);
-                if (lane >= off) inc += o;
-            }
-            if (b < nblk) dst_base[(int64_t)b * M + m] = carry + inc - v;
-            carry += __shfl(inc, 63);
-        }
-        if (lane == 0) dst_count[m] = carry;
-    }
-}
-
-__global__ void __launch_bounds__(RT_THREADS)
-dispatch_scatter_kernel(const uint8_t* exec_m, const uint8_t* loc_in, int64_t T, int k, int M, int tb,
-                        const int32_t* dst_base, const int32_t* dst_count, int32_t* dispatch) {
-    __shared__ int8_t s_dst[RT_TB2 * ORDERMOE_MAX_TOPK];
-    const int tid = threadIdx.x;
-    const int64_t t0 = (int64_t)blockIdx.x * tb;
+    const int64_t t0 = (int64_t)b * tb;
     const int n = tb * k;
     if (tid < n) {
         const int64_t t = t0 + tid / k;
@@ -735,14 +730,17 @@ dispatch_scatter_kernel(const uint8_t* exec_m, const uint8_t* loc_in, int64_t T,
         s_dst[tid] = (int8_t)dst;
     }
     __syncthreads();
+    if (tid == 0) {
+        int32_t acc = 0;
+        for (int m = 0; m < M; ++m) { s_start[m] = acc; acc += s_tot[m]; }
+    }
+    if (b == 0 && tid < M) dst_count[tid] = s_tot[tid];
+    __syncthreads();
     if (tid < n && s_dst[tid] >= 0) {
         const int dst = s_dst[tid];
         int rank = 0;
         for (int i = 0; i < tid; ++i) rank += (s_dst[i] == dst);
-        int32_t start = 0;                        // the destination's segment
-        for (int m = 0; m < dst; ++m) start += dst_count[m];
-        const int32_t pos = start + dst_base[(int64_t)blockIdx.x * M + dst] + rank;
-        dispatch[pos] = (int32_t)((t0 + tid / k) * k + tid % k);
+        dispatch[s_start[dst] + s_base[dst] + rank] = (int32_t)((t0 + tid / k) * k + tid % k);
     }
 }
 
@@ -886,7 +884,6 @@ int launch_route_select(const RouteArgs& a, void* stream) {
         }
         if (e) return e;
     }
-    hipError_t e;
     if (b.T * b.k <= DS_THREADS) {
         KernelTimer kt_("dispatch_small", st);
         hipLaunchKernelGGL(dispatch_small_kernel, dim3(1), dim3(DS_THREADS), 0, st, b.blk_cnt, b.nblk,
@@ -894,24 +891,14 @@ int launch_route_select(const RouteArgs& a, void* stream) {
                            b.out.dispatch);
         return (int)hipGetLastError();
     }
+    // here T k > DS_THREADS, so there is at least one routing block
     {
-        KernelTimer kt_("dispatch_scan", st);
-        hipLaunchKernelGGL(dispatch_scan_kernel, dim3(1), dim3(SCAN_THREADS), 0, st, b.blk_dst,
-                           b.blk_cnt, b.nblk, b.M, b.dst_base, b.out.dst_count, b.out.counters);
+        KernelTimer kt_("dispatch", st);
+        hipLaunchKernelGGL(dispatch_kernel, dim3(b.nblk), dim3(RT_THREADS), 0, st, b.blk_dst, b.blk_cnt, b.nblk,
+                           b.out.exec_m, b.loc_in, b.T, b.k, b.M, tb, b.out.dst_count, b.out.counters,
+                           b.out.dispatch);
     }
-    e = hipGetLastError();
-    if (e != hipSuccess) return (int)e;
-    if (b.nblk > 0) {
-        {
-            KernelTimer kt_("dispatch_scatter", st);
-            hipLaunchKernelGGL(dispatch_scatter_kernel, dim3(b.nblk), dim3(RT_THREADS), 0, st,
-                               b.out.exec_m, b.loc_in, b.T, b.k, b.M, tb, b.dst_base, b.out.dst_count,
-                               b.out.dispatch);
-        }
-        e = hipGetLastError();
-        if (e != hipSuccess) return (int)e;
-    }
-    return 0;
+    return (int)hipGetLastError();
 }
 
 }  // namespace ordermoe

@@ -294,7 +294,7 @@ def test_noalloc_route_select_rejects_batches_beyond_its_scratch():
     """The allocation-free routing call checks the batch's workspace against its
     fixed scratch on the host and returns ORDERMOE_EWORKSPACE before any launch."""
     L = om.lib()
-    T, k, M = 300000, 8, 32
+    T, k, M = 400000, 8, 32
     assert L.ordermoe_route_workspace_size(T, k, M) > om.NOALLOC_SCRATCH_BYTES
     assert L.ordermoe_route_workspace_size(65536, k, M) <= om.NOALLOC_SCRATCH_BYTES
     lay = om.Layer(dtype=om.BF16, d=512, E=64, k=k, M=M, gmax=3)
