@@ -871,6 +871,9 @@ def main():
                     help="run one leg alone (for profiling): the layer step without the other "
                          "legs, or only the similarity build / decode stream (prints that leg's "
                          "JSON object)")
+    ap.add_argument("--config", choices=("C2", "C3", "C4"), default="C2",
+                    help="with --only layer: the layer to step (C2 Mixtral-shaped, the headline; C3 "
+                         "Qwen-MoE-shaped; C4 DeepSeek-MoE-shaped), for profiling")
     ap.add_argument("--out", default=os.path.join(ROOT, "gpurun_out", "bench_full.json"),
                     help="file that receives every leg's results (stdout gets one compact line)")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -893,6 +896,11 @@ def main():
         from paper_2607_17154_amd import build as _b
         _b.build()
     cfg = wl.C2
+    if args.config != "C2":
+        if args.only != "layer":
+            print("--config applies to --only layer", file=sys.stderr)
+            sys.exit(2)
+        cfg = getattr(wl, args.config)
     torch.cuda.set_device(0)
     if args.only == "simbuild":
         print(json.dumps(_simbuild(torch, om)))
@@ -959,18 +967,20 @@ def main():
     # the gate/up GEMM is one launch per step: whole rounds of 256 x 256 tiles,
     # then the remaining tiles split along K over all workgroups
     gu_avg_s = kt["gemm_gate_up"][0] / kt["gemm_gate_up"][1] / 1e3
-    gu_flops = 2.0 * R * cfg.d * (2 * cfg.f)          # gate and up projections of R rows
+    # gate and up projections: 2 d 2f per routed row, 2 d 2 n_shared f per row of the shared group
+    r_routed = int(rows[len(st["local"])])
+    gu_flops = 2.0 * cfg.d * 2 * cfg.f * (r_routed + max(cfg.n_shared, 1) * (R - r_routed))
     achieved = gu_flops / gu_avg_s / 1e12
     ms_step = ms / args.steps
     metric = "MoE-layer tokens/s on 1 MI355X (route+substitute+grouped FFN); % MFMA peak"
     roofline = {"bound": "mfma", "kernel": "gemm_gate_up", "achieved": achieved,
                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
-                "traffic": _measured_traffic(), "flop_per_launch": gu_flops,
+                "traffic": _measured_traffic() if cfg is wl.C2 else None, "flop_per_launch": gu_flops,
                 "avg_launch_us": gu_avg_s * 1e6}
-    config = {"workload": cfg.name,
-              "why": "the Mixtral-8x7B-shaped layer: the paper's headline model (its latency, "
-                     "traffic and throughput results are on Mixtral-8x7B); the DeepSeek-shaped "
-                     "layer carries more FLOPs but is not a model the paper evaluates",
+    why = ("the Mixtral-8x7B-shaped layer: the paper's headline model (its latency, traffic and "
+           "throughput results are on Mixtral-8x7B); the DeepSeek-shaped layer carries more FLOPs "
+           "but is not a model the paper evaluates") if cfg is wl.C2 else "a profiling run of another layer"
+    config = {"workload": cfg.name, "why": why,
               "tokens": cfg.T, "hidden": cfg.d, "experts": cfg.E, "ffn": cfg.f, "top_k": cfg.k,
               "servers": cfg.M, "server": cfg.m0, "local_experts": st["local"], "local_rows": R,
               "classes_LE_LS_RE_RS": [int(v) for v in counters[:4]],
@@ -992,7 +1002,7 @@ def main():
         "roofline": roofline,
         "kernels_avg_us": {k: v[0] / v[1] * 1e3 for k, v in sorted(kt.items())},
         "ms_per_step_with_kernel_events": ms_events / args.steps,
-        "mfma_frac_ffn": (2.0 * R * cfg.d * 3 * cfg.f) / (ms_step / 1e3) / 1e12 / PEAK_BF16_TFLOPS,
+        "mfma_frac_ffn": (1.5 * gu_flops) / (ms_step / 1e3) / 1e12 / PEAK_BF16_TFLOPS,
     }
     if not args.no_simbuild:
         print("bench: similarity build", file=sys.stderr, flush=True)
