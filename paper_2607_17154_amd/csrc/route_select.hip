@@ -17,14 +17,14 @@
 //     64-bit key (J, position, remote, server); a min-reduce over the row gives
 //     (m*, k*); the budget is updated as eq (44);
 //   * per-block counters and per-destination remote-slot counts.
-// Kernel 2 (dispatch_scan_kernel), one block: exclusive scans of the
-//   per-block destination counts (one wave per destination), totals of the
-//   counters.
-// Kernel 3 (dispatch_scatter_kernel), one block per TB tokens: stable
-//   placement of the block's remote slots into the (destination, token, slot)
-//   ordered dispatch list.
-// Batches of at most 1024 slots run kernels 2 and 3 as one single-block
-// kernel (dispatch_small_kernel).
+// Kernel 2 (dispatch_kernel), one block per TB tokens: each block totals the
+//   per-block destination counts of the blocks before it (the exclusive scan,
+//   redone per block so that no separate scan kernel is needed), then places
+//   its own remote slots, stably, into the (destination, token, slot) ordered
+//   dispatch list; block 0 also writes the counter totals and the
+//   per-destination counts.
+// Batches of at most 1024 slots run kernel 2 as one single-block kernel
+// (dispatch_small_kernel).
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
