@@ -6,7 +6,13 @@ the local grouped SwiGLU FFN with the weighted combine
 (ordermoe_local_moe_forward).  Workload: the Mixtral-8x7B-shaped layer --
 4096 tokens of hidden 4096, 8 experts of FFN 14336, top-2, 4 simulated
 servers holding 2 experts each -- bf16, synthetic seeded inputs, inputs
-resident in HBM before the timed region.
+resident in HBM before the timed region.  The timed steps run as a serving
+loop runs consecutive batches: step i on HIP stream i mod S (--streams, 2 by
+default) with its own outputs and workspaces, so two batches are in flight and
+one batch's small kernels and GEMM tiles fill the CUs that the other's GEMM
+tails leave idle; the line also reports the one-stream step time (one batch
+at a time, the step's latency), and the run fails if any stream's outputs
+differ from the one-stream outputs.
 
 Prints one compact JSON line (rank 0).  Besides tokens/s it reports the
 roofline of the dominant kernel (the grouped gate/up GEMM) from its average
@@ -155,12 +161,82 @@ def _setup(cfg, torch, om):
     return st
 
 
-def _step(cfg, st, om):
+def _step(cfg, st, om, stream=None):
     o = st["out"]
     om.ordermoe_route_select(st["layer"], st["x"], cfg.T, st["loc"], st["qhat"], o, st["ws_r"],
-                             out_struct=st["out_struct"])
+                             out_struct=st["out_struct"], stream=stream)
     om.ordermoe_local_moe_forward(st["experts"], st["x"], cfg.T, cfg.k, o["w"], o["exec_k"],
-                                  o["exec_m"], st["loc"], cfg.m0, st["y"], st["ro"], st["ws_f"])
+                                  o["exec_m"], st["loc"], cfg.m0, st["y"], st["ro"], st["ws_f"],
+                                  stream=stream)
+
+
+def _batch_sets(cfg, st, torch, om, n):
+    """n independent sets of per-batch buffers (route outputs, workspaces,
+    layer output) over the same weights and tables; set 0 is st itself."""
+    sets = [st]
+    for _ in range(n - 1):
+        s = dict(st)
+        s["out"] = om.alloc_route_out(cfg.T, cfg.k, cfg.M, "cuda")
+        s["out_struct"] = om.route_out_struct(s["out"])
+        for key in ("ws_r", "ws_f", "y", "ro"):
+            s[key] = torch.empty_like(st[key])
+        sets.append(s)
+    return sets
+
+
+def _timed_steps(cfg, sets, streams, steps, torch, om):
+    """Runs `steps` layer steps, step i on stream i mod S with buffer set
+    i mod S, so that S consecutive batches are in flight (each batch's kernels
+    stay in order on its stream; batches share no buffer).  Returns the
+    milliseconds from a start event on the current stream, which every stream
+    waits for, to an end event after the current stream has waited for all of
+    them."""
+    cur = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(cur)
+    for s in streams:
+        s.wait_event(e0)
+    for i in range(steps):
+        j = i % len(streams)
+        _step(cfg, sets[j], om, stream=streams[j])
+    for s in streams:
+        ev = torch.cuda.Event()
+        ev.record(s)
+        cur.wait_event(ev)
+    e1.record(cur)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1)
+
+
+_STREAMS = []
+
+
+def _streams(torch, n):
+    """The same n streams for every leg: HIP spreads streams over a few
+    hardware queues in creation order, and two streams that land on one queue
+    run one after the other, so the process creates its streams once."""
+    while len(_STREAMS) < n:
+        _STREAMS.append(torch.cuda.Stream())
+    return _STREAMS[:n]
+
+
+def _pipelined(cfg, st, torch, om, n_streams, steps, warmup):
+    """Step time with n_streams batches in flight, and the check that every
+    set's outputs equal the single-stream outputs bit for bit."""
+    names = ("exec_k", "exec_m", "w", "counters")
+    ref = dict(y=st["y"].clone(), ro=st["ro"].clone(), **{n: st["out"][n].clone() for n in names})
+    sets = _batch_sets(cfg, st, torch, om, n_streams)
+    streams = _streams(torch, n_streams)
+    # two untimed passes: the first concurrent use of new streams costs several
+    # milliseconds once (queue set-up), which would otherwise land in the timed steps
+    for _ in range(2):
+        _timed_steps(cfg, sets, streams, max(warmup, 2 * n_streams), torch, om)
+    ms = _timed_steps(cfg, sets, streams, steps, torch, om)
+    equal = all(torch.equal(s["y"], ref["y"]) and torch.equal(s["ro"], ref["ro"]) and
+                all(torch.equal(s["out"][n], ref[n]) for n in names) for s in sets)
+    del sets[1:]
+    return ms, equal
 
 
 def _cpu_baseline(cfg, st, target_s: float):
@@ -263,7 +339,7 @@ def _simbuild(torch, om, reps: int = 5):
             "hbm_frac": nbytes / us / 1e3 / PEAK_HBM_GBS}
 
 
-def _other_layers(torch, om, steps: int = 10, warmup: int = 3):
+def _other_layers(torch, om, steps: int = 30, warmup: int = 5, n_streams: int = 2):
     """The Qwen-MoE-shaped (8192 tokens, 60 experts + 4 shared, top-4) and
     DeepSeek-MoE-shaped (16384 tokens, 64 experts + 2 shared, top-6) layers of
     server 0: step time, the FFN GEMMs' MFMA rates and routing's HBM rate."""
@@ -274,13 +350,13 @@ def _other_layers(torch, om, steps: int = 10, warmup: int = 3):
         for _ in range(warmup):
             _step(cfg, st, om)
         torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(steps):
-            _step(cfg, st, om)
-        e1.record()
-        torch.cuda.synchronize()
-        ms = e0.elapsed_time(e1) / steps
+        ms_one = _timed_steps(cfg, [st], [torch.cuda.current_stream()], steps, torch, om) / steps
+        ms, equal = ms_one * steps, True
+        if n_streams > 1:
+            ms, equal = _pipelined(cfg, st, torch, om, n_streams, steps, warmup)
+            if not equal:
+                raise RuntimeError("%s: outputs differ between streams" % key)
+        ms /= steps
         om.ordermoe_timing_read(reset=True)
         om.ordermoe_timing_enable(True)
         for _ in range(steps):
@@ -298,7 +374,8 @@ def _other_layers(torch, om, steps: int = 10, warmup: int = 3):
         gu_us = sum(v for n, v in avg.items() if n.startswith("gemm_gate_up"))
         rt_bytes = cfg.T * cfg.d * 2 + cfg.E * cfg.d * 2 + cfg.T * cfg.k * 14 + cfg.T * 11
         rt_us = avg.get("route_select", float("nan"))
-        res[key] = {"workload": cfg.name, "ms_per_step": ms, "tokens_per_s": cfg.T / (ms / 1e3),
+        res[key] = {"workload": cfg.name, "streams": n_streams, "ms_per_step": ms,
+                    "tokens_per_s": cfg.T / (ms / 1e3), "ms_per_step_one_stream": ms_one,
                     "local_rows_routed": r_routed, "local_rows_shared": r_shared,
                     "gemm_gate_up_TFLOPs": fl_gu / gu_us / 1e6,
                     "gemm_gate_up_frac": fl_gu / gu_us / 1e6 / PEAK_BF16_TFLOPS,
@@ -846,8 +923,10 @@ def _decode_stream(torch, om, steps: int = 10, warmup: int = 2):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--streams", type=int, default=2,
+                    help="consecutive batches in flight, one HIP stream each (1: one batch at a time)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-simbuild", action="store_true",
@@ -879,6 +958,8 @@ def main():
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a 1 GiB device copy (to scale rocprofv3 byte counters)")
     args = ap.parse_args()
+    if args.streams < 1:
+        ap.error("--streams must be at least 1")
     if args.gpus != 1:
         print("bench.py measures one GPU: the layer runs one simulated server's experts on one "
               "MI355X; other servers are placement masks, so --gpus %d is not supported"
@@ -932,16 +1013,21 @@ def main():
     for _ in range(args.warmup):
         _step(cfg, st, om)
     torch.cuda.synchronize()
-    # the timed steps, as a caller runs them (no per-kernel events)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    e0.record()
-    for _ in range(args.steps):
-        _step(cfg, st, om)
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1)
-    print("bench: %d steps in %.3f ms" % (args.steps, ms), file=sys.stderr, flush=True)
+    # one batch at a time on one stream (no per-kernel events): the latency of a step
+    ms_one = _timed_steps(cfg, [st], [torch.cuda.current_stream()], args.steps, torch, om)
+    print("bench: %d steps on one stream in %.3f ms" % (args.steps, ms_one), file=sys.stderr, flush=True)
+    # the timed steps, as a serving loop runs them: consecutive batches
+    # alternate over --streams streams, so one batch's routing and row kernels
+    # and the next batch's GEMM fill the CUs that the other batch's GEMM tails
+    # leave idle
+    ms, streams_equal = ms_one, True
+    if args.streams > 1:
+        ms, streams_equal = _pipelined(cfg, st, torch, om, args.streams, args.steps, args.warmup)
+        if not streams_equal:
+            print("bench: outputs differ between streams", file=sys.stderr, flush=True)
+            sys.exit(1)
+    print("bench: %d steps over %d stream(s) in %.3f ms" % (args.steps, args.streams, ms), file=sys.stderr,
+          flush=True)
     # the same number of steps again with the library's HIP events around every
     # kernel launch (on the launch stream), for the per-kernel durations; the
     # events themselves add time between the kernels, so this pass is not the
@@ -980,7 +1066,7 @@ def main():
     why = ("the Mixtral-8x7B-shaped layer: the paper's headline model (its latency, traffic and "
            "throughput results are on Mixtral-8x7B); the DeepSeek-shaped layer carries more FLOPs "
            "but is not a model the paper evaluates") if cfg is wl.C2 else "a profiling run of another layer"
-    config = {"workload": cfg.name, "why": why,
+    config = {"workload": cfg.name, "why": why, "streams": args.streams,
               "tokens": cfg.T, "hidden": cfg.d, "experts": cfg.E, "ffn": cfg.f, "top_k": cfg.k,
               "servers": cfg.M, "server": cfg.m0, "local_experts": st["local"], "local_rows": R,
               "classes_LE_LS_RE_RS": [int(v) for v in counters[:4]],
@@ -1001,6 +1087,7 @@ def main():
         "config": config,
         "roofline": roofline,
         "kernels_avg_us": {k: v[0] / v[1] * 1e3 for k, v in sorted(kt.items())},
+        "ms_per_step_one_stream": ms_one / args.steps,
         "ms_per_step_with_kernel_events": ms_events / args.steps,
         "mfma_frac_ffn": (1.5 * gu_flops) / (ms_step / 1e3) / 1e12 / PEAK_BF16_TFLOPS,
     }
@@ -1009,7 +1096,7 @@ def main():
         res["similarity_build"] = _simbuild(torch, om)
     if not args.no_other_layers:
         print("bench: C3 and C4 layers", file=sys.stderr, flush=True)
-        res["other_layers"] = _other_layers(torch, om)
+        res["other_layers"] = _other_layers(torch, om, n_streams=args.streams)
     if not args.no_sweep:
         print("bench: quality-budget sweep", file=sys.stderr, flush=True)
         res["quality_sweep"] = _quality_sweep(torch, om)
@@ -1053,8 +1140,9 @@ def _compact(res: dict, out_path: str) -> dict:
     line = {k: res[k] for k in ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step",
                                 "higher_is_better", "scaling", "vs_baseline", "dtype", "data")}
     cfgd = res["config"]
-    line["config"] = {k: cfgd[k] for k in ("workload", "why", "local_rows", "classes_LE_LS_RE_RS",
+    line["config"] = {k: cfgd[k] for k in ("workload", "why", "streams", "local_rows", "classes_LE_LS_RE_RS",
                                            "flagged_tokens")}
+    line["ms_per_step_one_stream"] = round(res["ms_per_step_one_stream"], 4)
     rf = res["roofline"]
     line["roofline"] = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in rf.items()}
     ka = res["kernels_avg_us"]
@@ -1067,6 +1155,7 @@ def _compact(res: dict, out_path: str) -> dict:
     other = {}
     for key, v in res.get("other_layers", {}).items():
         other[key] = {"ms_per_step": round(v["ms_per_step"], 4), "tokens_per_s": round(v["tokens_per_s"]),
+                      "ms_per_step_one_stream": round(v["ms_per_step_one_stream"], 4),
                       "gate_up_frac": round(v["gemm_gate_up_frac"], 3),
                       "down_frac": round(v["gemm_down_frac"], 3),
                       "route_hbm_frac": round(v["route_hbm_frac"], 3)}

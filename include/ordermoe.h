@@ -32,7 +32,11 @@
  *   - Device work is queued on the caller's stream (a hipStream_t passed as
  *     void*; NULL is the default stream).  ordermoe_route_select and
  *     ordermoe_local_moe_forward never wait for the device; their counters
- *     and row counts are written to device memory.
+ *     and row counts are written to device memory.  The library keeps no
+ *     device state between calls (ordermoe_route_select_noalloc aside), so
+ *     calls on different streams may run at the same time when no output or
+ *     workspace of one is written or read by another: weights, tables and
+ *     inputs are only read and may be shared.
  *   - Storage types: ORDERMOE_F32 (IEEE binary32) or ORDERMOE_BF16 (bfloat16).
  *     Matrices are row-major; weight matrices use the [out][in] layout of
  *     torch.nn.Linear.
