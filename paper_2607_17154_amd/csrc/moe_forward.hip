@@ -562,7 +562,8 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
         };
         // Each K tile of 64 is four MFMA sub-steps of 16.  The next K tile's
         // loads are issued into the idle buffer during the first two sub-steps
-        // (B, then A), a whole K tile ahead of their use; every sub-step also
+        // (A, then B: the gathered token rows first, 2-3% faster than the
+        // other order), a whole K tile ahead of their use; every sub-step also
         // reads the fragments of the next one.  A K tile ends with the wait
         // for this wave's loads and the barrier for everyone's.  The two
         // buffers are separate LDS arrays and the loop is unrolled by two, so
@@ -572,15 +573,15 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
         constexpr int NM = FM * FN, NR = FM + FN;
         constexpr int VMEM_READ = 0x020;
         auto ktile = [&](__bf16* ca, __bf16* cb, __bf16* na, __bf16* nb, int kn) {
-            dmaB(nb, kn);
+            dmaA(na, kn);
             fload(ca, cb, 1, 1);
             mfmas(0);
-            sched_interleave<0, NM, NR, BV, VMEM_READ>();
+            sched_interleave<0, NM, NR, AV, VMEM_READ>();
             __builtin_amdgcn_sched_barrier(0);
-            dmaA(na, kn);
+            dmaB(nb, kn);
             fload(ca, cb, 2, 0);
             mfmas(1);
-            sched_interleave<0, NM, NR, AV, VMEM_READ>();
+            sched_interleave<0, NM, NR, BV, VMEM_READ>();
             __builtin_amdgcn_sched_barrier(0);
             fload(ca, cb, 3, 1);
             mfmas(0);
