@@ -26,7 +26,9 @@
 // cut along K into pieces at the same positions in every tile when that keeps
 // at least two workgroups per tile busy, and the last workgroup to finish a
 // piece of a split tile adds the pieces in a fixed order and runs the
-// epilogue.
+// epilogue.  A shared group with a K at least twice the routed K has its tiles
+// cut into two K halves the same way, so that they no longer set the length of
+// the launch.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -443,7 +445,21 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
     const int grid = (int)gridDim.x;                // a multiple of 8, at most SK_MAX_GRID
     const int vid = (blockIdx.x & 7) * (grid >> 3) + (blockIdx.x >> 3);
     constexpr uint32_t OOR = 0x80000000u;           // offset past every buffer: reads zero
-    const int rounds = total / grid, head = rounds * grid;
+    // A shared group whose K is at least twice the routed K (the down
+    // projection of several shared experts) has tiles that outlast the routed
+    // ones several times over.  When the grid holds two pieces of each, every
+    // shared tile is cut along K into two halves: work item i < 2 nsh is half
+    // i / nsh of shared tile i mod nsh (the shared tiles come first in the
+    // list), and the routed tiles follow as whole items, so that they fill in
+    // around the halves.
+    int nsh = 0;
+    if (p.G > p.n_routed) {
+        const int rsh = p.offsets[p.n_routed + 1] - p.offsets[p.n_routed];
+        nsh = (rsh + BM - 1) / BM * (p.Ns / BN);
+    }
+    const bool sh_split = nsh > 0 && p.Ks >= 2 * p.Kr && p.Ks % (4 * BK) == 0 && 2 * nsh <= grid;
+    const int items = sh_split ? total + nsh : total;
+    const int rounds = items / grid, head = rounds * grid;
 
     // the tiles left after the whole rounds: when at least two workgroups per
     // tile are free, each tile is cut along K into `split` pieces at the same
@@ -454,24 +470,45 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
     // tiles have the same K: then every workgroup finishes its rounds at about
     // the same time (a shared group with a longer K keeps some workgroups busy
     // while the pieces would go out).
-    const int left = total - head;
+    const int left = items - head;
     int split = left > 0 ? grid / left : 0;
     if (split > SK_SPLIT) split = SK_SPLIT;
     if (split > p.Kr / (2 * BK)) split = p.Kr / (2 * BK);
     if (p.G > p.n_routed && p.Ks != p.Kr) split = 1;
+    // slots of the pieces of one split tile lie sstride apart
+    const int sstride = sh_split ? nsh : left;
 
     for (int r = 0; r <= rounds; ++r) {
+        // the thread index passes through an empty asm once per tile, so that
+        // the thread-dependent offsets below are recomputed per tile instead of
+        // being held (and spilled to scratch) across the whole persistent loop
+        int tid_r = tid;
+        asm volatile("" : "+v"(tid_r));
+        const int lane_r = tid_r & 63, wave_r = tid_r >> 6;
+        const int wm_r = wave_r >> 1, wn_r = wave_r & 1;
         TileLoc L;
         int kt_lo = 0, kt_hi = 0;       // K tiles of 64 of this piece
         int nseg = 1, ctr = 0, pslot = 0;
         if (r < rounds || split < 2) {
-            // whole tiles in rounds of `grid`, in snake order (odd rounds
-            // reversed), so that the workgroups that took the long tiles at the
-            // head of the list take the last tiles of the next round; the last
-            // round may be partial
-            const int tile = r * grid + ((r & 1) ? grid - 1 - vid : vid);
-            if (tile >= total || !decode_tile<BM, BN>(p, tile, L)) break;
-            kt_hi = L.K / BK;
+            // whole tiles (or shared halves) in rounds of `grid`, in snake
+            // order (odd rounds reversed), so that the workgroups that took
+            // the long tiles at the head of the list take the last tiles of
+            // the next round; the last round may be partial
+            const int item = r * grid + ((r & 1) ? grid - 1 - vid : vid);
+            if (item >= items) break;
+            if (sh_split && item < 2 * nsh) {
+                const int j = item / nsh;
+                ctr = item - j * nsh;
+                pslot = item;
+                if (!decode_tile<BM, BN>(p, ctr, L)) break;
+                const int half = L.K / (2 * BK);          // even: K is a multiple of 4 BK
+                kt_lo = j * half;
+                kt_hi = kt_lo + half;
+                nseg = 2;
+            } else {
+                if (!decode_tile<BM, BN>(p, sh_split ? item - nsh : item, L)) break;
+                kt_hi = L.K / BK;
+            }
         } else {
             const int pos = (rounds & 1) ? grid - 1 - vid : vid;
             if (pos >= split * left) break;
@@ -492,14 +529,14 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
         // LDS rows of 64 K values (128 bytes, unpadded); 16-byte chunk q of
         // row r holds the operand's chunk q ^ ((r >> 1) & 7), so that the 16
         // rows a fragment read serves per LDS cycle (16 lanes of 16 bytes over
-        // the 64 banks) fall on distinct banks.  Load instruction v of wave w
-        // covers rows (w AV + v) 8 .. +7 of the tile: lane l takes row + l / 8
+        // the 64 banks) fall on distinct banks.  Load instruction v of wave_r w
+        // covers rows (w AV + v) 8 .. +7 of the tile: lane_r l takes row + l / 8
         // and fetches the chunk that the direct-to-LDS load writes at position
         // l & 7 of that row, (l & 7) ^ ((r >> 1) & 7); with AV, BV even that is
         // gc0 for even v and gc1 for odd v.
-        const int gc0 = (lane & 7) ^ (lane >> 4);
-        const int gc1 = (lane & 7) ^ (4 | (lane >> 4));
-        const int rsub = lane >> 3;
+        const int gc0 = (lane_r & 7) ^ (lane_r >> 4);
+        const int gc1 = (lane_r & 7) ^ (4 | (lane_r >> 4));
+        const int rsub = lane_r >> 3;
         // A: the gathered token rows of X (gate/up) or the group's activation rows (down)
         const __bf16* Ab = MODE == 0 ? (const __bf16*)p.X
                                      : (shared ? (const __bf16*)p.As : (const __bf16*)p.Ar + (size_t)L.rowbase * K);
@@ -508,11 +545,11 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
         uint32_t aoff[AV];
 #pragma unroll
         for (int v = 0; v < AV; ++v) {
-            const int row = L.m0 + (wave * AV + v) * 8 + rsub;
+            const int row = L.m0 + (wave_r * AV + v) * 8 + rsub;
             const uint32_t src = MODE == 0 ? (row < L.R ? (uint32_t)p.row_tok[L.rowbase + row] : 0u) : (uint32_t)row;
             aoff[v] = row < L.R ? (src * (uint32_t)(MODE == 0 ? p.ldx : K) + ((v & 1) ? gc1 : gc0) * 8) * 2u : OOR;
         }
-        const uint32_t brow0 = (uint32_t)(L.n0 + wave * BV * 8 + rsub) * (uint32_t)K;
+        const uint32_t brow0 = (uint32_t)(L.n0 + wave_r * BV * 8 + rsub) * (uint32_t)K;
         const uint32_t boffe = (brow0 + gc0 * 8) * 2u, boffo = (brow0 + gc1 * 8) * 2u;
         const uint32_t bstride = 16u * (uint32_t)K;       // 8 rows, in bytes
 
@@ -531,23 +568,23 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
                 // (a local copy: the host pass drops the kernel when an array
                 // element captured by reference is the builtin's operand)
                 const uint32_t vo = aoff[v];
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(ra_rs, (lds_ptr)(sa + (wave * AV + v) * 8 * 64), 16, vo,
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(ra_rs, (lds_ptr)(sa + (wave_r * AV + v) * 8 * 64), 16, vo,
                                                          (uint32_t)k0 * 2u, 0, 0);
             }
         };
         auto dmaB = [&](__bf16* sb, int k0) {
 #pragma unroll
             for (int v = 0; v < BV; ++v)
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rb_rs, (lds_ptr)(sb + (wave * BV + v) * 8 * 64), 16,
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rb_rs, (lds_ptr)(sb + (wave_r * BV + v) * 8 * 64), 16,
                                                          ((v & 1) ? boffo : boffe) + v * bstride, (uint32_t)k0 * 2u,
                                                          0, 0);
         };
-        // fragment of row (lane & 31) of each 32-row block, K chunk 2 ks + lane / 32
-        const int arow = (wm * WM + (lane & 31)) * 64;
-        const int brow = (wn * WN + (lane & 31)) * 64;
+        // fragment of row (lane_r & 31) of each 32-row block, K chunk 2 ks + lane_r / 32
+        const int arow = (wm_r * WM + (lane_r & 31)) * 64;
+        const int brow = (wn_r * WN + (lane_r & 31)) * 64;
         bf16x8 af[2][FM], bfm[2][FN];
         auto fload = [&](const __bf16* sa, const __bf16* sb, int ks, int slot) {
-            const int pos = ((2 * ks + (lane >> 5)) ^ ((lane >> 1) & 7)) * 8;   // row & 31 = lane & 31
+            const int pos = ((2 * ks + (lane_r >> 5)) ^ ((lane_r >> 1) & 7)) * 8;   // row & 31 = lane_r & 31
 #pragma unroll
             for (int i = 0; i < FM; ++i) af[slot][i] = *(const bf16x8*)(sa + arow + i * 32 * 64 + pos);
 #pragma unroll
@@ -565,7 +602,7 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
         // (A, then B: the gathered token rows first, 2-3% faster than the
         // other order), a whole K tile ahead of their use; every sub-step also
         // reads the fragments of the next one.  A K tile ends with the wait
-        // for this wave's loads and the barrier for everyone's.  The two
+        // for this wave_r's loads and the barrier for everyone's.  The two
         // buffers are separate LDS arrays and the loop is unrolled by two, so
         // that the loads into one buffer are never taken to alias the reads of
         // the other.  After the last tile the last K tile is re-read into the
@@ -589,7 +626,7 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
             __builtin_amdgcn_sched_barrier(0);
             mfmas(1);
             __builtin_amdgcn_sched_barrier(0);
-            __builtin_amdgcn_s_waitcnt(0x0F70);          // vmcnt(0): this wave's loads are in LDS
+            __builtin_amdgcn_s_waitcnt(0x0F70);          // vmcnt(0): this wave_r's loads are in LDS
             __syncthreads();
             fload(na, nb, 0, 0);
             __builtin_amdgcn_sched_barrier(0);
@@ -607,10 +644,10 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
         }
 
         if (nseg > 1) {
-            // a piece of a split tile: its partial sums go to slot j left + ctr
-            // (its position in the round), thread tid's 16-byte group h of
-            // block (i, j) at byte (((i FN + j) 4 + h) 256 + tid) 16 of the slot
-            // (each store instruction writes 4 KB in a row).  Buffer stores and loads keep the lane's offset in
+            // a piece of a split tile: its partial sums go to slot j sstride + ctr
+            // (its position in the round), thread tid_r's 16-byte group h of
+            // block (i, j) at byte (((i FN + j) 4 + h) 256 + tid_r) 16 of the slot
+            // (each store instruction writes 4 KB in a row).  Buffer stores and loads keep the lane_r's offset in
             // one register and the slot and group in the scalar offset.  They
             // carry the sc1 cache bit (the bit of agent-scope atomic loads and
             // stores), so each location is coherent across the XCDs' L2 caches
@@ -620,7 +657,7 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
             // arrival's loads are issued after the count is read.
             constexpr uint32_t TILE_BYTES = (uint32_t)BM * BN * 4u;
             const __amdgpu_buffer_rsrc_t rp = make_rsrc(p.sk_part, (uint32_t)SK_MAX_GRID * TILE_BYTES);
-            const uint32_t lo = (uint32_t)tid * 16u;
+            const uint32_t lo = (uint32_t)tid_r * 16u;
 #pragma unroll
             for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -632,22 +669,22 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
                                                                (int)((uint32_t)pslot * TILE_BYTES +
                                                                      (uint32_t)((i * FN + j) * 4 + h) * 4096u), SC1);
                     }
-            __builtin_amdgcn_s_waitcnt(0x0F70);          // vmcnt(0): this wave's stores are done
+            __builtin_amdgcn_s_waitcnt(0x0F70);          // vmcnt(0): this wave_r's stores are done
             __syncthreads();
-            if (tid == 0) s_last = atomicAdd(p.sk_cnt + MODE * SK_MAX_GRID + ctr, 1) == nseg - 1;
+            if (tid_r == 0) s_last = atomicAdd(p.sk_cnt + MODE * SK_MAX_GRID + ctr, 1) == nseg - 1;
             __syncthreads();
             if (!s_last) continue;
             // the last arrival: the tile is the sum of its pieces in K order
-            // (piece j in slot j * left + ctr).  Every group reads SK_SPLIT
+            // (piece j in slot j * sstride + ctr).  Every group reads SK_SPLIT
             // pieces without a branch, so that the loads of many groups are in
-            // flight together: the pieces past nseg have a lane offset past the
-            // buffer (the range check covers the lane offset) and read as
+            // flight together: the pieces past nseg have a lane_r offset past the
+            // buffer (the range check covers the lane_r offset) and read as
             // zeros, and adding them leaves the sum as it is (up to the sign of
             // a zero).
             uint32_t pbase[SK_SPLIT], plo[SK_SPLIT];
 #pragma unroll
             for (int sg = 0; sg < SK_SPLIT; ++sg) {
-                pbase[sg] = sg < nseg ? (uint32_t)(ctr + sg * left) * TILE_BYTES : 0u;
+                pbase[sg] = sg < nseg ? (uint32_t)(ctr + sg * sstride) * TILE_BYTES : 0u;
                 plo[sg] = sg < nseg ? lo : OOR;
             }
 #pragma unroll
@@ -674,14 +711,14 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
                     }
         }
 
-        // epilogue: element e of a 32x32 block is row (e/4)*8 + (lane/32)*4 + e%4,
-        // column lane%32
-        const int rbase = L.m0 + wm * WM + (lane >> 5) * 4;
+        // epilogue: element e of a 32x32 block is row (e/4)*8 + (lane_r/32)*4 + e%4,
+        // column lane_r%32
+        const int rbase = L.m0 + wm_r * WM + (lane_r >> 5) * 4;
         if (MODE == 0) {
             __bf16* out = shared ? (__bf16*)p.Os : (__bf16*)p.Or;
             const int ldo = L.N / 2;
             const int orow0 = shared ? 0 : L.rowbase;
-            const int cbase = (L.n0 + wn * WN) / 2 + (lane & 31);
+            const int cbase = (L.n0 + wn_r * WN) / 2 + (lane_r & 31);
 #pragma unroll
             for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -698,7 +735,7 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
         } else {
             __bf16* out = (__bf16*)p.Or;
             const int ldo = L.N;
-            const int cbase = L.n0 + wn * WN + (lane & 31);
+            const int cbase = L.n0 + wn_r * WN + (lane_r & 31);
 #pragma unroll
             for (int i = 0; i < FM; ++i)
 #pragma unroll

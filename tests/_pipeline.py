@@ -296,7 +296,8 @@ def with_horizon(sc: StreamCase, H: int, allow_sub: Optional[int] = None) -> Str
 # mirror to know which of their shapes exercise the split.
 def gemm_plan(cfg, rows, n_local: int, cus: int = 256):
     """rows: the forward's row_offsets output [n_local + 2].  Returns
-    {"gate_up": (tiles, grid, rounds, left, split), "down": (...)}."""
+    {"gate_up": (tiles, grid, rounds, left, split, shared_halves), "down": (...)};
+    shared_halves is 1 when the shared tiles are cut into two K halves."""
     R = np.diff(np.asarray(rows, dtype=np.int64))       # rows per group, shared last
     has_sh = cfg.n_shared > 0
     T, k, d, f, ns = cfg.T, cfg.k, cfg.d, cfg.f, cfg.n_shared
@@ -313,12 +314,15 @@ def gemm_plan(cfg, rows, n_local: int, cus: int = 256):
         if has_sh:
             tiles += -(-int(R[n_local]) // bm) * (Ns // bn)
         grid = grid_of(ub)
-        rounds = tiles // grid
-        left = tiles - rounds * grid
+        nsh = -(-int(R[n_local]) // bm) * (Ns // bn) if has_sh else 0
+        halves = int(nsh > 0 and Ks >= 2 * Kr and Ks % 256 == 0 and 2 * nsh <= grid)
+        items = tiles + nsh * halves
+        rounds = items // grid
+        left = items - rounds * grid
         split = min(grid // left, 4, Kr // 128) if left else 0
         if has_sh and Ks != Kr:
             split = 1
-        return tiles, grid, rounds, left, split
+        return tiles, grid, rounds, left, split, halves
 
     ub_gu = (-(-rr // 256) + n_local) * (2 * f // 256) + ((-(-rs // 256) + 1) * (2 * ns * f // 256) if has_sh else 0)
     ub_dn = (-(-(rr + rs) // 192) + n_local + int(has_sh)) * (d // 256)

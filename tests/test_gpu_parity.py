@@ -49,10 +49,15 @@ SMALL = {
     # pieces with no whole round, and 3 pieces
     "C3split": wl.C3.with_(T=600, d=1024, f=512, n_shared=1, T_cal=4096),
     "C4split": wl.C4.with_(T=1200, d=1024, f=768, n_shared=1, T_cal=4096),
+    # four shared experts: the down projection's shared K is four times the
+    # routed K, so its shared tiles are cut into two K halves
+    "C3sh": wl.C3.with_(T=600, d=1024, f=512, n_shared=4, T_cal=4096),
 }
 # shapes whose GEMM plan splits leftover tiles along K (checked on the GPU's rows)
 SPLIT = {"C3split": {"gate_up": 4, "down": 4}, "C4split": {"gate_up": 3, "down": 3},
          "C2": {"gate_up": 2}, "C2x": {"gate_up": 3}}
+# shapes whose down projection cuts its shared tiles into two K halves
+SHARED_HALVES = {"C3sh", "C3"}
 # decode-sized batches (at most 128 tokens): the thin-GEMM path of the forward
 DECODE = {
     "C2d": wl.C2.with_(T=64, T_cal=4096),
@@ -138,12 +143,15 @@ def _check_output(case, dec, y_gpu, tokens, ok, tol):
 def _check_split(name, case, rows):
     """The shapes meant to exercise the split along K do split (host mirror of
     the launch plan, from the GPU's own row counts)."""
-    if name not in SPLIT:
+    if name not in SPLIT and name not in SHARED_HALVES:
         return
     plan = gemm_plan(case.cfg, rows, len(case.local))
-    print("[%s] GEMM plan (tiles, grid, rounds, left, split): %s" % (case.cfg.name, plan), flush=True)
-    for gemm, want in SPLIT[name].items():
+    print("[%s] GEMM plan (tiles, grid, rounds, left, split, shared halves): %s" % (case.cfg.name, plan),
+          flush=True)
+    for gemm, want in SPLIT.get(name, {}).items():
         assert plan[gemm][4] == want, (gemm, plan[gemm])
+    assert plan["down"][5] == int(name in SHARED_HALVES), plan["down"]
+    assert plan["gate_up"][5] == 0, plan["gate_up"]
 
 
 @pytest.mark.parametrize("name", list(SMALL))
@@ -333,11 +341,11 @@ def test_invalid_locations_are_counted_not_routed():
     assert c[:4].sum() == (case.X.shape[0] - 2) * case.cfg.k
 
 
-@pytest.mark.parametrize("name", ["C3s", "C3d", "C3split", "C2"])
+@pytest.mark.parametrize("name", ["C3s", "C3d", "C3split", "C3sh", "C2"])
 def test_runs_are_bitwise_deterministic(name):
-    """Two runs give the same bits; C3split and the full C2 layer split GEMM
-    tiles along K, whose pieces are summed in K order by whichever workgroup
-    arrives last."""
+    """Two runs give the same bits; C3split, C3sh and the full C2 layer split
+    GEMM tiles along K, whose pieces are summed in K order by whichever
+    workgroup arrives last."""
     case, tabs = _case(name, {**SMALL, **DECODE, **FULL}[name])
     dl = DeviceLayer(case, tabs)
     x, loc, qh = dl.inputs()
