@@ -87,13 +87,13 @@ def _flags(dec, out):
     return (dec["margin"] < 1e-4) | (host(out["margin"]) < 1e-4)
 
 
-def _check_decisions(case, dec, out):
+def _check_decisions(case, dec, out, max_flagged=0.01):
     cfg = case.cfg
     T, k = dec["idx"].shape
     fl = _flags(dec, out)
     ok = ~fl
     print("[%s] T=%d flagged=%d" % (cfg.name, T, int(fl.sum())), flush=True)
-    assert fl.sum() <= max(2, 0.01 * T)
+    assert fl.sum() <= max(2, max_flagged * T)
     g = {n: host(out[n]) for n in ("idx", "exec_k", "exec_m", "cls", "qhat_out", "loc_out", "flag")}
     np.testing.assert_array_equal(g["idx"][ok], dec["idx"][ok])
     np.testing.assert_array_equal(g["exec_k"][ok], dec["exec_k"][ok])
