@@ -378,6 +378,19 @@ __device__ inline bool decode_tile(const GemmArgs& p, int tile, TileLoc& L) {
     return false;
 }
 
+// Position of workgroup vid in round r of n work items (n <= grid): odd
+// rounds mirrored (snake order); with `spread`, a partial round is shared
+// evenly by the 8 XCDs (vid / (grid / 8) is the workgroup's XCD), so that no
+// XCD sits idle while another runs a full share.  -1: no item for this
+// workgroup.
+__device__ inline int round_pos(int vid, int r, int n, int grid, bool spread) {
+    const int v = (r & 1) ? grid - 1 - vid : vid;
+    if (n >= grid || !spread) return v < n ? v : -1;
+    const int g8 = grid >> 3, x = v / g8, j = v - x * g8;
+    const int lo = x * n / 8, hi = (x + 1) * n / 8;
+    return j < hi - lo ? lo + j : -1;
+}
+
 __device__ inline float silu_f(float g) { return g / (1.0f + __expf(-g)); }
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -477,6 +490,10 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
     if (p.G > p.n_routed && p.Ks != p.Kr) split = 1;
     // slots of the pieces of one split tile lie sstride apart
     const int sstride = sh_split ? nsh : left;
+    // the last, partial round is spread over the XCDs when every tile has the
+    // same K; otherwise the snake order gives it to the workgroups that just
+    // ran short tiles
+    const bool spread = !(p.G > p.n_routed && p.Ks != p.Kr);
 
     for (int r = 0; r <= rounds; ++r) {
         // the thread index passes through an empty asm once per tile, so that
@@ -494,7 +511,9 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
             // order (odd rounds reversed), so that the workgroups that took
             // the long tiles at the head of the list take the last tiles of
             // the next round; the last round may be partial
-            const int item = r * grid + ((r & 1) ? grid - 1 - vid : vid);
+            const int pos = round_pos(vid, r, r < rounds ? grid : items - head, grid, spread);
+            if (pos < 0) break;
+            const int item = r * grid + pos;
             if (item >= items) break;
             if (sh_split && item < 2 * nsh) {
                 const int j = item / nsh;
@@ -510,8 +529,8 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
                 kt_hi = L.K / BK;
             }
         } else {
-            const int pos = (rounds & 1) ? grid - 1 - vid : vid;
-            if (pos >= split * left) break;
+            const int pos = round_pos(vid, rounds, split * left, grid, spread);
+            if (pos < 0) break;
             const int j = pos / left;
             ctr = pos - j * left;
             pslot = pos;
