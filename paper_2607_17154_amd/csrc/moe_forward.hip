@@ -803,7 +803,14 @@ ggemm_thin(const GemmArgs p) {
     const int vid = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
     constexpr uint32_t OOR = 0x80000000u;
 
-    for (int tile = vid; tile < total; tile += gridDim.x) {
+    // rounds of gridDim.x tiles; the last, partial round shared evenly by the
+    // XCDs when every tile has the same K
+    const bool spread = !(p.G > p.n_routed && p.Ks != p.Kr);
+    for (int r = 0; r * (int)gridDim.x < total; ++r) {
+        const int n = total - r * (int)gridDim.x;
+        const int pos = round_pos(vid, 0, n, (int)gridDim.x, spread);
+        if (pos < 0) break;
+        const int tile = r * (int)gridDim.x + pos;
         TileLoc L;
         if (!decode_tile<TH_BM, TH_BN>(p, tile, L)) break;
         const bool shared = L.g >= p.n_routed;
