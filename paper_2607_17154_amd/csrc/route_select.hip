@@ -1,7 +1,8 @@
 // Routing and runtime server-expert selection of one MoE layer on gfx950.
 //
 // Kernel 1 (route_select_kernel), one block of 8 waves per TB tokens (TB = 16,
-// or 32 for large batches of at most 64 experts):
+// or 32 for large batches of at most 64 experts), compiled for slot bounds of
+// 2, 4, 6 and 8 (the smallest that holds k runs):
 //   * the first words of the candidate tables are read into registers first,
 //     so that their latency hides behind the router loop, and stored to LDS
 //     after it together with the rest;
@@ -334,10 +335,13 @@ __host__ __device__ inline int route_region0_floats(int tb, int E) {
     return part > wbuf ? part : wbuf;
 }
 
-// up to 64 experts: at most 128 VGPRs (4 waves per SIMD), so two blocks share a CU
-template <int NBT, int TB>
+// up to 64 experts: at most 128 VGPRs (4 waves per SIMD), so two blocks share a CU.
+// KM: the slot arrays and loops of the token stage are sized for k <= KM (2, 4,
+// 6 or 8), so that a top-2 layer does not carry the work of eight slots.
+template <int NBT, int TB, int KM>
 __global__ void __launch_bounds__(RT_THREADS) __attribute__((amdgpu_waves_per_eu(NBT <= 4 ? 4 : 2)))
 route_select_kernel(const RouteArgs a) {
+    static_assert(KM >= 1 && KM <= ORDERMOE_MAX_TOPK, "slots");
     constexpr int RG = TB / 16;                 // 16-token row groups of the router
     constexpr int KW = RT_WAVES / RG;           // waves sharing one row group's K loop
     static_assert(KW == 8 || KW == RT_SLOTS, "one or two reduction rounds");
@@ -516,10 +520,10 @@ route_select_kernel(const RouteArgs a) {
         okey[i] = e < E ? f2ord(v) : 0u;
     }
     uint32_t removed = 0;                    // bit i: local element j + 16 i taken
-    int sel_e[ORDERMOE_MAX_TOPK + 1];
-    float sel_v[ORDERMOE_MAX_TOPK + 1];
+    int sel_e[KM + 1];
+    float sel_v[KM + 1];
 #pragma unroll
-    for (int r = 0; r < ORDERMOE_MAX_TOPK + 1; ++r) {
+    for (int r = 0; r < KM + 1; ++r) {
         if (r < kk1) {
             uint64_t best = 0;
 #pragma unroll
@@ -538,7 +542,7 @@ route_select_kernel(const RouteArgs a) {
     }
     float mg = __builtin_inff();
 #pragma unroll
-    for (int r = 0; r < ORDERMOE_MAX_TOPK; ++r) {
+    for (int r = 0; r < KM; ++r) {
         if (r + 1 < kk1) {
             float gap = sel_v[r] - sel_v[r + 1];
             mg = gap < mg ? gap : mg;
@@ -548,7 +552,7 @@ route_select_kernel(const RouteArgs a) {
     float den = 0.f;
     if (a.renorm) {
 #pragma unroll
-        for (int r = 0; r < ORDERMOE_MAX_TOPK; ++r)
+        for (int r = 0; r < KM; ++r)
             if (r < k) den += expf(sel_v[r] - sel_v[0]);
     } else {
         for (int e = j; e < E; e += 16) den += expf(lg[e] - sel_v[0]);
@@ -569,15 +573,15 @@ route_select_kernel(const RouteArgs a) {
     const bool subs_on = a.allow_sub && a.Qbar > 0.f;
     const uint32_t mmask = M >= 32 ? 0xFFFFFFFFu : ((1u << M) - 1u);   // servers that exist
     const int jm1 = j >= 1 ? j - 1 : 0;
-    int ke[ORDERMOE_MAX_TOPK];
-    float qe[ORDERMOE_MAX_TOPK];
-    uint32_t msv[ORDERMOE_MAX_TOPK];
-    uint64_t key[ORDERMOE_MAX_TOPK];
-    bool search[ORDERMOE_MAX_TOPK];
+    int ke[KM];
+    float qe[KM];
+    uint32_t msv[KM];
+    uint64_t key[KM];
+    bool search[KM];
     // every slot's table reads are issued (slots past k read slot 0's entries,
     // discarded), then masked, so that no per-slot branch serialises them
 #pragma unroll
-    for (int slot = 0; slot < ORDERMOE_MAX_TOPK; ++slot) {
+    for (int slot = 0; slot < KM; ++slot) {
         const bool on = slot < k;
         const int r = sel_e[on ? slot : 0];
         const uint32_t rmask = s_mask[r];
@@ -597,7 +601,7 @@ route_select_kernel(const RouteArgs a) {
     // server in the Local Substitute Only mode)
     const uint32_t lmask = a.allow_sub == 2 && j >= 1 ? 1u << (s_loc & 31) : ~0u;
 #pragma unroll
-    for (int slot = 0; slot < ORDERMOE_MAX_TOPK; ++slot) {
+    for (int slot = 0; slot < KM; ++slot) {
         const uint32_t hm = s_mask[ke[slot] >= 0 ? ke[slot] : 0];
         msv[slot] = search[slot] && ke[slot] >= 0 ? hm & mmask & lmask : 0u;
     }
@@ -605,10 +609,10 @@ route_select_kernel(const RouteArgs a) {
     for (;;) {
         uint32_t any = 0;
 #pragma unroll
-        for (int slot = 0; slot < ORDERMOE_MAX_TOPK; ++slot) any |= msv[slot];
+        for (int slot = 0; slot < KM; ++slot) any |= msv[slot];
         if (!__builtin_amdgcn_ballot_w64(any != 0)) break;
 #pragma unroll
-        for (int slot = 0; slot < ORDERMOE_MAX_TOPK; ++slot) {
+        for (int slot = 0; slot < KM; ++slot) {
             if (msv[slot]) {
                 const int m = __builtin_ctz(msv[slot]);
                 msv[slot] &= msv[slot] - 1;
@@ -624,7 +628,7 @@ route_select_kernel(const RouteArgs a) {
     int first_m = s_loc, ncls[4] = {0, 0, 0, 0}, nremote = 0;
     uint32_t dstmask = 0;
 #pragma unroll
-    for (int slot = 0; slot < ORDERMOE_MAX_TOPK; ++slot) {
+    for (int slot = 0; slot < KM; ++slot) {
         if (slot >= k) break;
         const int r = sel_e[slot];
         int km = r, mm = s_loc;
@@ -797,16 +801,25 @@ dispatch_small_kernel(const int64_t* blk_cnt, int nblk, const uint8_t* exec_m, c
     }
 }
 
-template <int NBT, int TB>
-int launch_route_kernel(const RouteArgs& a, size_t smem, hipStream_t st) {
+template <int NBT, int TB, int KM>
+int launch_route_kernel_k(const RouteArgs& a, size_t smem, hipStream_t st) {
     if (smem > 65536) {
-        hipError_t e = hipFuncSetAttribute((const void*)route_select_kernel<NBT, TB>,
+        hipError_t e = hipFuncSetAttribute((const void*)route_select_kernel<NBT, TB, KM>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
         if (e != hipSuccess) return (int)e;
     }
     KernelTimer kt_("route_select", st);
-    hipLaunchKernelGGL((route_select_kernel<NBT, TB>), dim3(a.nblk), dim3(RT_THREADS), smem, st, a);
+    hipLaunchKernelGGL((route_select_kernel<NBT, TB, KM>), dim3(a.nblk), dim3(RT_THREADS), smem, st, a);
     return (int)hipGetLastError();
+}
+
+// the kernel sized for the smallest slot bound (2, 4, 6, 8) that holds k
+template <int NBT, int TB>
+int launch_route_kernel(const RouteArgs& a, size_t smem, hipStream_t st) {
+    if (a.k <= 2) return launch_route_kernel_k<NBT, TB, 2>(a, smem, st);
+    if (a.k <= 4) return launch_route_kernel_k<NBT, TB, 4>(a, smem, st);
+    if (a.k <= 6) return launch_route_kernel_k<NBT, TB, 6>(a, smem, st);
+    return launch_route_kernel_k<NBT, TB, ORDERMOE_MAX_TOPK>(a, smem, st);
 }
 
 size_t route_smem(int tb, int E, int gmax, int M, bool S_in_lds) {
