@@ -393,6 +393,16 @@ __device__ inline int round_pos(int vid, int r, int n, int grid, bool spread) {
 
 __device__ inline float silu_f(float g) { return g / (1.0f + __expf(-g)); }
 
+// Workgroup barrier of the K loop.  __syncthreads() (and a workgroup fence on
+// LDS alone) waits for every outstanding load into LDS (vmcnt 0), which would
+// also drain the loads of a buffer that is read only a tile later; this one
+// is the bare s_barrier, and the memory clobber keeps the compiler from moving
+// memory accesses across it.  The caller first waits (s_waitcnt vmcnt) for its
+// own loads into the buffers read after the barrier, and every LDS read of a
+// buffer has returned its data (it fed an MFMA) before the barrier that
+// precedes the next load into that buffer.
+__device__ inline void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void* lds_ptr;
@@ -439,7 +449,7 @@ __device__ inline void sched_interleave() {
 // arrival completes the tile's counter sums the tile's pieces in K order (so
 // the result does not depend on who is last) and runs the epilogue.  No
 // workgroup waits for another.
-template <int BM, int BN, int MODE>
+template <int BM, int BN, int MODE, int NBB>
 __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
     constexpr int BK = 64;
     constexpr int WM = BM / 2, WN = BN / 2;
@@ -449,7 +459,10 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
     static_assert(FN % 2 == 0, "gate/up pairs need an even number of 32-column blocks");
     static_assert(BM % 64 == 0 && BN % 64 == 0, "an even number of load instructions per wave");
     // two buffers of the A and B tiles, [rows][64] bf16 each
+    static_assert(NBB == 2 || NBB == 3, "two or three weight buffers");
+    // two buffers of the A tile and NBB of the B tile, [rows][64] bf16 each
     __shared__ __attribute__((aligned(16))) __bf16 sA0[BM * 64], sA1[BM * 64], sB0[BN * 64], sB1[BN * 64];
+    __shared__ __attribute__((aligned(16))) __bf16 sB2[NBB == 3 ? BN * 64 : 8];
     __shared__ int s_last;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -628,13 +641,20 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
         // idle buffer, never used.
         constexpr int NM = FM * FN, NR = FM + FN;
         constexpr int VMEM_READ = 0x020;
-        auto ktile = [&](__bf16* ca, __bf16* cb, __bf16* na, __bf16* nb, int kn) {
-            dmaA(na, kn);
+        // wait at the end of a K tile: with three B buffers the B loads of the
+        // tile after next (the last BV loads issued) stay in flight
+        constexpr int KT_WAIT = NBB == 3 ? 0x0F70 | BV : 0x0F70;
+        static_assert(BV < 16, "vmcnt field");
+        // one K tile: ca/cb hold it; na/nbn will hold the next tile's A and B;
+        // the A loads of tile kna and the B loads of tile knb (the next tile
+        // with two B buffers, the tile after next with three) go to na and nbl
+        auto ktile = [&](__bf16* ca, __bf16* cb, __bf16* na, __bf16* nbn, __bf16* nbl, int kna, int knb) {
+            dmaA(na, kna);
             fload(ca, cb, 1, 1);
             mfmas(0);
             sched_interleave<0, NM, NR, AV, VMEM_READ>();
             __builtin_amdgcn_sched_barrier(0);
-            dmaB(nb, kn);
+            dmaB(nbl, knb);
             fload(ca, cb, 2, 0);
             mfmas(1);
             sched_interleave<0, NM, NR, BV, VMEM_READ>();
@@ -645,21 +665,42 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
             __builtin_amdgcn_sched_barrier(0);
             mfmas(1);
             __builtin_amdgcn_sched_barrier(0);
-            __builtin_amdgcn_s_waitcnt(0x0F70);          // vmcnt(0): this wave_r's loads are in LDS
-            __syncthreads();
-            fload(na, nb, 0, 0);
+            __builtin_amdgcn_s_waitcnt(KT_WAIT);         // this wave_r's loads of the next tile are in LDS
+            lds_barrier();
+            fload(na, nbn, 0, 0);
             __builtin_amdgcn_sched_barrier(0);
         };
-        // the piece's K tiles [kt_lo, kt_hi): an even number (K units of 128)
+        // the piece's K tiles [kt_lo, kt_hi): an even number (K units of 128).
+        // Loads past the piece re-read its last K tile into an idle buffer.
+        const int klast = kt_hi - 1;
+        auto kc = [&](int k) { return (k < kt_hi ? k : klast) * BK; };
         dmaA(sA0, kt_lo * BK);
         dmaB(sB0, kt_lo * BK);
-        __builtin_amdgcn_s_waitcnt(0x0F70);
-        __syncthreads();
+        if constexpr (NBB == 3) dmaB(sB1, kc(kt_lo + 1));
+        __builtin_amdgcn_s_waitcnt(KT_WAIT);
+        lds_barrier();
         fload(sA0, sB0, 0, 0);
         __builtin_amdgcn_sched_barrier(0);
-        for (int kt = kt_lo; kt < kt_hi; kt += 2) {
-            ktile(sA0, sB0, sA1, sB1, (kt + 1) * BK);
-            ktile(sA1, sB1, sA0, sB0, (kt + 2 < kt_hi ? kt + 2 : kt + 1) * BK);
+        if constexpr (NBB == 2) {
+            for (int kt = kt_lo; kt < kt_hi; kt += 2) {
+                ktile(sA0, sB0, sA1, sB1, sB1, (kt + 1) * BK, (kt + 1) * BK);
+                ktile(sA1, sB1, sA0, sB0, sB0, kc(kt + 2), kc(kt + 2));
+            }
+        } else {
+            // A buffers alternate over two tiles, B buffers over three: six
+            // tiles per pass, leaving after any even number of them
+            for (int kt = kt_lo; kt < kt_hi; kt += 6) {
+                ktile(sA0, sB0, sA1, sB1, sB2, kc(kt + 1), kc(kt + 2));
+                ktile(sA1, sB1, sA0, sB2, sB0, kc(kt + 2), kc(kt + 3));
+                if (kt + 2 >= kt_hi) break;
+                ktile(sA0, sB2, sA1, sB0, sB1, kc(kt + 3), kc(kt + 4));
+                ktile(sA1, sB0, sA0, sB1, sB2, kc(kt + 4), kc(kt + 5));
+                if (kt + 4 >= kt_hi) break;
+                ktile(sA0, sB1, sA1, sB2, sB0, kc(kt + 5), kc(kt + 6));
+                ktile(sA1, sB2, sA0, sB0, sB1, kc(kt + 6), kc(kt + 7));
+            }
+            // B loads of the tile after the last may still be in flight
+            __builtin_amdgcn_s_waitcnt(0x0F70);
         }
 
         if (nseg > 1) {
@@ -1158,7 +1199,7 @@ int launch_local_forward(const ForwardArgs& f, void* stream) {
     } else if (f.dtype == ORDERMOE_BF16) {
         {
         KernelTimer kt_("gemm_gate_up", st);
-        ggemm_bf16<GU_BM, GU_BN, 0><<<dim3(bf16_grid(ub_gu)), dim3(256), 0, st>>>(g);
+        ggemm_bf16<GU_BM, GU_BN, 0, 2><<<dim3(bf16_grid(ub_gu)), dim3(256), 0, st>>>(g);
         }
         if ((e = hipGetLastError()) != hipSuccess) return (int)e;
     } else {
@@ -1181,7 +1222,7 @@ int launch_local_forward(const ForwardArgs& f, void* stream) {
     } else if (f.dtype == ORDERMOE_BF16) {
         {
         KernelTimer kt_("gemm_down", st);
-        ggemm_bf16<DN_BM, DN_BN, 1><<<dim3(bf16_grid(ub_dn)), dim3(256), 0, st>>>(g);
+        ggemm_bf16<DN_BM, DN_BN, 1, 3><<<dim3(bf16_grid(ub_dn)), dim3(256), 0, st>>>(g);
         }
     } else {
         {
