@@ -463,7 +463,10 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
     // two buffers of the A tile and NBB of the B tile, [rows][64] bf16 each
     __shared__ __attribute__((aligned(16))) __bf16 sA0[BM * 64], sA1[BM * 64], sB0[BN * 64], sB1[BN * 64];
     __shared__ __attribute__((aligned(16))) __bf16 sB2[NBB == 3 ? BN * 64 : 8];
-    __shared__ int s_last;
+    // the split-tile arrival flag lives in sB2, which is idle from the end of
+    // a K loop until the first K tile of the next one (the next prologue loads
+    // sA0, sB0 and sB1 only), so that three 256 x 256 buffers fill the LDS
+    int* const s_last = (int*)sB2;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
@@ -516,6 +519,9 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
         asm volatile("" : "+v"(tid_r));
         const int lane_r = tid_r & 63, wave_r = tid_r >> 6;
         const int wm_r = wave_r >> 1, wn_r = wave_r & 1;
+        // the wave index as a scalar: the LDS destinations of the loads into LDS
+        // (the M0 operand) are then scalar expressions, not VGPRs held per buffer
+        const int wave_u = __builtin_amdgcn_readfirstlane(wave_r);
         TileLoc L;
         int kt_lo = 0, kt_hi = 0;       // K tiles of 64 of this piece
         int nseg = 1, ctr = 0, pslot = 0;
@@ -600,14 +606,14 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
                 // (a local copy: the host pass drops the kernel when an array
                 // element captured by reference is the builtin's operand)
                 const uint32_t vo = aoff[v];
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(ra_rs, (lds_ptr)(sa + (wave_r * AV + v) * 8 * 64), 16, vo,
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(ra_rs, (lds_ptr)(sa + (wave_u * AV + v) * 8 * 64), 16, vo,
                                                          (uint32_t)k0 * 2u, 0, 0);
             }
         };
         auto dmaB = [&](__bf16* sb, int k0) {
 #pragma unroll
             for (int v = 0; v < BV; ++v)
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rb_rs, (lds_ptr)(sb + (wave_r * BV + v) * 8 * 64), 16,
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rb_rs, (lds_ptr)(sb + (wave_u * BV + v) * 8 * 64), 16,
                                                          ((v & 1) ? boffo : boffe) + v * bstride, (uint32_t)k0 * 2u,
                                                          0, 0);
         };
@@ -689,15 +695,23 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
         } else {
             // A buffers alternate over two tiles, B buffers over three: six
             // tiles per pass, leaving after any even number of them
-            for (int kt = kt_lo; kt < kt_hi; kt += 6) {
+            int kt = kt_lo;
+            for (; kt + 6 <= kt_hi; kt += 6) {
                 ktile(sA0, sB0, sA1, sB1, sB2, kc(kt + 1), kc(kt + 2));
                 ktile(sA1, sB1, sA0, sB2, sB0, kc(kt + 2), kc(kt + 3));
-                if (kt + 2 >= kt_hi) break;
                 ktile(sA0, sB2, sA1, sB0, sB1, kc(kt + 3), kc(kt + 4));
                 ktile(sA1, sB0, sA0, sB1, sB2, kc(kt + 4), kc(kt + 5));
-                if (kt + 4 >= kt_hi) break;
                 ktile(sA0, sB1, sA1, sB2, sB0, kc(kt + 5), kc(kt + 6));
                 ktile(sA1, sB2, sA0, sB0, sB1, kc(kt + 6), kc(kt + 7));
+            }
+            // the remaining two or four tiles start a pass
+            if (kt < kt_hi) {
+                ktile(sA0, sB0, sA1, sB1, sB2, kc(kt + 1), kc(kt + 2));
+                ktile(sA1, sB1, sA0, sB2, sB0, kc(kt + 2), kc(kt + 3));
+                if (kt + 2 < kt_hi) {
+                    ktile(sA0, sB2, sA1, sB0, sB1, kc(kt + 3), kc(kt + 4));
+                    ktile(sA1, sB0, sA0, sB1, sB2, kc(kt + 4), kc(kt + 5));
+                }
             }
             // B loads of the tile after the last may still be in flight
             __builtin_amdgcn_s_waitcnt(0x0F70);
@@ -731,9 +745,9 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
                     }
             __builtin_amdgcn_s_waitcnt(0x0F70);          // vmcnt(0): this wave_r's stores are done
             __syncthreads();
-            if (tid_r == 0) s_last = atomicAdd(p.sk_cnt + MODE * SK_MAX_GRID + ctr, 1) == nseg - 1;
+            if (tid_r == 0) *s_last = atomicAdd(p.sk_cnt + MODE * SK_MAX_GRID + ctr, 1) == nseg - 1;
             __syncthreads();
-            if (!s_last) continue;
+            if (!*s_last) continue;
             // the last arrival: the tile is the sum of its pieces in K order
             // (piece j in slot j * sstride + ctr).  Every group reads SK_SPLIT
             // pieces without a branch, so that the loads of many groups are in
@@ -1199,7 +1213,7 @@ int launch_local_forward(const ForwardArgs& f, void* stream) {
     } else if (f.dtype == ORDERMOE_BF16) {
         {
         KernelTimer kt_("gemm_gate_up", st);
-        ggemm_bf16<GU_BM, GU_BN, 0, 2><<<dim3(bf16_grid(ub_gu)), dim3(256), 0, st>>>(g);
+        ggemm_bf16<GU_BM, GU_BN, 0, 3><<<dim3(bf16_grid(ub_gu)), dim3(256), 0, st>>>(g);
         }
         if ((e = hipGetLastError()) != hipSuccess) return (int)e;
     } else {
