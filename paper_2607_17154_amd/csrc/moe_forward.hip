@@ -31,6 +31,8 @@
 // the launch.
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include <cstdint>
 
 #include "common.hpp"
@@ -449,7 +451,7 @@ __device__ inline void sched_interleave() {
 // arrival completes the tile's counter sums the tile's pieces in K order (so
 // the result does not depend on who is last) and runs the epilogue.  No
 // workgroup waits for another.
-template <int BM, int BN, int MODE, int NBB>
+template <int BM, int BN, int MODE, int NBA, int NBB>
 __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
     constexpr int BK = 64;
     constexpr int WM = BM / 2, WN = BN / 2;
@@ -459,14 +461,16 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
     static_assert(FN % 2 == 0, "gate/up pairs need an even number of 32-column blocks");
     static_assert(BM % 64 == 0 && BN % 64 == 0, "an even number of load instructions per wave");
     // two buffers of the A and B tiles, [rows][64] bf16 each
-    static_assert(NBB == 2 || NBB == 3, "two or three weight buffers");
-    // two buffers of the A tile and NBB of the B tile, [rows][64] bf16 each
+    static_assert((NBA == 2 || NBA == 3) && (NBB == 2 || NBB == 3) && NBA + NBB <= 5,
+                  "two buffers of each operand, or three of one");
+    // NBA buffers of the A tile and NBB of the B tile, [rows][64] bf16 each
     __shared__ __attribute__((aligned(16))) __bf16 sA0[BM * 64], sA1[BM * 64], sB0[BN * 64], sB1[BN * 64];
-    __shared__ __attribute__((aligned(16))) __bf16 sB2[NBB == 3 ? BN * 64 : 8];
-    // the split-tile arrival flag lives in sB2, which is idle from the end of
-    // a K loop until the first K tile of the next one (the next prologue loads
-    // sA0, sB0 and sB1 only), so that three 256 x 256 buffers fill the LDS
-    int* const s_last = (int*)sB2;
+    __shared__ __attribute__((aligned(16))) __bf16 sA2[NBA == 3 ? BM * 64 : 8], sB2[NBB == 3 ? BN * 64 : 8];
+    // the split-tile arrival flag lives in the third buffer (sB2 when there
+    // is none), which is idle from the end of a K loop until the first K tile
+    // of the next one (the next prologue loads the first two buffers only),
+    // so that three 256 x 256 buffers fill the LDS
+    int* const s_last = NBA == 3 ? (int*)sA2 : (int*)sB2;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
@@ -647,23 +651,25 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
         // idle buffer, never used.
         constexpr int NM = FM * FN, NR = FM + FN;
         constexpr int VMEM_READ = 0x020;
-        // wait at the end of a K tile: with three B buffers the B loads of the
-        // tile after next (the last BV loads issued) stay in flight
-        constexpr int KT_WAIT = NBB == 3 ? 0x0F70 | BV : 0x0F70;
-        static_assert(BV < 16, "vmcnt field");
+        // An operand with three buffers has its loads issued two K tiles
+        // ahead, and after the other operand's, so that at the end of a tile
+        // its last loads (the tile after next) may stay in flight while the
+        // wait covers everything the next tile reads.
+        constexpr int KT_WAIT = NBB == 3 ? 0x0F70 | BV : NBA == 3 ? 0x0F70 | AV : 0x0F70;
+        static_assert(AV < 16 && BV < 16, "vmcnt field");
         // one K tile: ca/cb hold it; na/nbn will hold the next tile's A and B;
-        // the A loads of tile kna and the B loads of tile knb (the next tile
-        // with two B buffers, the tile after next with three) go to na and nbl
-        auto ktile = [&](__bf16* ca, __bf16* cb, __bf16* na, __bf16* nbn, __bf16* nbl, int kna, int knb) {
-            dmaA(na, kna);
+        // the A loads of tile kna go to nal, the B loads of tile knb to nbl
+        auto ktile = [&](__bf16* ca, __bf16* cb, __bf16* na, __bf16* nbn, __bf16* nal, __bf16* nbl, int kna,
+                         int knb) __attribute__((always_inline)) {
+            if constexpr (NBA == 3) dmaB(nbl, knb); else dmaA(nal, kna);
             fload(ca, cb, 1, 1);
             mfmas(0);
-            sched_interleave<0, NM, NR, AV, VMEM_READ>();
+            sched_interleave<0, NM, NR, NBA == 3 ? BV : AV, VMEM_READ>();
             __builtin_amdgcn_sched_barrier(0);
-            dmaB(nbl, knb);
+            if constexpr (NBA == 3) dmaA(nal, kna); else dmaB(nbl, knb);
             fload(ca, cb, 2, 0);
             mfmas(1);
-            sched_interleave<0, NM, NR, BV, VMEM_READ>();
+            sched_interleave<0, NM, NR, NBA == 3 ? AV : BV, VMEM_READ>();
             __builtin_amdgcn_sched_barrier(0);
             fload(ca, cb, 3, 1);
             mfmas(0);
@@ -680,40 +686,57 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
         // Loads past the piece re-read its last K tile into an idle buffer.
         const int klast = kt_hi - 1;
         auto kc = [&](int k) { return (k < kt_hi ? k : klast) * BK; };
+        // buffers of the tile kt_lo + u of a pass (compile-time u)
+        auto bufA = [&](auto u) -> __bf16* {
+            constexpr int j = decltype(u)::value % NBA;
+            if constexpr (j == 0) return sA0; else if constexpr (j == 1) return sA1; else return sA2;
+        };
+        auto bufB = [&](auto u) -> __bf16* {
+            constexpr int j = decltype(u)::value % NBB;
+            if constexpr (j == 0) return sB0; else if constexpr (j == 1) return sB1; else return sB2;
+        };
+        using I0 = std::integral_constant<int, 0>;
+        using I1 = std::integral_constant<int, 1>;
         dmaA(sA0, kt_lo * BK);
         dmaB(sB0, kt_lo * BK);
+        if constexpr (NBA == 3) dmaA(sA1, kc(kt_lo + 1));
         if constexpr (NBB == 3) dmaB(sB1, kc(kt_lo + 1));
         __builtin_amdgcn_s_waitcnt(KT_WAIT);
         lds_barrier();
         fload(sA0, sB0, 0, 0);
         __builtin_amdgcn_sched_barrier(0);
-        if constexpr (NBB == 2) {
+        // tile kt + U of a pass
+        auto step = [&](auto u, int kt) __attribute__((always_inline)) {
+            constexpr int U = decltype(u)::value;
+            using N1 = std::integral_constant<int, U + 1>;
+            using LA = std::integral_constant<int, U + NBA - 1>;
+            using LB = std::integral_constant<int, U + NBB - 1>;
+            ktile(bufA(u), bufB(u), bufA(N1{}), bufB(N1{}), bufA(LA{}), bufB(LB{}), kc(kt + U + NBA - 1),
+                  kc(kt + U + NBB - 1));
+        };
+        if constexpr (NBA == 2 && NBB == 2) {
             for (int kt = kt_lo; kt < kt_hi; kt += 2) {
-                ktile(sA0, sB0, sA1, sB1, sB1, (kt + 1) * BK, (kt + 1) * BK);
-                ktile(sA1, sB1, sA0, sB0, sB0, kc(kt + 2), kc(kt + 2));
+                step(I0{}, kt);
+                step(I1{}, kt);
             }
         } else {
-            // A buffers alternate over two tiles, B buffers over three: six
-            // tiles per pass, leaving after any even number of them
+            // the buffers of one operand cycle over two tiles, of the other over
+            // three: six tiles per pass, then the two or four tiles left as the
+            // start of a pass
+            using I2 = std::integral_constant<int, 2>;
+            using I3 = std::integral_constant<int, 3>;
+            using I4 = std::integral_constant<int, 4>;
+            using I5 = std::integral_constant<int, 5>;
             int kt = kt_lo;
             for (; kt + 6 <= kt_hi; kt += 6) {
-                ktile(sA0, sB0, sA1, sB1, sB2, kc(kt + 1), kc(kt + 2));
-                ktile(sA1, sB1, sA0, sB2, sB0, kc(kt + 2), kc(kt + 3));
-                ktile(sA0, sB2, sA1, sB0, sB1, kc(kt + 3), kc(kt + 4));
-                ktile(sA1, sB0, sA0, sB1, sB2, kc(kt + 4), kc(kt + 5));
-                ktile(sA0, sB1, sA1, sB2, sB0, kc(kt + 5), kc(kt + 6));
-                ktile(sA1, sB2, sA0, sB0, sB1, kc(kt + 6), kc(kt + 7));
+                step(I0{}, kt); step(I1{}, kt); step(I2{}, kt);
+                step(I3{}, kt); step(I4{}, kt); step(I5{}, kt);
             }
-            // the remaining two or four tiles start a pass
             if (kt < kt_hi) {
-                ktile(sA0, sB0, sA1, sB1, sB2, kc(kt + 1), kc(kt + 2));
-                ktile(sA1, sB1, sA0, sB2, sB0, kc(kt + 2), kc(kt + 3));
-                if (kt + 2 < kt_hi) {
-                    ktile(sA0, sB2, sA1, sB0, sB1, kc(kt + 3), kc(kt + 4));
-                    ktile(sA1, sB0, sA0, sB1, sB2, kc(kt + 4), kc(kt + 5));
-                }
+                step(I0{}, kt); step(I1{}, kt);
+                if (kt + 2 < kt_hi) { step(I2{}, kt); step(I3{}, kt); }
             }
-            // B loads of the tile after the last may still be in flight
+            // loads of the tile after the last may still be in flight
             __builtin_amdgcn_s_waitcnt(0x0F70);
         }
 
@@ -1105,6 +1128,7 @@ __global__ void __launch_bounds__(256) combine_kernel(const CombineArgs c) {
 
 
 constexpr int GU_BM = 256, GU_BN = 256, DN_BM = 192, DN_BN = 256;   // bf16 GEMM tiles
+constexpr int DN_NBA = 2, DN_NBB = 3;   // down: LDS buffers of the activation and weight tiles
 constexpr int F32_BM = 64, F32_BN = 64;
 // bf16 batches of at most THIN_MAX_T tokens (every expert then has at most that
 // many rows) take the thin GEMM, THIN_PER_CU resident workgroups per CU
@@ -1213,7 +1237,7 @@ int launch_local_forward(const ForwardArgs& f, void* stream) {
     } else if (f.dtype == ORDERMOE_BF16) {
         {
         KernelTimer kt_("gemm_gate_up", st);
-        ggemm_bf16<GU_BM, GU_BN, 0, 3><<<dim3(bf16_grid(ub_gu)), dim3(256), 0, st>>>(g);
+        ggemm_bf16<GU_BM, GU_BN, 0, 2, 3><<<dim3(bf16_grid(ub_gu)), dim3(256), 0, st>>>(g);
         }
         if ((e = hipGetLastError()) != hipSuccess) return (int)e;
     } else {
@@ -1236,7 +1260,7 @@ int launch_local_forward(const ForwardArgs& f, void* stream) {
     } else if (f.dtype == ORDERMOE_BF16) {
         {
         KernelTimer kt_("gemm_down", st);
-        ggemm_bf16<DN_BM, DN_BN, 1, 3><<<dim3(bf16_grid(ub_dn)), dim3(256), 0, st>>>(g);
+        ggemm_bf16<DN_BM, DN_BN, 1, DN_NBA, DN_NBB><<<dim3(bf16_grid(ub_dn)), dim3(256), 0, st>>>(g);
         }
     } else {
         {
