@@ -393,7 +393,9 @@ __device__ inline int round_pos(int vid, int r, int n, int grid, bool spread) {
     return j < hi - lo ? lo + j : -1;
 }
 
-__device__ inline float silu_f(float g) { return g / (1.0f + __expf(-g)); }
+// silu(g) = g / (1 + e^-g), with the hardware reciprocal (1 ulp) instead of an
+// IEEE divide: the result is rounded to bf16 right after
+__device__ inline float silu_f(float g) { return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)); }
 
 // Workgroup barrier of the K loop.  __syncthreads() (and a workgroup fence on
 // LDS alone) waits for every outstanding load into LDS (vmcnt 0), which would
@@ -471,6 +473,8 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
     // of the next one (the next prologue loads the first two buffers only),
     // so that three 256 x 256 buffers fill the LDS
     int* const s_last = NBA == 3 ? (int*)sA2 : (int*)sB2;
+    // down: the gate weights of the tile's rows, for the epilogue
+    __shared__ float s_roww[MODE == 1 ? BM : 1];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
@@ -584,6 +588,16 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
                                      : (shared ? (const __bf16*)p.As : (const __bf16*)p.Ar + (size_t)L.rowbase * K);
         const __amdgpu_buffer_rsrc_t ra_rs =
             make_rsrc(Ab, MODE == 0 ? p.x_bytes : (uint32_t)((size_t)L.R * K * 2));
+        // down: thread tid_r < BM reads the gate weight of tile row tid_r now (one
+        // branch-free load, rows past the group read zero) and parks it in LDS
+        // after the K loop, so that the epilogue waits for no global load
+        float roww = 0.f;
+        if constexpr (MODE == 1) {
+            const __amdgpu_buffer_rsrc_t rw_rs = make_rsrc(p.row_w + L.rowbase, (uint32_t)L.R * 4u);
+            const int rr = L.m0 + tid_r;
+            roww = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                                 rw_rs, tid_r < BM && rr < L.R ? rr * 4 : (int)OOR, 0, 0));
+        }
         uint32_t aoff[AV];
 #pragma unroll
         for (int v = 0; v < AV; ++v) {
@@ -809,9 +823,15 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
         }
 
         // epilogue: element e of a 32x32 block is row (e/4)*8 + (lane_r/32)*4 + e%4,
-        // column lane_r%32
+        // column lane_r%32.  Down scales each row by its gate weight, parked in
+        // LDS by the workgroup (the barrier also orders it after the previous
+        // tile's reads, which precede this tile's K-loop barriers).
+        if constexpr (MODE == 1) {
+            if (tid_r < BM) s_roww[tid_r] = roww;
+            lds_barrier();
+        }
         const int rbase = L.m0 + wm_r * WM + (lane_r >> 5) * 4;
-        if (MODE == 0) {
+        if constexpr (MODE == 0) {
             __bf16* out = shared ? (__bf16*)p.Os : (__bf16*)p.Or;
             const int ldo = L.N / 2;
             const int orow0 = shared ? 0 : L.rowbase;
@@ -838,8 +858,8 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
 #pragma unroll
                 for (int e = 0; e < 16; ++e) {
                     const int row = rbase + i * 32 + (e >> 2) * 8 + (e & 3);
+                    const float wr = s_roww[row - L.m0];
                     if (row < L.R) {
-                        const float wr = p.row_w[L.rowbase + row];
 #pragma unroll
                         for (int j = 0; j < FN; ++j)
                             out[(size_t)(L.rowbase + row) * ldo + cbase + j * 32] = (__bf16)(acc[i][j][e] * wr);
@@ -1077,7 +1097,7 @@ __global__ void __launch_bounds__(256) ggemm_f32(const GemmArgs p) {
                 const int blk = c >> 5, cc = c & 31;
                 const float gv = sC[r][blk * 64 + cc], uv = sC[r][blk * 64 + 32 + cc];
                 const int orow = (shared ? 0 : L.rowbase) + row;
-                out[(int64_t)orow * ldo + L.n0 / 2 + c] = silu_f(gv) * uv;
+                out[(int64_t)orow * ldo + L.n0 / 2 + c] = gv / (1.0f + __expf(-gv)) * uv;   // fp32: IEEE divide
             }
             __syncthreads();
         }
