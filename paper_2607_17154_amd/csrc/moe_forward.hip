@@ -646,6 +646,26 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
 #pragma unroll
             for (int j = 0; j < FN; ++j) bfm[slot][j] = *(const bf16x8*)(sb + brow + j * 32 * 64 + pos);
         };
+        // the first sub-step's fragments after the barrier, in the order the
+        // MFMAs consume them (A0 B0, then B1.., then A1..), each read fenced so
+        // that the first MFMAs wait for their own operands only (the scheduler
+        // had issued B0 and B1 last, so every K tile began by waiting for seven
+        // of the eight reads)
+        auto fload_first = [&](const __bf16* sa, const __bf16* sb) {
+            const int pos = ((lane_r >> 5) ^ ((lane_r >> 1) & 7)) * 8;   // sub-step 0
+            af[0][0] = *(const bf16x8*)(sa + arow + pos);
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int j = 0; j < FN; ++j) {
+                bfm[0][j] = *(const bf16x8*)(sb + brow + j * 32 * 64 + pos);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+#pragma unroll
+            for (int i = 1; i < FM; ++i) {
+                af[0][i] = *(const bf16x8*)(sa + arow + i * 32 * 64 + pos);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        };
         auto mfmas = [&](int slot) {
 #pragma unroll
             for (int i = 0; i < FM; ++i)
@@ -693,7 +713,7 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
             __builtin_amdgcn_sched_barrier(0);
             __builtin_amdgcn_s_waitcnt(KT_WAIT);         // this wave_r's loads of the next tile are in LDS
             lds_barrier();
-            fload(na, nbn, 0, 0);
+            fload_first(na, nbn);
             __builtin_amdgcn_sched_barrier(0);
         };
         // the piece's K tiles [kt_lo, kt_hi): an even number (K units of 128).
@@ -717,7 +737,7 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
         if constexpr (NBB == 3) dmaB(sB1, kc(kt_lo + 1));
         __builtin_amdgcn_s_waitcnt(KT_WAIT);
         lds_barrier();
-        fload(sA0, sB0, 0, 0);
+        fload_first(sA0, sB0);
         __builtin_amdgcn_sched_barrier(0);
         // tile kt + U of a pass
         auto step = [&](auto u, int kt) __attribute__((always_inline)) {
