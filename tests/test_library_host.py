@@ -239,6 +239,18 @@ def test_device_entry_points_validate_before_launch():
     assert rc == om.EINVAL and "null pointer" in om.last_error()          # H > 1 needs every input
 
 
+@pytest.mark.parametrize("E", [129, 200, 256])
+def test_similarity_build_rejects_more_than_128_experts(E):
+    """The device build of eq 3-5 covers E <= 128 (its tile holds 128 experts);
+    routing accepts up to 256.  Between the two the build returns EINVAL with a
+    message naming the limit, before any pointer is looked at or anything is
+    launched (all pointers here are null)."""
+    rc = om.lib().ordermoe_build_similarity(None, 1024, 4096, None, E, om.BF16, 2, 0.7, 0.5,
+                                            *([None] * 9), None, 0, None)
+    assert rc == om.EINVAL
+    assert "[1, 128]" in om.last_error()
+
+
 def test_workspace_sizes_are_monotone():
     a = om.ordermoe_route_workspace_size(100, 2, 4)
     b = om.ordermoe_route_workspace_size(10000, 2, 4)
