@@ -397,6 +397,12 @@ __device__ inline int round_pos(int vid, int r, int n, int grid, bool spread) {
 // IEEE divide: the result is rounded to bf16 right after
 __device__ inline float silu_f(float g) { return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)); }
 
+// s_waitcnt operand on gfx9-class GPUs: vmcnt (6 bits, split), expcnt (left at
+// its maximum), lgkmcnt (4 bits)
+constexpr int waitcnt_enc(int vm, int lgkm) { return (vm & 0xF) | ((vm >> 4) << 14) | (7 << 4) | ((lgkm & 0xF) << 8); }
+// bf16 GEMMs: the K-tile barrier before the last sub-step (see the K loop)
+constexpr bool GEMM_EARLY_BARRIER = true;
+
 // Workgroup barrier of the K loop.  __syncthreads() (and a workgroup fence on
 // LDS alone) waits for every outstanding load into LDS (vmcnt 0), which would
 // also drain the loads of a buffer that is read only a tile later; this one
@@ -716,6 +722,40 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
             fload_first(na, nbn);
             __builtin_amdgcn_sched_barrier(0);
         };
+        // Two A buffers and three B buffers (both GEMMs): the barrier of K tile
+        // t sits before its last sub-step.  Sub-step 0 issues the B loads of
+        // tile t + 2 (into the buffer tile t - 1 read, free since barrier t - 1);
+        // after sub-step 2 every fragment of tile t has been read, so the wave
+        // waits for its own loads of tile t + 1 (everything but the B loads
+        // just issued) and its reads, and the barrier follows; sub-step 3's
+        // MFMAs then overlap the first fragment reads of tile t + 1 and the A
+        // loads of tile t + 2 into the A buffer tile t has just finished with.
+        // The A loads keep a lead of four sub-steps, the B loads of seven; no
+        // tile starts by waiting for its first fragments.
+        constexpr bool EARLY = NBA == 2 && NBB == 3 && GEMM_EARLY_BARRIER;
+        auto ktile_early = [&](__bf16* ca, __bf16* cb, __bf16* na, __bf16* nbn, __bf16* nbl, int kn2)
+                               __attribute__((always_inline)) {
+            dmaB(nbl, kn2);
+            fload(ca, cb, 1, 1);
+            mfmas(0);
+            sched_interleave<0, NM, NR, BV, VMEM_READ>();
+            __builtin_amdgcn_sched_barrier(0);
+            fload(ca, cb, 2, 0);
+            mfmas(1);
+            sched_interleave<0, NM, NR, 0, VMEM_READ>();
+            __builtin_amdgcn_sched_barrier(0);
+            fload(ca, cb, 3, 1);
+            mfmas(0);
+            sched_interleave<0, NM, NR, 0, VMEM_READ>();
+            __builtin_amdgcn_sched_barrier(0);
+            __builtin_amdgcn_s_waitcnt(waitcnt_enc(BV, 0));
+            lds_barrier();
+            dmaA(ca, kn2);
+            fload(na, nbn, 0, 0);
+            mfmas(1);
+            sched_interleave<0, NM, NR, AV, VMEM_READ>();
+            __builtin_amdgcn_sched_barrier(0);
+        };
         // the piece's K tiles [kt_lo, kt_hi): an even number (K units of 128).
         // Loads past the piece re-read its last K tile into an idle buffer.
         const int klast = kt_hi - 1;
@@ -735,7 +775,12 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
         dmaB(sB0, kt_lo * BK);
         if constexpr (NBA == 3) dmaA(sA1, kc(kt_lo + 1));
         if constexpr (NBB == 3) dmaB(sB1, kc(kt_lo + 1));
-        __builtin_amdgcn_s_waitcnt(KT_WAIT);
+        if constexpr (EARLY) {
+            dmaA(sA1, kc(kt_lo + 1));
+            __builtin_amdgcn_s_waitcnt(waitcnt_enc(AV + BV, 15));   // tile kt_lo's loads are in LDS
+        } else {
+            __builtin_amdgcn_s_waitcnt(KT_WAIT);
+        }
         lds_barrier();
         fload_first(sA0, sB0);
         __builtin_amdgcn_sched_barrier(0);
@@ -745,8 +790,13 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
             using N1 = std::integral_constant<int, U + 1>;
             using LA = std::integral_constant<int, U + NBA - 1>;
             using LB = std::integral_constant<int, U + NBB - 1>;
-            ktile(bufA(u), bufB(u), bufA(N1{}), bufB(N1{}), bufA(LA{}), bufB(LB{}), kc(kt + U + NBA - 1),
-                  kc(kt + U + NBB - 1));
+            if constexpr (EARLY) {
+                using N2 = std::integral_constant<int, U + 2>;
+                ktile_early(bufA(u), bufB(u), bufA(N1{}), bufB(N1{}), bufB(N2{}), kc(kt + U + 2));
+            } else {
+                ktile(bufA(u), bufB(u), bufA(N1{}), bufB(N1{}), bufA(LA{}), bufB(LB{}), kc(kt + U + NBA - 1),
+                      kc(kt + U + NBB - 1));
+            }
         };
         if constexpr (NBA == 2 && NBB == 2) {
             for (int kt = kt_lo; kt < kt_hi; kt += 2) {
