@@ -191,52 +191,83 @@ __global__ void __launch_bounds__(ST_THREADS, 1) sim_tile_kernel(const SimArgs a
         // activation counts: top-k of each token's logits, ties to the lower
         // index.  Two threads per token: lanes l and l + 32 of wave w take token
         // 32 w + l % 32, the first scanning experts 0..63, the second 64..127.
-        // Each keeps a sorted top list in registers by a branch-free insertion
-        // network: the incoming logit moves down the list past every entry it
-        // does not exceed, so an equal logit never passes one of lower index.
-        // The lower half then inserts the upper half's list, whose indices are
-        // all higher, in its sorted order.
+        // A logit and its expert form one 64-bit key (order-preserving bits of
+        // the logit, -0 as +0, then 0xFFFF - expert), so that a larger key is a
+        // larger logit or, on equal logits, the lower index; -inf, NaN and the
+        // padding past E get key 0 and are never counted.  Each thread keeps
+        // its top eight keys sorted: every batch of eight logits is sorted by a
+        // 19-comparator network and merged in (the elementwise larger of the
+        // list and the reversed batch is bitonic and holds the top eight; three
+        // half-cleaner stages sort it).  The two halves' lists merge the same
+        // way.
         {
             constexpr int MK = ORDERMOE_MAX_TOPK;
-            const int tt = wave * 32 + (lane & 31);
-            const int half = lane >> 5;
-            float tv[MK];
-            int te[MK];
+            static_assert(MK == 8, "the sorting networks are for eight keys");
+            // the lane index passes through an empty asm, so that the token's
+            // addresses are formed here rather than held across the tile loop
+            int lane_t = lane;
+            asm volatile("" : "+v"(lane_t));
+            const int tt = wave * 32 + (lane_t & 31);
+            const int half = lane_t >> 5;
+            auto cx = [](uint64_t& x, uint64_t& y) {          // x <- larger, y <- smaller
+                const bool c = x < y;
+                const uint64_t hi = c ? y : x, lo = c ? x : y;
+                x = hi;
+                y = lo;
+            };
+            auto sort8 = [&](uint64_t* s) {
+                cx(s[0], s[1]); cx(s[2], s[3]); cx(s[4], s[5]); cx(s[6], s[7]);
+                cx(s[0], s[2]); cx(s[1], s[3]); cx(s[4], s[6]); cx(s[5], s[7]);
+                cx(s[1], s[2]); cx(s[5], s[6]);
+                cx(s[0], s[4]); cx(s[1], s[5]); cx(s[2], s[6]); cx(s[3], s[7]);
+                cx(s[2], s[4]); cx(s[3], s[5]);
+                cx(s[1], s[2]); cx(s[3], s[4]); cx(s[5], s[6]);
+            };
+            // L <- top eight of L and S, both sorted in descending order
+            auto merge8 = [&](uint64_t* L, const uint64_t* S) {
 #pragma unroll
-            for (int r = 0; r < MK; ++r) { tv[r] = -__builtin_inff(); te[r] = -1; }
-            auto insert = [&](float v, int e) {
-#pragma unroll
-                for (int r = 0; r < MK; ++r) {
-                    const bool c = v > tv[r];
-                    const float kv = c ? v : tv[r];
-                    const int ke = c ? e : te[r];
-                    v = c ? tv[r] : v;
-                    e = c ? te[r] : e;
-                    tv[r] = kv;
-                    te[r] = ke;
-                }
+                for (int r = 0; r < 8; ++r) L[r] = L[r] > S[7 - r] ? L[r] : S[7 - r];
+                cx(L[0], L[4]); cx(L[1], L[5]); cx(L[2], L[6]); cx(L[3], L[7]);
+                cx(L[0], L[2]); cx(L[1], L[3]); cx(L[4], L[6]); cx(L[5], L[7]);
+                cx(L[0], L[1]); cx(L[2], L[3]); cx(L[4], L[5]); cx(L[6], L[7]);
+            };
+            auto key = [&](float v, int e) -> uint64_t {
+                const bool keep = e < E && v > -__builtin_inff();          // false for NaN too
+                const uint32_t u = __float_as_uint(v == 0.f ? 0.f : v);
+                const uint32_t o = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+                return keep ? ((uint64_t)o << 32) | (uint32_t)(0xFFFF - e) : 0ull;
             };
             const float* row = sH + (tt < nt ? tt : 0) * ST_LDH + half * (SIM_EMAX / 2);
-#pragma unroll 2
-            for (int e4 = 0; e4 < SIM_EMAX / 2; e4 += 4) {
-                const f32x4 v4 = *(const f32x4*)(row + e4);
+            const int e0 = half * (SIM_EMAX / 2);
+            uint64_t L[8], S[8];
+            auto batch = [&](int b) {
+                const f32x4 v0 = *(const f32x4*)(row + 8 * b), v1 = *(const f32x4*)(row + 8 * b + 4);
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
-                    const int e = half * (SIM_EMAX / 2) + e4 + q;
-                    insert(e < E ? v4[q] : -__builtin_inff(), e);   // padding: never kept
+                    S[q] = key(v0[q], e0 + 8 * b + q);
+                    S[4 + q] = key(v1[q], e0 + 8 * b + 4 + q);
                 }
+                sort8(S);
+            };
+            batch(0);
+#pragma unroll
+            for (int r = 0; r < 8; ++r) L[r] = S[r];
+#pragma unroll 1
+            for (int b = 1; b < SIM_EMAX / 2 / 8; ++b) {
+                batch(b);
+                merge8(L, S);
             }
-            float pv[MK];
-            int pe[MK];
 #pragma unroll
-            for (int r = 0; r < MK; ++r) { pv[r] = __shfl_xor(tv[r], 32); pe[r] = __shfl_xor(te[r], 32); }
-#pragma unroll
-            for (int r = 0; r < MK; ++r) insert(pv[r], pe[r]);
+            for (int r = 0; r < 8; ++r) {
+                const uint32_t lo = (uint32_t)L[r], hi = (uint32_t)(L[r] >> 32);
+                S[r] = ((uint64_t)(uint32_t)__shfl_xor((int)hi, 32) << 32) | (uint32_t)__shfl_xor((int)lo, 32);
+            }
+            merge8(L, S);
             if (half == 0 && tt < nt) {
-                if (a.top1) a.top1[t0 + tt] = te[0];
+                if (a.top1) a.top1[t0 + tt] = L[0] ? (int)(0xFFFFu - (uint32_t)(L[0] & 0xFFFFu)) : -1;
 #pragma unroll
                 for (int r = 0; r < MK; ++r)
-                    if (r < a.k && te[r] >= 0) atomicAdd(&s_cnt[te[r]], 1);
+                    if (r < a.k && L[r]) atomicAdd(&s_cnt[0xFFFFu - (uint32_t)(L[r] & 0xFFFFu)], 1);
             }
         }
         __syncthreads();   // the top-k is done with the fp32 H tile
