@@ -400,8 +400,6 @@ __device__ inline float silu_f(float g) { return g * __builtin_amdgcn_rcpf(1.0f 
 // s_waitcnt operand on gfx9-class GPUs: vmcnt (6 bits, split), expcnt (left at
 // its maximum), lgkmcnt (4 bits)
 constexpr int waitcnt_enc(int vm, int lgkm) { return (vm & 0xF) | ((vm >> 4) << 14) | (7 << 4) | ((lgkm & 0xF) << 8); }
-// bf16 GEMMs: the K-tile barrier before the last sub-step (see the K loop)
-constexpr bool GEMM_EARLY_BARRIER = true;
 
 // Workgroup barrier of the K loop.  __syncthreads() (and a workgroup fence on
 // LDS alone) waits for every outstanding load into LDS (vmcnt 0), which would
@@ -459,7 +457,7 @@ __device__ inline void sched_interleave() {
 // arrival completes the tile's counter sums the tile's pieces in K order (so
 // the result does not depend on who is last) and runs the epilogue.  No
 // workgroup waits for another.
-template <int BM, int BN, int MODE, int NBA, int NBB>
+template <int BM, int BN, int MODE>
 __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
     constexpr int BK = 64;
     constexpr int WM = BM / 2, WN = BN / 2;
@@ -469,16 +467,13 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
     static_assert(FN % 2 == 0, "gate/up pairs need an even number of 32-column blocks");
     static_assert(BM % 64 == 0 && BN % 64 == 0, "an even number of load instructions per wave");
     // two buffers of the A and B tiles, [rows][64] bf16 each
-    static_assert((NBA == 2 || NBA == 3) && (NBB == 2 || NBB == 3) && NBA + NBB <= 5,
-                  "two buffers of each operand, or three of one");
-    // NBA buffers of the A tile and NBB of the B tile, [rows][64] bf16 each
+    // two buffers of the A tile and three of the B tile, [rows][64] bf16 each
     __shared__ __attribute__((aligned(16))) __bf16 sA0[BM * 64], sA1[BM * 64], sB0[BN * 64], sB1[BN * 64];
-    __shared__ __attribute__((aligned(16))) __bf16 sA2[NBA == 3 ? BM * 64 : 8], sB2[NBB == 3 ? BN * 64 : 8];
-    // the split-tile arrival flag lives in the third buffer (sB2 when there
-    // is none), which is idle from the end of a K loop until the first K tile
-    // of the next one (the next prologue loads the first two buffers only),
-    // so that three 256 x 256 buffers fill the LDS
-    int* const s_last = NBA == 3 ? (int*)sA2 : (int*)sB2;
+    __shared__ __attribute__((aligned(16))) __bf16 sB2[BN * 64];
+    // the split-tile arrival flag lives in sB2, which is idle from the end of a
+    // K loop until the first K tile of the next one (a prologue loads sA0, sA1,
+    // sB0 and sB1 only), so that the buffers of 256 x 256 tiles fill the LDS
+    int* const s_last = (int*)sB2;
     // down: the gate weights of the tile's rows, for the epilogue
     __shared__ float s_roww[MODE == 1 ? BM : 1];
 
@@ -679,62 +674,26 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
                 for (int j = 0; j < FN; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[slot][i], bfm[slot][j], acc[i][j], 0, 0, 0);
         };
-        // Each K tile of 64 is four MFMA sub-steps of 16.  The next K tile's
-        // loads are issued into the idle buffer during the first two sub-steps
-        // (A, then B: the gathered token rows first, 2-3% faster than the
-        // other order), a whole K tile ahead of their use; every sub-step also
-        // reads the fragments of the next one.  A K tile ends with the wait
-        // for this wave_r's loads and the barrier for everyone's.  The two
-        // buffers are separate LDS arrays and the loop is unrolled by two, so
-        // that the loads into one buffer are never taken to alias the reads of
-        // the other.  After the last tile the last K tile is re-read into the
-        // idle buffer, never used.
+        // Each K tile of 64 is four MFMA sub-steps of 16; every sub-step reads
+        // the fragments of the next one.  The buffers are separate LDS arrays
+        // and the loop is unrolled over a pass of six tiles (A cycles over two
+        // buffers, B over three), so that every access names a fixed array and
+        // the loads into one buffer are never taken to alias the reads of
+        // another.  The barrier of K tile t sits before its last sub-step.
+        // Sub-step 0 issues the B loads of tile t + 2 (into the buffer tile
+        // t - 1 read, free since barrier t - 1); after sub-step 2 every fragment
+        // of tile t has been read, so the wave waits for its own loads of tile
+        // t + 1 (everything but the B loads just issued) and its reads, and the
+        // barrier follows; sub-step 3's MFMAs then overlap the first fragment
+        // reads of tile t + 1 and the A loads of tile t + 2 into the A buffer
+        // tile t has just finished with.  The A loads keep a lead of four
+        // sub-steps, the B loads of seven; no tile starts by waiting for its
+        // first fragments.  Loads past the piece re-read its last K tile into
+        // an idle buffer.
         constexpr int NM = FM * FN, NR = FM + FN;
         constexpr int VMEM_READ = 0x020;
-        // An operand with three buffers has its loads issued two K tiles
-        // ahead, and after the other operand's, so that at the end of a tile
-        // its last loads (the tile after next) may stay in flight while the
-        // wait covers everything the next tile reads.
-        constexpr int KT_WAIT = NBB == 3 ? 0x0F70 | BV : NBA == 3 ? 0x0F70 | AV : 0x0F70;
-        static_assert(AV < 16 && BV < 16, "vmcnt field");
-        // one K tile: ca/cb hold it; na/nbn will hold the next tile's A and B;
-        // the A loads of tile kna go to nal, the B loads of tile knb to nbl
-        auto ktile = [&](__bf16* ca, __bf16* cb, __bf16* na, __bf16* nbn, __bf16* nal, __bf16* nbl, int kna,
-                         int knb) __attribute__((always_inline)) {
-            if constexpr (NBA == 3) dmaB(nbl, knb); else dmaA(nal, kna);
-            fload(ca, cb, 1, 1);
-            mfmas(0);
-            sched_interleave<0, NM, NR, NBA == 3 ? BV : AV, VMEM_READ>();
-            __builtin_amdgcn_sched_barrier(0);
-            if constexpr (NBA == 3) dmaA(nal, kna); else dmaB(nbl, knb);
-            fload(ca, cb, 2, 0);
-            mfmas(1);
-            sched_interleave<0, NM, NR, NBA == 3 ? AV : BV, VMEM_READ>();
-            __builtin_amdgcn_sched_barrier(0);
-            fload(ca, cb, 3, 1);
-            mfmas(0);
-            sched_interleave<0, NM, NR, 0, VMEM_READ>();
-            __builtin_amdgcn_sched_barrier(0);
-            mfmas(1);
-            __builtin_amdgcn_sched_barrier(0);
-            __builtin_amdgcn_s_waitcnt(KT_WAIT);         // this wave_r's loads of the next tile are in LDS
-            lds_barrier();
-            fload_first(na, nbn);
-            __builtin_amdgcn_sched_barrier(0);
-        };
-        // Two A buffers and three B buffers (both GEMMs): the barrier of K tile
-        // t sits before its last sub-step.  Sub-step 0 issues the B loads of
-        // tile t + 2 (into the buffer tile t - 1 read, free since barrier t - 1);
-        // after sub-step 2 every fragment of tile t has been read, so the wave
-        // waits for its own loads of tile t + 1 (everything but the B loads
-        // just issued) and its reads, and the barrier follows; sub-step 3's
-        // MFMAs then overlap the first fragment reads of tile t + 1 and the A
-        // loads of tile t + 2 into the A buffer tile t has just finished with.
-        // The A loads keep a lead of four sub-steps, the B loads of seven; no
-        // tile starts by waiting for its first fragments.
-        constexpr bool EARLY = NBA == 2 && NBB == 3 && GEMM_EARLY_BARRIER;
-        auto ktile_early = [&](__bf16* ca, __bf16* cb, __bf16* na, __bf16* nbn, __bf16* nbl, int kn2)
-                               __attribute__((always_inline)) {
+        auto ktile = [&](__bf16* ca, __bf16* cb, __bf16* na, __bf16* nbn, __bf16* nbl, int kn2)
+                         __attribute__((always_inline)) {
             dmaB(nbl, kn2);
             fload(ca, cb, 1, 1);
             mfmas(0);
@@ -756,73 +715,49 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
             sched_interleave<0, NM, NR, AV, VMEM_READ>();
             __builtin_amdgcn_sched_barrier(0);
         };
-        // the piece's K tiles [kt_lo, kt_hi): an even number (K units of 128).
-        // Loads past the piece re-read its last K tile into an idle buffer.
+        // the piece's K tiles [kt_lo, kt_hi): an even number (K units of 128)
         const int klast = kt_hi - 1;
         auto kc = [&](int k) { return (k < kt_hi ? k : klast) * BK; };
-        // buffers of the tile kt_lo + u of a pass (compile-time u)
-        auto bufA = [&](auto u) -> __bf16* {
-            constexpr int j = decltype(u)::value % NBA;
-            if constexpr (j == 0) return sA0; else if constexpr (j == 1) return sA1; else return sA2;
-        };
+        // buffers of tile kt + u of a pass (compile-time u)
+        auto bufA = [&](auto u) -> __bf16* { return decltype(u)::value % 2 == 0 ? sA0 : sA1; };
         auto bufB = [&](auto u) -> __bf16* {
-            constexpr int j = decltype(u)::value % NBB;
+            constexpr int j = decltype(u)::value % 3;
             if constexpr (j == 0) return sB0; else if constexpr (j == 1) return sB1; else return sB2;
         };
-        using I0 = std::integral_constant<int, 0>;
-        using I1 = std::integral_constant<int, 1>;
+        // prologue: tiles kt_lo and kt_lo + 1 of both operands
         dmaA(sA0, kt_lo * BK);
         dmaB(sB0, kt_lo * BK);
-        if constexpr (NBA == 3) dmaA(sA1, kc(kt_lo + 1));
-        if constexpr (NBB == 3) dmaB(sB1, kc(kt_lo + 1));
-        if constexpr (EARLY) {
-            dmaA(sA1, kc(kt_lo + 1));
-            __builtin_amdgcn_s_waitcnt(waitcnt_enc(AV + BV, 15));   // tile kt_lo's loads are in LDS
-        } else {
-            __builtin_amdgcn_s_waitcnt(KT_WAIT);
-        }
+        dmaB(sB1, kc(kt_lo + 1));
+        dmaA(sA1, kc(kt_lo + 1));
+        static_assert(AV + BV < 64, "vmcnt field");
+        __builtin_amdgcn_s_waitcnt(waitcnt_enc(AV + BV, 15));   // tile kt_lo's loads are in LDS
         lds_barrier();
         fload_first(sA0, sB0);
         __builtin_amdgcn_sched_barrier(0);
-        // tile kt + U of a pass
         auto step = [&](auto u, int kt) __attribute__((always_inline)) {
             constexpr int U = decltype(u)::value;
             using N1 = std::integral_constant<int, U + 1>;
-            using LA = std::integral_constant<int, U + NBA - 1>;
-            using LB = std::integral_constant<int, U + NBB - 1>;
-            if constexpr (EARLY) {
-                using N2 = std::integral_constant<int, U + 2>;
-                ktile_early(bufA(u), bufB(u), bufA(N1{}), bufB(N1{}), bufB(N2{}), kc(kt + U + 2));
-            } else {
-                ktile(bufA(u), bufB(u), bufA(N1{}), bufB(N1{}), bufA(LA{}), bufB(LB{}), kc(kt + U + NBA - 1),
-                      kc(kt + U + NBB - 1));
-            }
+            using N2 = std::integral_constant<int, U + 2>;
+            ktile(bufA(u), bufB(u), bufA(N1{}), bufB(N1{}), bufB(N2{}), kc(kt + U + 2));
         };
-        if constexpr (NBA == 2 && NBB == 2) {
-            for (int kt = kt_lo; kt < kt_hi; kt += 2) {
-                step(I0{}, kt);
-                step(I1{}, kt);
-            }
-        } else {
-            // the buffers of one operand cycle over two tiles, of the other over
-            // three: six tiles per pass, then the two or four tiles left as the
-            // start of a pass
-            using I2 = std::integral_constant<int, 2>;
-            using I3 = std::integral_constant<int, 3>;
-            using I4 = std::integral_constant<int, 4>;
-            using I5 = std::integral_constant<int, 5>;
-            int kt = kt_lo;
-            for (; kt + 6 <= kt_hi; kt += 6) {
-                step(I0{}, kt); step(I1{}, kt); step(I2{}, kt);
-                step(I3{}, kt); step(I4{}, kt); step(I5{}, kt);
-            }
-            if (kt < kt_hi) {
-                step(I0{}, kt); step(I1{}, kt);
-                if (kt + 2 < kt_hi) { step(I2{}, kt); step(I3{}, kt); }
-            }
-            // loads of the tile after the last may still be in flight
-            __builtin_amdgcn_s_waitcnt(0x0F70);
+        using I0 = std::integral_constant<int, 0>;
+        using I1 = std::integral_constant<int, 1>;
+        using I2 = std::integral_constant<int, 2>;
+        using I3 = std::integral_constant<int, 3>;
+        using I4 = std::integral_constant<int, 4>;
+        using I5 = std::integral_constant<int, 5>;
+        int kt = kt_lo;
+        for (; kt + 6 <= kt_hi; kt += 6) {
+            step(I0{}, kt); step(I1{}, kt); step(I2{}, kt);
+            step(I3{}, kt); step(I4{}, kt); step(I5{}, kt);
         }
+        // the two or four tiles left start a pass
+        if (kt < kt_hi) {
+            step(I0{}, kt); step(I1{}, kt);
+            if (kt + 2 < kt_hi) { step(I2{}, kt); step(I3{}, kt); }
+        }
+        // loads of the tiles after the last may still be in flight
+        __builtin_amdgcn_s_waitcnt(0x0F70);
 
         if (nseg > 1) {
             // a piece of a split tile: its partial sums go to slot j sstride + ctr
@@ -1218,7 +1153,6 @@ __global__ void __launch_bounds__(256) combine_kernel(const CombineArgs c) {
 
 
 constexpr int GU_BM = 256, GU_BN = 256, DN_BM = 192, DN_BN = 256;   // bf16 GEMM tiles
-constexpr int DN_NBA = 2, DN_NBB = 3;   // down: LDS buffers of the activation and weight tiles
 constexpr int F32_BM = 64, F32_BN = 64;
 // bf16 batches of at most THIN_MAX_T tokens (every expert then has at most that
 // many rows) take the thin GEMM, THIN_PER_CU resident workgroups per CU
@@ -1327,7 +1261,7 @@ int launch_local_forward(const ForwardArgs& f, void* stream) {
     } else if (f.dtype == ORDERMOE_BF16) {
         {
         KernelTimer kt_("gemm_gate_up", st);
-        ggemm_bf16<GU_BM, GU_BN, 0, 2, 3><<<dim3(bf16_grid(ub_gu)), dim3(256), 0, st>>>(g);
+        ggemm_bf16<GU_BM, GU_BN, 0><<<dim3(bf16_grid(ub_gu)), dim3(256), 0, st>>>(g);
         }
         if ((e = hipGetLastError()) != hipSuccess) return (int)e;
     } else {
@@ -1350,7 +1284,7 @@ int launch_local_forward(const ForwardArgs& f, void* stream) {
     } else if (f.dtype == ORDERMOE_BF16) {
         {
         KernelTimer kt_("gemm_down", st);
-        ggemm_bf16<DN_BM, DN_BN, 1, DN_NBA, DN_NBB><<<dim3(bf16_grid(ub_dn)), dim3(256), 0, st>>>(g);
+        ggemm_bf16<DN_BM, DN_BN, 1><<<dim3(bf16_grid(ub_dn)), dim3(256), 0, st>>>(g);
         }
     } else {
         {
