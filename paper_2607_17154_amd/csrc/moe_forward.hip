@@ -53,6 +53,7 @@ constexpr int MAXR = ORDERMOE_MAX_TOPK + 1;   // rows per token (routed + shared
 // SK_SPLIT pieces (the last arrival reads them all).
 constexpr int SK_MAX_GRID = 256;
 constexpr int SK_SPLIT = 4;
+constexpr int SK_MIN_PIECE_KT = 16;   // K tiles of 64 per piece, at least
 
 struct RowsArgs {
     int64_t T;
@@ -512,6 +513,10 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
     int split = left > 0 ? grid / left : 0;
     if (split > SK_SPLIT) split = SK_SPLIT;
     if (split > p.Kr / (2 * BK)) split = p.Kr / (2 * BK);
+    // a piece keeps at least SK_MIN_PIECE_KT K tiles: shorter pieces cost more
+    // in partial-tile stores and fix-up reads than the idle workgroups they
+    // fill, most of all when another batch's kernels can take those CUs
+    if (split > p.Kr / BK / SK_MIN_PIECE_KT) split = p.Kr / BK / SK_MIN_PIECE_KT;
     if (p.G > p.n_routed && p.Ks != p.Kr) split = 1;
     // slots of the pieces of one split tile lie sstride apart
     const int sstride = sh_split ? nsh : left;

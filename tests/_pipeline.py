@@ -291,8 +291,9 @@ def with_horizon(sc: StreamCase, H: int, allow_sub: Optional[int] = None) -> Str
 # The bf16 grouped GEMMs of the local forward (batches above 128 tokens) run
 # 256 x 256 gate/up tiles and 192 x 256 down tiles over a persistent grid of at
 # most 256 workgroups (one per CU on MI355X, at most four per tile); the tiles
-# left after whole rounds are cut along K into up to 4 pieces when at least two
-# workgroups per tile are free and every group has the same K.  Tests use this
+# left after whole rounds are cut along K into up to 4 pieces of at least 16 K
+# tiles of 64 when at least two workgroups per tile are free and every group
+# has the same K.  Tests use this
 # mirror to know which of their shapes exercise the split.
 def gemm_plan(cfg, rows, n_local: int, cus: int = 256):
     """rows: the forward's row_offsets output [n_local + 2].  Returns
@@ -319,7 +320,7 @@ def gemm_plan(cfg, rows, n_local: int, cus: int = 256):
         items = tiles + nsh * halves
         rounds = items // grid
         left = items - rounds * grid
-        split = min(grid // left, 4, Kr // 128) if left else 0
+        split = min(grid // left, 4, Kr // 128, Kr // 64 // 16) if left else 0
         if has_sh and Ks != Kr:
             split = 1
         return tiles, grid, rounds, left, split, halves

@@ -44,17 +44,18 @@ SMALL = {
     "C4s_M12": wl.C4.with_(T=1700, T_cal=4096, M=12, capacity=(8.0,) * 12, loc_mode="uniform"),
     "C4s_M16": wl.C4.with_(T=1700, T_cal=4096, M=16, capacity=(8.0,) * 16, loc_mode="uniform"),
     "Cmax": CMAX,
-    # the leftover-tile split along K in both GEMMs, with one shared expert (so
-    # the down projection's shared tiles have the routed K and split too): 4
-    # pieces with no whole round, and 3 pieces
-    "C3split": wl.C3.with_(T=600, d=1024, f=512, n_shared=1, T_cal=4096),
-    "C4split": wl.C4.with_(T=1200, d=1024, f=768, n_shared=1, T_cal=4096),
+    # the leftover-tile split along K (pieces of at least 16 K tiles), with one
+    # shared expert so that the down projection's shared tiles have the routed K
+    # and split too: the down projection in 2 pieces with no whole round (128
+    # tiles), and the gate/up projection in 2 pieces after a whole round (312)
+    "C3split": wl.C3.with_(T=600, d=2048, f=2048, n_shared=1, T_cal=4096),
+    "C4split": wl.C4.with_(T=1200, d=2048, f=3072, n_shared=1, T_cal=4096),
     # four shared experts: the down projection's shared K is four times the
     # routed K, so its shared tiles are cut into two K halves
     "C3sh": wl.C3.with_(T=600, d=1024, f=512, n_shared=4, T_cal=4096),
 }
 # shapes whose GEMM plan splits leftover tiles along K (checked on the GPU's rows)
-SPLIT = {"C3split": {"gate_up": 4, "down": 4}, "C4split": {"gate_up": 3, "down": 3},
+SPLIT = {"C3split": {"gate_up": 0, "down": 2}, "C4split": {"gate_up": 2, "down": 1},
          "C2": {"gate_up": 2}, "C2x": {"gate_up": 3}}
 # shapes whose down projection cuts its shared tiles into two K halves
 SHARED_HALVES = {"C3sh", "C3"}
