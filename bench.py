@@ -133,7 +133,7 @@ def _setup(cfg, torch, om):
         g, u, dn = wl.expert(cfg, j)
         gd, ud = up(g), up(u)
         om.ordermoe_pack_gate_up(gd.unsqueeze(0), ud.unsqueeze(0), w_gu[i:i + 1])
-        w_dn[i] = up(dn)
+        om.ordermoe_pack_down(up(dn).unsqueeze(0), w_dn[i:i + 1])
         del gd, ud
     w_sh_gu = w_sh_dn = None
     if cfg.n_shared:
@@ -142,8 +142,10 @@ def _setup(cfg, torch, om):
         su = torch.cat([up(a[1]) for a in sh], 0).unsqueeze(0).contiguous()
         w_sh_gu = torch.empty((1, 2 * cfg.n_shared * cfg.f, cfg.d), dtype=tdt, device=dev)
         om.ordermoe_pack_gate_up(sg, su, w_sh_gu)
-        w_sh_dn = torch.cat([up(a[2]) for a in sh], 1).contiguous()
-        del sg, su
+        sd = torch.cat([up(a[2]) for a in sh], 1).unsqueeze(0).contiguous()
+        w_sh_dn = torch.empty_like(sd)
+        om.ordermoe_pack_down(sd, w_sh_dn)
+        del sg, su, sd
     experts = om.make_experts(code, cfg.d, cfg.f, cfg.E, local, w_gu, w_dn, cfg.n_shared, w_sh_gu, w_sh_dn)
     X = wl.tokens(cfg)
     st = dict(layer=layer, experts=experts, keep=(w_router, tabs_dev, w_gu, w_dn, w_sh_gu, w_sh_dn), local=local,
@@ -410,13 +412,19 @@ def _quality_sweep(torch, om):
     w_gu_all = torch.empty((E, 2 * f, d), dtype=bf, device=dev)
     om.ordermoe_pack_gate_up(g, u, w_gu_all)
     del g, u
-    w_dn_all = torch.randn((E, d, f), generator=gen, device=dev, dtype=bf) * 0.02
+    dn = torch.randn((E, d, f), generator=gen, device=dev, dtype=bf) * 0.02
+    w_dn_all = torch.empty_like(dn)
+    om.ordermoe_pack_down(dn, w_dn_all)
+    del dn
     sg = torch.randn((1, nsh * f, d), generator=gen, device=dev, dtype=bf) * 0.02
     su = torch.randn((1, nsh * f, d), generator=gen, device=dev, dtype=bf) * 0.02
     w_sh_gu = torch.empty((1, 2 * nsh * f, d), dtype=bf, device=dev)
     om.ordermoe_pack_gate_up(sg, su, w_sh_gu)
     del sg, su
-    w_sh_dn = torch.randn((d, nsh * f), generator=gen, device=dev, dtype=bf) * 0.02
+    sd = torch.randn((1, d, nsh * f), generator=gen, device=dev, dtype=bf) * 0.02
+    w_sh_dn = torch.empty_like(sd)
+    om.ordermoe_pack_down(sd, w_sh_dn)
+    del sd
     servers = []
     for m in range(M):
         local = [int(j) for j in np.nonzero(x_dep[m])[0]]
@@ -834,7 +842,10 @@ def _decode_stream(torch, om, steps: int = 10, warmup: int = 2):
         w_gu = torch.empty((n, 2 * cfg.f, cfg.d), dtype=torch.bfloat16, device=dev)
         om.ordermoe_pack_gate_up(g, u, w_gu)
         del g, u
-        w_dn = torch.randn((n, cfg.d, cfg.f), generator=gen, device=dev, dtype=torch.bfloat16) * 0.02
+        dn = torch.randn((n, cfg.d, cfg.f), generator=gen, device=dev, dtype=torch.bfloat16) * 0.02
+        w_dn = torch.empty_like(dn)
+        om.ordermoe_pack_down(dn, w_dn)
+        del dn
         ex = om.make_experts(om.BF16, cfg.d, cfg.f, E, local, w_gu, w_dn)
         out = om.alloc_route_out(T, k, M, dev)
         layers.append(dict(L=L, keep=(tdev, w_gu, w_dn), ex=ex, out=out, os=om.route_out_struct(out),

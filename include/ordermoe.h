@@ -416,9 +416,10 @@ typedef struct {
     int32_t n_shared;            /* shared experts (0 = none) */
     const int32_t* local_experts;/* host [n_local] expert ids, strictly increasing */
     const void* w_gate_up;       /* dev [n_local][2f][d] packed by ordermoe_pack_gate_up */
-    const void* w_down;          /* dev [n_local][d][f] */
+    const void* w_down;          /* dev [n_local][d][f] packed by ordermoe_pack_down */
     const void* w_shared_gate_up;/* dev [2*n_shared*f][d] packed, or NULL if n_shared = 0 */
-    const void* w_shared_down;   /* dev [d][n_shared*f] (the n_shared W_down side by side) */
+    const void* w_shared_down;   /* dev [d][n_shared*f] packed by ordermoe_pack_down (n = 1): the
+                                    n_shared W_down side by side */
 } ordermoe_experts;
 
 /* Requirements: bf16 d % 256 == 0 and f % 128 == 0, fp32 d % 64 == 0 and
@@ -443,12 +444,27 @@ int ordermoe_local_moe_forward(const ordermoe_experts* W, const void* x, int64_t
                                const uint8_t* loc_in, int32_t server, void* y,
                                int32_t* row_offsets, void* ws, size_t ws_bytes, void* stream);
 
-/* One-time weight packing for ordermoe_local_moe_forward (device).
- * w_gate, w_up: dev [n][f][d]; out: dev [n][2f][d] where, for every block b of
- * 32 FFN columns, rows [64b, 64b+32) hold gate rows [32b, 32b+32) and rows
- * [64b+32, 64b+64) hold the matching up rows.  Requires f % 32 == 0. */
+/* One-time weight packing for ordermoe_local_moe_forward (device, ordered on
+ * `stream`; out must not overlap the inputs).  The FFN weights of eq (15)'s
+ * experts in the torch Linear layout [out][in] go in; the forward reads only
+ * the packed copies.
+ *
+ * ordermoe_pack_gate_up: w_gate, w_up: dev [n][f][d]; out: dev [n][2f][d]
+ * holding, for every block b of 32 FFN columns, the gate rows [32b, 32b+32) as
+ * rows [64b, 64b+32) and the matching up rows as rows [64b+32, 64b+64).
+ * ordermoe_pack_down: w_down: dev [n][d][f]; out: dev [n][d][f].
+ * fp32: the rows of each expert's matrix stay in row order.  bf16: each
+ * expert's matrix [N][K] (gate/up N = 2f, K = d; down N = d, K = f) is stored
+ * tile-blocked as [N/256][K/64][256][64], element (r, c) at
+ * ((r/256) (K/64) + c/64) 16384 + (r%256) 64 + c%64: the 256 rows of one
+ * 64-deep K step of a GEMM tile are one contiguous 32 KB block.
+ * Requires gate/up f % 32 == 0 and d % 8 == 0 (bf16: f % 128 == 0 and
+ * d % 64 == 0), down f % 8 == 0 (bf16: d % 256 == 0 and f % 64 == 0), and
+ * 16-byte aligned pointers; else ORDERMOE_EINVAL. */
 int ordermoe_pack_gate_up(int32_t dtype, int32_t n, int32_t f, int32_t d, const void* w_gate,
                           const void* w_up, void* out, void* stream);
+int ordermoe_pack_down(int32_t dtype, int32_t n, int32_t d, int32_t f, const void* w_down, void* out,
+                       void* stream);
 
 /* ------------------------------------------------------------------------
  * Kernel timing (measurement support, off by default).

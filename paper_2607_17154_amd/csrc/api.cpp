@@ -352,9 +352,28 @@ extern "C" int ordermoe_pack_gate_up(int32_t dtype, int32_t n, int32_t f, int32_
     if (dtype != ORDERMOE_F32 && dtype != ORDERMOE_BF16) return fail(ORDERMOE_EDTYPE, "pack_gate_up: dtype");
     if (n < 0 || f < 32 || f % 32 != 0 || d < 8 || d % 8 != 0)
         return fail(ORDERMOE_EINVAL, "pack_gate_up: need n >= 0, f % 32 == 0, d % 8 == 0");
+    if (dtype == ORDERMOE_BF16 && (f % 128 != 0 || d % 64 != 0))
+        return fail(ORDERMOE_EINVAL, "pack_gate_up: bf16 needs f % 128 == 0 and d % 64 == 0");
     if (n > 0 && (!w_gate || !w_up || !out)) return fail(ORDERMOE_EINVAL, "pack_gate_up: null pointer");
+    if (n > 0 && (!aligned16(w_gate) || !aligned16(w_up) || !aligned16(out)))
+        return fail(ORDERMOE_EINVAL, "pack_gate_up: pointers must be 16-byte aligned");
     const int e = launch_pack_gate_up(dtype, n, f, d, w_gate, w_up, out, stream);
     if (e) return hip_fail(e, "pack_gate_up launch");
+    clear_error();
+    return ORDERMOE_OK;
+}
+
+extern "C" int ordermoe_pack_down(int32_t dtype, int32_t n, int32_t d, int32_t f, const void* w_down,
+                                  void* out, void* stream) {
+    if (dtype != ORDERMOE_F32 && dtype != ORDERMOE_BF16) return fail(ORDERMOE_EDTYPE, "pack_down: dtype");
+    if (n < 0 || d < 1 || f < 8 || f % 8 != 0) return fail(ORDERMOE_EINVAL, "pack_down: need n >= 0, d >= 1, f % 8 == 0");
+    if (dtype == ORDERMOE_BF16 && (d % 256 != 0 || f % 64 != 0))
+        return fail(ORDERMOE_EINVAL, "pack_down: bf16 needs d % 256 == 0 and f % 64 == 0");
+    if (n > 0 && (!w_down || !out)) return fail(ORDERMOE_EINVAL, "pack_down: null pointer");
+    if (n > 0 && (!aligned16(w_down) || !aligned16(out)))
+        return fail(ORDERMOE_EINVAL, "pack_down: pointers must be 16-byte aligned");
+    const int e = launch_pack_down(dtype, n, d, f, w_down, out, stream);
+    if (e) return hip_fail(e, "pack_down launch");
     clear_error();
     return ORDERMOE_OK;
 }

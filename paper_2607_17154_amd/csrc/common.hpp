@@ -157,5 +157,6 @@ int launch_lookahead_device(const LookaheadDeviceArgs& d, void* stream);
 
 int launch_pack_gate_up(int dtype, int n, int f, int d, const void* g, const void* u, void* out,
                         void* stream);
+int launch_pack_down(int dtype, int n, int d, int f, const void* w, void* out, void* stream);
 
 }  // namespace ordermoe

@@ -330,6 +330,56 @@ __global__ void __launch_bounds__(SCAN_THREADS) rows_small_kernel(const RowsArgs
     }
 }
 
+// ---------------------------------------------------------------- weights
+// One-time packing (offline).  bf16 weights are stored tile-blocked: a matrix
+// [N][K] (N % 256 == 0, K % 64 == 0) becomes [N/256][K/64][256][64], so that
+// the 256 weight rows a GEMM tile reads in one 64-deep K step are one 32 KB
+// block (and the 64 rows a thin-GEMM workgroup reads per K step 8 KB of it):
+// the weight stream leaves DRAM in whole contiguous blocks instead of 128-byte
+// slices of rows 8 or 28 KB apart.  fp32 weights keep the row layout.
+constexpr int WB_ROWS = 256, WB_K = 64;
+__host__ __device__ inline int64_t wblk_elem(int64_t n, int64_t k, int64_t K) {
+    return ((n / WB_ROWS) * (K / WB_K) + k / WB_K) * (WB_ROWS * WB_K) + (n % WB_ROWS) * WB_K + k % WB_K;
+}
+
+// gate/up: one block per packed row p of the n 2f rows; rows [64b, 64b+32) of
+// an expert <- gate rows [32b, 32b+32), rows [64b+32, 64b+64) <- the matching up
+// rows; bf16 rows then go to their blocked places in 16-byte pieces
+__global__ void pack_gate_up_kernel(int esz, int64_t n, int f, int d, const char* g, const char* u, char* out) {
+    const int64_t prow = blockIdx.x;                  // over n * 2f rows
+    const int64_t ex = prow / (2 * f);
+    const int pr = (int)(prow % (2 * f));
+    const int blk = pr / 64, within = pr % 64;
+    const int src_row = blk * 32 + (within & 31);
+    const char* src = (within < 32 ? g : u) + ((ex * f + src_row) * (int64_t)d) * esz;
+    if (esz == 4) {
+        char* dst = out + prow * (int64_t)d * esz;
+        for (int64_t i = threadIdx.x * 4; i < (int64_t)d * esz; i += blockDim.x * 4)
+            *(uint32_t*)(dst + i) = *(const uint32_t*)(src + i);
+        return;
+    }
+    __bf16* dst = (__bf16*)out + ex * 2 * f * (int64_t)d;
+    for (int k = threadIdx.x * 8; k < d; k += blockDim.x * 8)
+        *(uint4*)(dst + wblk_elem(pr, k, d)) = *(const uint4*)((const __bf16*)src + k);
+}
+
+// down: one block per row p of the n d rows of [n][d][f]
+__global__ void pack_down_kernel(int esz, int64_t n, int d, int f, const char* w, char* out) {
+    const int64_t row = blockIdx.x;                   // over n * d rows
+    const int64_t ex = row / d;
+    const int r = (int)(row % d);
+    const char* src = w + row * (int64_t)f * esz;
+    if (esz == 4) {
+        char* dst = out + row * (int64_t)f * esz;
+        for (int64_t i = threadIdx.x * 4; i < (int64_t)f * esz; i += blockDim.x * 4)
+            *(uint32_t*)(dst + i) = *(const uint32_t*)(src + i);
+        return;
+    }
+    __bf16* dst = (__bf16*)out + ex * (int64_t)d * f;
+    for (int k = threadIdx.x * 8; k < f; k += blockDim.x * 8)
+        *(uint4*)(dst + wblk_elem(r, k, f)) = *(const uint4*)((const __bf16*)src + k);
+}
+
 // ---------------------------------------------------------------- GEMMs
 struct GemmArgs {
     const int32_t* offsets;   // [G + 1] row offsets of the groups (device)
@@ -611,9 +661,12 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
             const uint32_t src = MODE == 0 ? (row < L.R ? (uint32_t)p.row_tok[L.rowbase + row] : 0u) : (uint32_t)row;
             aoff[v] = row < L.R ? (src * (uint32_t)(MODE == 0 ? p.ldx : K) + ((v & 1) ? gc1 : gc0) * 8) * 2u : OOR;
         }
-        const uint32_t brow0 = (uint32_t)(L.n0 + wave_r * BV * 8 + rsub) * (uint32_t)K;
-        const uint32_t boffe = (brow0 + gc0 * 8) * 2u, boffo = (brow0 + gc1 * 8) * 2u;
-        const uint32_t bstride = 16u * (uint32_t)K;       // 8 rows, in bytes
+        // B: the blocked weights (256-row blocks of 64-deep K steps, 128-byte
+        // rows): load instruction v of wave_r w covers rows (w BV + v) 8 .. +7
+        // of the tile's block, 1 KB in a row; the K step goes in the scalar offset
+        static_assert(BN == WB_ROWS, "a tile's weight rows are one block");
+        const uint32_t bblk = (uint32_t)(L.n0 / BN) * (uint32_t)(K / WB_K) * (uint32_t)(BN * WB_K * 2) +
+                              (uint32_t)(wave_r * BV * 8 + rsub) * (WB_K * 2u);
 
         f32x16 acc[FM][FN];
 #pragma unroll
@@ -638,8 +691,8 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
 #pragma unroll
             for (int v = 0; v < BV; ++v)
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(rb_rs, (lds_ptr)(sb + (wave_u * BV + v) * 8 * 64), 16,
-                                                         ((v & 1) ? boffo : boffe) + v * bstride, (uint32_t)k0 * 2u,
-                                                         0, 0);
+                                                         bblk + v * 1024u + (uint32_t)((v & 1) ? gc1 : gc0) * 16u,
+                                                         (uint32_t)k0 * (uint32_t)(BN * 2), 0, 0);
         };
         // fragment of row (lane_r & 31) of each 32-row block, K chunk 2 ks + lane_r / 32
         const int arow = (wm_r * WM + (lane_r & 31)) * 64;
@@ -926,9 +979,11 @@ ggemm_thin(const GemmArgs p) {
         const __bf16* Bw = shared ? (const __bf16*)p.Ws
                                   : (const __bf16*)p.Wr + (size_t)L.g * L.N * K;
         const __amdgpu_buffer_rsrc_t rb_rs = make_rsrc(Bw, (uint32_t)((size_t)L.N * K * 2));
-        // weight reads: lane l takes row 8i + l/8, 16-byte chunk l%8 of the step's 128 bytes
-        const uint32_t wrow0 = ((uint32_t)(L.n0 + (lane >> 3)) * (uint32_t)K + 8u * (lane & 7)) * 2u;
-        const uint32_t wstride8 = 16u * (uint32_t)K;                 // 8 rows, in bytes
+        // weight reads from the blocked layout: the tile's 64 rows of one K step
+        // are 8 KB in a row; lane l takes row 8i + l/8, 16-byte chunk l%8 of
+        // that row's 128 bytes, and the K step goes in the scalar offset
+        const uint32_t wblk0 = (uint32_t)(L.n0 / WB_ROWS) * (uint32_t)(K / WB_K) * (uint32_t)(WB_ROWS * WB_K * 2) +
+                               (uint32_t)((L.n0 % WB_ROWS) + (lane >> 3)) * (WB_K * 2u) + (uint32_t)(lane & 7) * 16u;
         char* stg = th_lds + wave * (TH_BN * TH_LDK);
         char* wdst = stg + (lane >> 3) * TH_LDK + (lane & 7) * 16;
         const char* frag = stg + c * TH_LDK + h * 16;                  // row c, chunk 2i + h
@@ -954,9 +1009,10 @@ ggemm_thin(const GemmArgs p) {
             const int st = wave + it * TH_WAVES;
             // a step past the end reads zeros through the range check and adds nothing
             const uint32_t ok = it < nst ? 0u : OOR;
-            const uint32_t k0 = (uint32_t)st * 128u;   // bytes
+            const uint32_t k0 = (uint32_t)st * 128u;   // bytes into a token or activation row
+            const uint32_t kb = (uint32_t)st * (uint32_t)(WB_ROWS * WB_K * 2);   // bytes into the weight blocks
 #pragma unroll
-            for (int i = 0; i < 8; ++i) w[buf][i] = buf_load16(rb_rs, (wrow0 + i * wstride8) | ok, k0);
+            for (int i = 0; i < 8; ++i) w[buf][i] = buf_load16(rb_rs, (wblk0 + i * 1024u) | ok, kb);
 #pragma unroll
             for (int i = 0; i < 4; ++i) a[buf][i] = buf_load16(ra_rs, aoff | ok, k0 + 32u * i);
         };
@@ -1308,6 +1364,25 @@ int launch_local_forward(const ForwardArgs& f, void* stream) {
         }
     if ((e = hipGetLastError()) != hipSuccess) return (int)e;
     return 0;
+}
+
+int launch_pack_gate_up(int dtype, int n, int f, int d, const void* g, const void* u, void* out,
+                        void* stream) {
+    const int esz = dtype == ORDERMOE_BF16 ? 2 : 4;
+    const int64_t rows = (int64_t)n * 2 * f;
+    if (rows == 0) return 0;
+    hipLaunchKernelGGL(pack_gate_up_kernel, dim3((unsigned)rows), dim3(256), 0, (hipStream_t)stream,
+                       esz, (int64_t)n, f, d, (const char*)g, (const char*)u, (char*)out);
+    return (int)hipGetLastError();
+}
+
+int launch_pack_down(int dtype, int n, int d, int f, const void* w, void* out, void* stream) {
+    const int esz = dtype == ORDERMOE_BF16 ? 2 : 4;
+    const int64_t rows = (int64_t)n * d;
+    if (rows == 0) return 0;
+    hipLaunchKernelGGL(pack_down_kernel, dim3((unsigned)rows), dim3(256), 0, (hipStream_t)stream,
+                       esz, (int64_t)n, d, f, (const char*)w, (char*)out);
+    return (int)hipGetLastError();
 }
 
 }  // namespace ordermoe

@@ -553,21 +553,6 @@ __global__ void __launch_bounds__(256) sim_normalise_kernel(const SimArgs a, con
     a.sim[p] = out;
 }
 
-__global__ void pack_gate_up_kernel(int esz, int64_t n, int f, int d, const char* g, const char* u,
-                                    char* out) {
-    // one block per packed row; rows [64b, 64b+32) <- gate [32b, 32b+32), [64b+32, 64b+64) <- up
-    const int64_t prow = blockIdx.x;                  // over n * 2f rows
-    const int64_t ex = prow / (2 * f);
-    const int pr = (int)(prow % (2 * f));
-    const int blk = pr / 64, within = pr % 64;
-    const int src_row = blk * 32 + (within & 31);
-    const char* src = (within < 32 ? g : u) + ((ex * f + src_row) * (int64_t)d) * esz;
-    char* dst = out + prow * (int64_t)d * esz;
-    const int64_t nbytes = (int64_t)d * esz;
-    for (int64_t i = threadIdx.x * 4; i < nbytes; i += blockDim.x * 4)
-        *(uint32_t*)(dst + i) = *(const uint32_t*)(src + i);
-}
-
 }  // namespace
 
 int64_t similarity_tokens_per_chunk(int) { return SIM_TC; }
@@ -608,16 +593,6 @@ int launch_similarity(const SimArgs& a, void* stream) {
     }
     e = hipGetLastError();
     return (int)e;
-}
-
-int launch_pack_gate_up(int dtype, int n, int f, int d, const void* g, const void* u, void* out,
-                        void* stream) {
-    const int esz = dtype == ORDERMOE_BF16 ? 2 : 4;
-    const int64_t rows = (int64_t)n * 2 * f;
-    if (rows == 0) return 0;
-    hipLaunchKernelGGL(pack_gate_up_kernel, dim3((unsigned)rows), dim3(256), 0, (hipStream_t)stream,
-                       esz, (int64_t)n, f, d, (const char*)g, (const char*)u, (char*)out);
-    return (int)hipGetLastError();
 }
 
 }  // namespace ordermoe

@@ -30,7 +30,7 @@ EXPORTS = ("ordermoe_last_error", "ordermoe_similarity_workspace_size", "ordermo
            "ordermoe_group_experts", "ordermoe_place", "ordermoe_build_tables",
            "ordermoe_build_lookahead", "ordermoe_route_workspace_size", "ordermoe_route_select",
            "ordermoe_forward_workspace_size", "ordermoe_local_moe_forward",
-           "ordermoe_pack_gate_up", "ordermoe_timing_enable", "ordermoe_timing_read",
+           "ordermoe_pack_gate_up", "ordermoe_pack_down", "ordermoe_timing_enable", "ordermoe_timing_read",
            "ordermoe_estimate_transitions", "ordermoe_theta_layer", "ordermoe_adapt_weights",
            "ordermoe_place_random", "ordermoe_simulate_delay", "ordermoe_lookahead_device_workspace_size",
            "ordermoe_build_lookahead_device", "ordermoe_transitions_device_workspace_size",
@@ -129,6 +129,8 @@ def lib() -> ctypes.CDLL:
                                              _P, _I32, _P, _P, _P, _SZ, _P]
     L.ordermoe_pack_gate_up.restype = ctypes.c_int
     L.ordermoe_pack_gate_up.argtypes = [_I32, _I32, _I32, _I32, _P, _P, _P, _P]
+    L.ordermoe_pack_down.restype = ctypes.c_int
+    L.ordermoe_pack_down.argtypes = [_I32, _I32, _I32, _I32, _P, _P, _P]
     L.ordermoe_timing_enable.restype = ctypes.c_int
     L.ordermoe_timing_enable.argtypes = [_I32]
     L.ordermoe_timing_read.restype = ctypes.c_int
@@ -517,8 +519,17 @@ def ordermoe_pack_gate_up(w_gate, w_up, out, stream=None):
     import torch
     n, f, d = w_gate.shape
     code = BF16 if w_gate.dtype == torch.bfloat16 else F32
-    _check(lib().ordermoe_pack_gate_up(code, n, f, d, _dev(w_gate), _dev(w_up), _dev(out),
-                                       _stream(stream)))
+    _check(lib().ordermoe_pack_gate_up(code, n, f, d, _dev(w_gate), _dev(w_up, w_gate.dtype, n * f * d),
+                                       _dev(out, w_gate.dtype, 2 * n * f * d), _stream(stream)))
+
+
+def ordermoe_pack_down(w_down, out, stream=None):
+    """w_down: [n, d, f] device tensor; out: [n, d, f] (packed layout)."""
+    import torch
+    n, d, f = w_down.shape
+    code = BF16 if w_down.dtype == torch.bfloat16 else F32
+    _check(lib().ordermoe_pack_down(code, n, d, f, _dev(w_down), _dev(out, w_down.dtype, n * d * f),
+                                    _stream(stream)))
 
 
 def ordermoe_timing_enable(on: bool = True):

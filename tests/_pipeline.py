@@ -138,7 +138,8 @@ class DeviceLayer:
             dn[i] = to_device(Wd, cfg.dtype)
         self.w_gu = torch.empty((max(n, 1), 2 * cfg.f, cfg.d), dtype=tdt, device="cuda")
         om.ordermoe_pack_gate_up(g, u, self.w_gu)
-        self.w_dn = dn
+        self.w_dn = torch.empty_like(dn)
+        om.ordermoe_pack_down(dn, self.w_dn)
         self.w_sh_gu = self.w_sh_dn = None
         if cfg.n_shared:
             sh = case.shared()
@@ -146,9 +147,11 @@ class DeviceLayer:
             su = torch.cat([to_device(s[1], cfg.dtype) for s in sh], 0).unsqueeze(0).contiguous()
             self.w_sh_gu = torch.empty((1, 2 * cfg.n_shared * cfg.f, cfg.d), dtype=tdt, device="cuda")
             om.ordermoe_pack_gate_up(sg, su, self.w_sh_gu)
-            self.w_sh_dn = torch.cat([to_device(s[2], cfg.dtype) for s in sh], 1).contiguous()
+            sd = torch.cat([to_device(s[2], cfg.dtype) for s in sh], 1).unsqueeze(0).contiguous()
+            self.w_sh_dn = torch.empty_like(sd)
+            om.ordermoe_pack_down(sd, self.w_sh_dn)
         torch.cuda.synchronize()
-        del g, u
+        del g, u, dn
         self.experts = om.make_experts(self.code, cfg.d, cfg.f, cfg.E, case.local, self.w_gu,
                                        self.w_dn, cfg.n_shared, self.w_sh_gu, self.w_sh_dn)
 

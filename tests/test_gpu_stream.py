@@ -227,8 +227,10 @@ def test_local_forward_of_a_stream_layer(stream_case, chain, oracle_chain, layer
         wg[i], wu[i], wd[i] = to_device(a, "bf16"), to_device(b, "bf16"), to_device(c, "bf16")
     wgu = torch.empty((n, 2 * cfg.f, cfg.d), dtype=torch.bfloat16, device="cuda")
     om.ordermoe_pack_gate_up(wg, wu, wgu)
-    del wg, wu
-    ex = om.make_experts(om.BF16, cfg.d, cfg.f, cfg.E, local, wgu, wd)
+    wdp = torch.empty_like(wd)
+    om.ordermoe_pack_down(wd, wdp)
+    del wg, wu, wd
+    ex = om.make_experts(om.BF16, cfg.d, cfg.f, cfg.E, local, wgu, wdp)
     T = cfg.T
     y = torch.empty((T, cfg.d), dtype=torch.bfloat16, device="cuda")
     ro = torch.empty(n + 2, dtype=torch.int32, device="cuda")

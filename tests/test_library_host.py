@@ -220,6 +220,12 @@ def test_device_entry_points_validate_before_launch():
                                             None, 0, None)
     assert rc == om.EINVAL
     assert om.lib().ordermoe_pack_gate_up(om.BF16, 1, 10, 64, None, None, None, None) == om.EINVAL
+    # bf16 packing blocks 256 rows by 64 K: the shapes must divide (checked before any pointer)
+    assert om.lib().ordermoe_pack_gate_up(om.BF16, 1, 96, 64, None, None, None, None) == om.EINVAL
+    assert om.lib().ordermoe_pack_down(om.BF16, 1, 100, 128, None, None, None) == om.EINVAL
+    assert om.lib().ordermoe_pack_down(om.BF16, 1, 256, 96, None, None, None) == om.EINVAL
+    assert om.lib().ordermoe_pack_down(om.BF16, 1, 256, 128, None, None, None) == om.EINVAL   # null pointers
+    assert om.lib().ordermoe_pack_down(om.F32, 0, 100, 8, None, None, None) == om.OK           # nothing to do
     # the device builds of eq 41-42: sizes, pointers and workspace checked before any launch
     L = om.lib()
     assert L.ordermoe_estimate_transitions_device(4, 300, 10, None, None, None, 0, None) == om.EINVAL
