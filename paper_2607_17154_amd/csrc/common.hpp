@@ -69,11 +69,11 @@ struct RouteArgs {
     int nblk;
     int S_in_lds;          // set by the launcher: stage the cost table in LDS
     int ksplit;            // set by the launcher: K slices of the split router (0: fused)
+    int x_lds;             // set by the launcher: bytes of the LDS-staged token rows (0: none)
 };
 int launch_route_select(const RouteArgs& a, void* stream);
 int route_tokens_per_block();
 size_t route_split_buffer_floats(int64_t T);
-size_t route_smem_bytes(int E, int gmax, int M, bool S_in_lds);
 
 struct ForwardArgs {
     int dtype, d, f, E, n_local, n_shared, k;

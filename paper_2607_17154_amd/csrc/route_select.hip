@@ -162,6 +162,57 @@ __device__ inline void router_k_loop(const RouteArgs& a, int kw, int lane, int64
     }
 }
 
+// Router partial logits of a 16-token block of at most 16 experts whose token
+// rows fit in LDS (d % 512 == 0, d <= RT_XLDS_MAX_D): the block's 16 rows go
+// from memory straight into LDS in whole 1 KB pieces, every piece of every wave
+// issued at once beside the wave's router fragments (into registers), so that
+// the block's whole share of the token stream is in flight together instead of
+// two groups of steps per wave.  Row r sits at r (2d + RT_XPAD) bytes: the pad
+// puts the 16 rows of one fragment read on distinct banks.  Then the wave's K
+// steps (kw, kw + KW, ...) as in router_k_loop, token fragments read from LDS.
+// Rows past the batch lie past the buffer resource and arrive as zeros.
+constexpr int RT_XLDS_MAX_D = 4096;
+constexpr int RT_XPAD = 16;                  // bytes
+
+__host__ __device__ inline int route_xlds_bytes(int d) { return RT_TB * (2 * d + RT_XPAD); }
+
+typedef __attribute__((address_space(3))) void* lds_ptr;
+
+template <int KW>
+__device__ inline void router_dma_loop(const RouteArgs& a, int kw, int lane, int64_t tr0, f32x4* acc, char* sx) {
+    constexpr int MAXS = RT_XLDS_MAX_D / (32 * KW);   // K steps (and pieces) per wave
+    const int d = a.d, E = a.E;
+    const int r16 = lane & 15, kg = (lane >> 4) * 8;
+    const int64_t left = a.T - tr0;                   // >= 1: the block holds a token
+    const int nrows = left > 16 ? 16 : (int)left;
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc((const __bf16*)a.x + tr0 * (int64_t)d, (uint32_t)nrows * (uint32_t)d * 2u);
+    const __amdgpu_buffer_rsrc_t rw = make_rsrc(a.w_router, (uint32_t)E * (uint32_t)d * 2u);
+    const int ns = d / (32 * KW);
+    const int cpr = d / 512;                          // 1 KB pieces per token row
+    const uint32_t xs = 2u * (uint32_t)d + RT_XPAD;
+    const uint32_t wo = r16 < E ? ((uint32_t)r16 * (uint32_t)d + kg) * 2u : RT_OOR;
+    bf16x8 wv[MAXS];
+#pragma unroll
+    for (int i = 0; i < MAXS; ++i)
+        if (i < ns) wv[i] = buf_load16(rw, wo, (uint32_t)(kw + KW * i) * 64u);
+#pragma unroll
+    for (int i = 0; i < MAXS; ++i)
+        if (i < ns) {
+            const int p = kw + KW * i;                // piece p: row p / cpr, chunk p % cpr
+            const int row = p / cpr, ch = p - row * cpr;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_ptr)(sx + row * xs + ch * 1024), 16, lane * 16,
+                                                     (uint32_t)row * 2u * (uint32_t)d + (uint32_t)ch * 1024u, 0, 0);
+        }
+    __syncthreads();                                  // waits for every piece (vmcnt 0), then the barrier
+    const char* fr = sx + r16 * xs + kg * 2;
+#pragma unroll
+    for (int i = 0; i < MAXS; ++i)
+        if (i < ns) {
+            const bf16x8 av = *(const bf16x8*)(fr + (kw + KW * i) * 64);
+            acc[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, wv[i], acc[0], 0, 0, 0);
+        }
+}
+
 // Router partial logits for 32-token blocks of more than 16 experts: the
 // router rows are shared by both 16-token row groups through LDS.  The K axis
 // goes in chunks of RT_CK = 128 (one 32-step per K wave of a row group); the
@@ -326,13 +377,14 @@ __global__ void __launch_bounds__(64) router_split_kernel(const RouteArgs a) {
 
 // floats of the first LDS region: the partial-sum slots, or (32-token blocks of
 // more than 16 experts) the two staged router-row buffers if larger
-__host__ __device__ inline int route_region0_floats(int tb, int E) {
+__host__ __device__ inline int route_region0_floats(int tb, int E, int xlds) {
     const int Epad = (E + 15) & ~15;
     const int part = RT_SLOTS * tb * Epad;
     // the staged loop keeps NBT * 16 rows per buffer (32 or 64), two buffers of bf16
     const int rows = Epad <= 32 ? 32 : 64;
     const int wbuf = (tb == RT_TB2 && Epad > 16 && Epad <= 64) ? rows * RT_WLD : 0;
-    return part > wbuf ? part : wbuf;
+    const int r = part > wbuf ? part : wbuf;
+    return r > xlds / 4 ? r : xlds / 4;               // the LDS-staged token rows
 }
 
 // up to 64 experts: at most 128 VGPRs (4 waves per SIMD), so two blocks share a CU.
@@ -355,7 +407,7 @@ route_select_kernel(const RouteArgs a) {
     extern __shared__ float smem[];
     float* s_part = smem;                               // [RT_SLOTS][TB][Epad]
     float* s_logit = smem;                              // reuses slot 0 after the sum
-    int32_t* s_t1k = (int32_t*)(smem + route_region0_floats(TB, E));   // [E][gmax]
+    int32_t* s_t1k = (int32_t*)(smem + route_region0_floats(TB, E, a.x_lds));   // [E][gmax]
     float* s_t1q = (float*)(s_t1k + E * a.gmax);                   // [E][gmax]
     int32_t* s_t1n = (int32_t*)(s_t1q + E * a.gmax);               // [E]
     uint32_t* s_mask = (uint32_t*)(s_t1n + E);                     // [E]
@@ -413,13 +465,16 @@ route_select_kernel(const RouteArgs a) {
         }
     } else if (a.dtype == ORDERMOE_BF16) {
         const int nblk = Epad / 16;
-        const int rg = wave / KW, kw = wave % KW;
+        const int rg = wave / KW, kw = __builtin_amdgcn_readfirstlane(wave % KW);
         f32x4 acc[NBT];
 #pragma unroll
         for (int i = 0; i < NBT; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
         // group size: two groups of reads in flight per wave, within 128
         // registers so that two blocks share a CU
-        if constexpr (NBT == 1) router_k_loop<1, 4, KW>(a, kw, lane, t0 + rg * 16, acc);
+        if constexpr (NBT == 1 && TB == RT_TB) {
+            if (a.x_lds) router_dma_loop<KW>(a, kw, lane, t0, acc, (char*)smem);
+            else router_k_loop<1, 4, KW>(a, kw, lane, t0, acc);
+        } else if constexpr (NBT == 1) router_k_loop<1, 4, KW>(a, kw, lane, t0 + rg * 16, acc);
         else if constexpr (TB == RT_TB2 && NBT == 2) router_lds_loop<2>(a, kw, lane, tid, t0 + rg * 16, acc, (__bf16*)smem);
         else if constexpr (TB == RT_TB2 && NBT == 4) router_lds_loop<4>(a, kw, lane, tid, t0 + rg * 16, acc, (__bf16*)smem);
         else if constexpr (NBT == 2) router_k_loop<2, 2, KW>(a, kw, lane, t0 + rg * 16, acc);
@@ -431,8 +486,10 @@ route_select_kernel(const RouteArgs a) {
         // row group, waves 4-7 first hand their sums to waves 0-3.
         const int r16 = lane & 15;
         const int trow = rg * 16 + (lane >> 4) * 4;
-        // the staged router rows share LDS with the partial-sum slots
+        // the staged router rows and token rows share LDS with the partial-sum slots
         if constexpr (TB == RT_TB2 && (NBT == 2 || NBT == 4)) __syncthreads();
+        if constexpr (NBT == 1 && TB == RT_TB)
+            if (a.x_lds) __syncthreads();
         if (KW == 8 && wave >= RT_SLOTS) {
 #pragma unroll
             for (int nb = 0; nb < NBT; ++nb)
@@ -822,16 +879,18 @@ int launch_route_kernel(const RouteArgs& a, size_t smem, hipStream_t st) {
     return launch_route_kernel_k<NBT, TB, ORDERMOE_MAX_TOPK>(a, smem, st);
 }
 
-size_t route_smem(int tb, int E, int gmax, int M, bool S_in_lds) {
-    return sizeof(float) * (size_t)route_region0_floats(tb, E) + (size_t)E * gmax * 8 + (size_t)E * 8 +
+size_t route_smem(int tb, int E, int gmax, int M, bool S_in_lds, int xlds) {
+    return sizeof(float) * (size_t)route_region0_floats(tb, E, xlds) + (size_t)E * gmax * 8 + (size_t)E * 8 +
            sizeof(int) * (size_t)(8 + M) + (S_in_lds ? sizeof(float) * (size_t)M * M * E : 0);
 }
 
+constexpr size_t RT_LDS_MAX = 160 * 1024;
+
 // the cost table is staged in LDS when it is small enough to leave room for
 // two blocks per CU, or, for batches of at most one block per CU, when it fits
-bool route_S_in_lds(int tb, int E, int gmax, int M, int nblk) {
-    const size_t b = route_smem(tb, E, gmax, M, true);
-    return b <= 64 * 1024 || (nblk <= 256 && b <= 150 * 1024);
+bool route_S_in_lds(int tb, int E, int gmax, int M, int nblk, int xlds) {
+    const size_t b = route_smem(tb, E, gmax, M, true, xlds);
+    return b <= 64 * 1024 || (nblk <= 256 && b <= (xlds ? RT_LDS_MAX : 150 * 1024));
 }
 
 }  // namespace
@@ -839,7 +898,6 @@ bool route_S_in_lds(int tb, int E, int gmax, int M, int nblk) {
 // the workspace is sized for blocks of RT_TB tokens, the smallest block
 int route_tokens_per_block() { return RT_TB; }
 
-size_t route_smem_bytes(int E, int gmax, int M, bool S_in_lds) { return route_smem(RT_TB, E, gmax, M, S_in_lds); }
 
 // partial logits of the split router: at most 256 blocks of RT_TB tokens times
 // the K slices (the launcher keeps slices * blocks <= 256), every expert count
@@ -864,9 +922,15 @@ int launch_route_select(const RouteArgs& a, void* stream) {
     const int tb = staged || (bf && nbt == 1 && nb16 > 512) ? RT_TB2 : RT_TB;
     RouteArgs b = a;
     b.nblk = (int)((a.T + tb - 1) / tb);
+    // batches of at most one 16-token block per CU stage their token rows in
+    // LDS when the rows and the tables fit
+    b.x_lds = 0;
+    if (bf && nbt == 1 && tb == RT_TB && b.nblk <= 256 && a.d % 512 == 0 && a.d <= RT_XLDS_MAX_D &&
+        route_smem(tb, a.E, a.gmax, a.M, false, route_xlds_bytes(a.d)) <= RT_LDS_MAX)
+        b.x_lds = route_xlds_bytes(a.d);
     if (b.nblk > 0) {
-        b.S_in_lds = route_S_in_lds(tb, a.E, a.gmax, a.M, b.nblk) ? 1 : 0;
-        const size_t smem = route_smem(tb, a.E, a.gmax, a.M, b.S_in_lds != 0);
+        b.S_in_lds = route_S_in_lds(tb, a.E, a.gmax, a.M, b.nblk, b.x_lds) ? 1 : 0;
+        const size_t smem = route_smem(tb, a.E, a.gmax, a.M, b.S_in_lds != 0, b.x_lds);
         b.ksplit = 0;
         if (split) {
             // enough waves to cover the CUs, K slices a multiple of 32
