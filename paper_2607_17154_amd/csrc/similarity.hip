@@ -46,7 +46,8 @@ constexpr int ST_LDH = SIM_EMAX + 4;       // row stride of the parked H tile (f
 constexpr int ST_LDT = ST_BM + 8;          // row stride of the h / l planes of H^T (bf16)
 constexpr int ST_LDA = 144;                // bytes per staged token row (64 bf16 + 16)
 constexpr size_t ST_LDS_A = (size_t)ST_BM * ST_LDA;      // token staging, 32 rows per wave
-constexpr size_t ST_LDS_KLOOP = (size_t)2 * SIM_EMAX * ST_LDK * 2 + ST_LDS_A;
+constexpr int ST_WCH = 2;                 // K steps per W chunk (one barrier per chunk)
+constexpr size_t ST_LDS_KLOOP = (size_t)2 * ST_WCH * SIM_EMAX * ST_LDK * 2 + ST_LDS_A;
 constexpr size_t ST_LDS_H = (size_t)ST_BM * ST_LDH * 4;
 constexpr size_t ST_LDS_HL = (size_t)2 * SIM_EMAX * ST_LDT * 2;
 constexpr size_t ST_LDS_MAX2 = ST_LDS_KLOOP > ST_LDS_H ? ST_LDS_KLOOP : ST_LDS_H;
@@ -74,7 +75,7 @@ __global__ void __launch_bounds__(ST_THREADS, 1) sim_tile_kernel(const SimArgs a
     constexpr int BV = BN * BK / 8 / ST_THREADS;        // W loads per thread per K step
     extern __shared__ __attribute__((aligned(16))) char lds_raw[];
     __shared__ int s_cnt[SIM_EMAX];
-    __bf16* sB = (__bf16*)lds_raw;                      // [2][BN][LDK]
+    __bf16* sB = (__bf16*)lds_raw;                      // [2][ST_WCH][BN][LDK]
     float* sH = (float*)lds_raw;                        // [ST_BM][ST_LDH], after the K loop
 
     const int tid = threadIdx.x, lane = tid & 63;
@@ -90,7 +91,7 @@ __global__ void __launch_bounds__(ST_THREADS, 1) sim_tile_kernel(const SimArgs a
     const uint32_t bstride = 128u * (uint32_t)d;        // 64 rows, in bytes
     const int brow_off = (lane & 31) * LDK + (lane >> 5) * 8;
     // this wave's token staging rows, after the W buffers
-    char* astg = lds_raw + (size_t)2 * BN * LDK * 2 + (size_t)wave * 32 * ST_LDA;
+    char* astg = lds_raw + (size_t)2 * ST_WCH * BN * LDK * 2 + (size_t)wave * 32 * ST_LDA;
     char* adst = astg + (lane >> 3) * ST_LDA + (lane & 7) * 16;
     const char* afrag = astg + (lane & 31) * ST_LDA + (lane >> 5) * 16;   // row lane%32, chunk 2ks + h
     constexpr uint32_t OOR = 0x80000000u;
@@ -128,13 +129,14 @@ __global__ void __launch_bounds__(ST_THREADS, 1) sim_tile_kernel(const SimArgs a
             for (int v = 0; v < BV; ++v)
                 rb[st][v] = st_load16(rb_rs, (boff0 + v * bstride) | ok, (uint32_t)step * BK * 2u);
         };
-        auto storeB = [&](int st, int buf) {
-            __bf16* p = sB + buf * BN * LDK + lrow * LDK + lch;
+        // W of one K step into sub-buffer `sub` of LDS buffer `buf`
+        auto storeB = [&](int st, int buf, int sub) {
+            __bf16* p = sB + (buf * ST_WCH + sub) * BN * LDK + lrow * LDK + lch;
 #pragma unroll
             for (int v = 0; v < BV; ++v) *(bf16x8*)(p + v * 64 * LDK) = rb[st][v];
         };
-        auto mma = [&](int st, int buf) {
-            const __bf16* pb = sB + buf * BN * LDK + brow_off;
+        auto mma = [&](int st, int buf, int sub) {
+            const __bf16* pb = sB + (buf * ST_WCH + sub) * BN * LDK + brow_off;
             // the wave's own token rows: stores, then fragment reads, in program order
 #pragma unroll
             for (int i = 0; i < 4; ++i) *(bf16x8*)(adst + i * 8 * ST_LDA) = ax[st][i];
@@ -152,28 +154,36 @@ __global__ void __launch_bounds__(ST_THREADS, 1) sim_tile_kernel(const SimArgs a
         };
         // The reads of one K step (tokens, then W rows) form a batch issued S
         // steps before the step is multiplied.  The memory counter retires reads
-        // in issue order, so waiting for the W rows of step kt + 1 (to put them
-        // in LDS) never waits for the S - 1 younger batches still in flight.
-        // prologue: batches 0 .. S-1, W of step 0 in LDS
+        // in issue order, so waiting for the W rows of the next chunk (to put
+        // them in LDS) never waits for the younger batches still in flight.
+        // W goes to LDS in chunks of ST_WCH = 2 K steps, one barrier per chunk
+        // (a barrier per step cost about a tenth of the stream rate).
+        // prologue: batches 0 .. S-1, W of chunk 0 in LDS
+        static_assert(S % ST_WCH == 0 && ST_WCH == 2, "whole chunks per unrolled pass");
 #pragma unroll
         for (int st = 0; st < S; ++st) { loadA(st, st); loadB(st, st); }
-        storeB(0, 0);
+        storeB(0, 0, 0);
+        storeB(1, 0, 1);
         __syncthreads();
         // steady state, unrolled by S so that every register stage has a fixed name:
-        // step kt multiplies stage kt % S and LDS buffer kt & 1, refills the stage
-        // with batch kt + S, and moves W of step kt + 1 to the other buffer
-        // (KT is a multiple of S: d % 256 == 0 for this kernel)
+        // step kt multiplies stage kt % S from sub-buffer kt % 2 of LDS buffer
+        // (kt / 2) & 1 and refills the stage with batch kt + S; after the second
+        // step of a chunk, W of the next chunk (steps kt + 1, kt + 2) moves to
+        // the other buffer (KT is a multiple of S: d % 256 == 0 for this kernel)
         for (int kt0 = 0; kt0 < KT; kt0 += S) {
 #pragma unroll
             for (int u = 0; u < S; ++u) {
                 const int kt = kt0 + u;
-                mma(u, kt & 1);
+                mma(u, (kt >> 1) & 1, u & 1);
                 __builtin_amdgcn_sched_barrier(0);
                 loadA(u, kt + S);
                 loadB(u, kt + S);
                 __builtin_amdgcn_sched_barrier(0);
-                storeB((u + 1) % S, (kt + 1) & 1);
-                __syncthreads();
+                if (u & 1) {
+                    storeB((u + 1) % S, ((kt + 1) >> 1) & 1, 0);
+                    storeB((u + 2) % S, ((kt + 1) >> 1) & 1, 1);
+                    __syncthreads();
+                }
             }
         }
         __syncthreads();   // every wave is done with the W buffers
