@@ -76,27 +76,42 @@ struct RowsArgs {
     int n_gu_r, n_gu_s, n_dn;
 };
 
+// One token's slots as read from memory: executing server, expert and gate
+// weight per slot, and the token's server.  The reads are issued together
+// (unused slots re-read the last slot, in range, and are discarded, so no
+// branch separates them); the placement kernels issue them first, so that
+// their latency overlaps the reads of the count table.  The arrays are
+// indexed only by unrolled constants so that they stay in registers.
+struct TokSlots {
+    int m[ORDERMOE_MAX_TOPK], ek[ORDERMOE_MAX_TOPK];
+    float wv[ORDERMOE_MAX_TOPK];
+    int loc;
+};
+__device__ inline void token_read(const RowsArgs& a, int64_t t, TokSlots& s) {
+#pragma unroll
+    for (int i = 0; i < ORDERMOE_MAX_TOPK; ++i) {
+        const int64_t o = t * a.k + (i < a.k ? i : a.k - 1);
+        s.m[i] = a.exec_m[o];
+        s.ek[i] = a.exec_k[o];
+        s.wv[i] = a.w[o];
+    }
+    s.loc = a.has_shared ? (int)a.loc_in[t] : -1;
+}
+
 // rows of one token: group ids (local slot, or n_local for the shared group)
-// and merged gate weights, in slot order of first occurrence.  The token's
-// slots are read up front (independent loads); the arrays are indexed only by
-// unrolled constants so that they stay in registers.
-__device__ inline int token_rows(const RowsArgs& a, const int32_t* s_lidx, int64_t t, int* grp,
+// and merged gate weights, in slot order of first occurrence
+__device__ inline int token_rows(const RowsArgs& a, const int32_t* s_lidx, const TokSlots& ts, int* grp,
                                  float* wsum) {
     int m[ORDERMOE_MAX_TOPK], ek[ORDERMOE_MAX_TOPK];
     float wv[ORDERMOE_MAX_TOPK];
-    // all slot reads issued together: unused slots re-read the last slot (in
-    // range) and are discarded, so no branch separates the reads
 #pragma unroll
     for (int s = 0; s < ORDERMOE_MAX_TOPK; ++s) {
-        const int64_t o = t * a.k + (s < a.k ? s : a.k - 1);
-        m[s] = a.exec_m[o];
-        ek[s] = a.exec_k[o];
-        wv[s] = a.w[o];
+        const bool used = s < a.k;
+        m[s] = used ? ts.m[s] : -1;
+        ek[s] = used ? ts.ek[s] : -1;
+        wv[s] = used ? ts.wv[s] : 0.f;
     }
-#pragma unroll
-    for (int s = 0; s < ORDERMOE_MAX_TOPK; ++s)
-        if (s >= a.k) { m[s] = -1; ek[s] = -1; wv[s] = 0.f; }
-    const int loc = a.has_shared ? (int)a.loc_in[t] : -1;
+    const int loc = ts.loc;
 #pragma unroll
     for (int q = 0; q < MAXR; ++q) { grp[q] = -1; wsum[q] = 0.f; }
     int n = 0;
@@ -155,9 +170,11 @@ __global__ void __launch_bounds__(FT_TB) rows_count_kernel(const RowsArgs a) {
     __syncthreads();
     const int64_t t = (int64_t)blockIdx.x * FT_TB + threadIdx.x;
     if (t < a.T) {
+        TokSlots ts;
+        token_read(a, t, ts);
         int grp[MAXR];
         float ws[MAXR];
-        const int n = token_rows(a, s_lidx, t, grp, ws);
+        const int n = token_rows(a, s_lidx, ts, grp, ws);
 #pragma unroll
         for (int q = 0; q < MAXR; ++q)
             if (q < n) atomicAdd(&s_h[grp[q]], 1);
@@ -227,6 +244,9 @@ __global__ void __launch_bounds__(FT_TB) rows_scatter_kernel(const RowsArgs a) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int G = a.n_local + a.has_shared;
     const int b = (int)blockIdx.x;
+    const int64_t t = (int64_t)b * FT_TB + tid;
+    TokSlots ts;
+    if (t < a.T) token_read(a, t, ts);
     for (int i = tid; i < a.E; i += FT_TB) s_lidx[i] = a.lidx[i];
     if (b == 0)
         for (int i = tid; i < 2 * SK_MAX_GRID; i += FT_TB) a.sk_cnt[i] = 0;
@@ -244,12 +264,11 @@ __global__ void __launch_bounds__(FT_TB) rows_scatter_kernel(const RowsArgs a) {
         if (lane == 0) { s_lo[g] = lo; s_tot[g] = tot; }
     }
     __syncthreads();
-    const int64_t t = (int64_t)b * FT_TB + tid;
     int grp[MAXR], rank[MAXR];
     float ws[MAXR];
     int n = 0;
     if (t < a.T) {
-        n = token_rows(a, s_lidx, t, grp, ws);
+        n = token_rows(a, s_lidx, ts, grp, ws);
     } else {
 #pragma unroll
         for (int q = 0; q < MAXR; ++q) { grp[q] = -1; ws[q] = 0.f; }
@@ -288,15 +307,17 @@ __global__ void __launch_bounds__(SCAN_THREADS) rows_small_kernel(const RowsArgs
     __shared__ int32_t s_first[MAXG], s_tot[MAXG];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int G = a.n_local + a.has_shared;
+    const int64_t t = tid;
+    TokSlots ts;
+    if (t < a.T) token_read(a, t, ts);
     for (int i = tid; i < a.E; i += SCAN_THREADS) s_lidx[i] = a.lidx[i];
     for (int i = tid; i < 2 * SK_MAX_GRID; i += SCAN_THREADS) a.sk_cnt[i] = 0;
     __syncthreads();
-    const int64_t t = tid;
     int grp[MAXR], rank[MAXR];
     float ws[MAXR];
     int n = 0;
     if (t < a.T) {
-        n = token_rows(a, s_lidx, t, grp, ws);
+        n = token_rows(a, s_lidx, ts, grp, ws);
     } else {
 #pragma unroll
         for (int q = 0; q < MAXR; ++q) { grp[q] = -1; ws[q] = 0.f; }

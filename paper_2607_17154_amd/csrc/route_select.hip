@@ -178,8 +178,9 @@ __host__ __device__ inline int route_xlds_bytes(int d) { return RT_TB * (2 * d +
 
 typedef __attribute__((address_space(3))) void* lds_ptr;
 
+// The reads: the wave's router fragments into wv, its token pieces into LDS.
 template <int KW>
-__device__ inline void router_dma_loop(const RouteArgs& a, int kw, int lane, int64_t tr0, f32x4* acc, char* sx) {
+__device__ inline void router_dma_issue(const RouteArgs& a, int kw, int lane, int64_t tr0, char* sx, bf16x8* wv) {
     constexpr int MAXS = RT_XLDS_MAX_D / (32 * KW);   // K steps (and pieces) per wave
     const int d = a.d, E = a.E;
     const int r16 = lane & 15, kg = (lane >> 4) * 8;
@@ -191,7 +192,6 @@ __device__ inline void router_dma_loop(const RouteArgs& a, int kw, int lane, int
     const int cpr = d / 512;                          // 1 KB pieces per token row
     const uint32_t xs = 2u * (uint32_t)d + RT_XPAD;
     const uint32_t wo = r16 < E ? ((uint32_t)r16 * (uint32_t)d + kg) * 2u : RT_OOR;
-    bf16x8 wv[MAXS];
 #pragma unroll
     for (int i = 0; i < MAXS; ++i)
         if (i < ns) wv[i] = buf_load16(rw, wo, (uint32_t)(kw + KW * i) * 64u);
@@ -203,6 +203,17 @@ __device__ inline void router_dma_loop(const RouteArgs& a, int kw, int lane, int
             __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_ptr)(sx + row * xs + ch * 1024), 16, lane * 16,
                                                      (uint32_t)row * 2u * (uint32_t)d + (uint32_t)ch * 1024u, 0, 0);
         }
+}
+
+// The MFMAs, after every piece of the block has arrived.
+template <int KW>
+__device__ inline void router_dma_mma(const RouteArgs& a, int kw, int lane, f32x4* acc, const char* sx,
+                                      const bf16x8* wv) {
+    constexpr int MAXS = RT_XLDS_MAX_D / (32 * KW);
+    const int d = a.d;
+    const int r16 = lane & 15, kg = (lane >> 4) * 8;
+    const int ns = d / (32 * KW);
+    const uint32_t xs = 2u * (uint32_t)d + RT_XPAD;
     __syncthreads();                                  // waits for every piece (vmcnt 0), then the barrier
     const char* fr = sx + r16 * xs + kg * 2;
 #pragma unroll
@@ -472,8 +483,20 @@ route_select_kernel(const RouteArgs a) {
         // group size: two groups of reads in flight per wave, within 128
         // registers so that two blocks share a CU
         if constexpr (NBT == 1 && TB == RT_TB) {
-            if (a.x_lds) router_dma_loop<KW>(a, kw, lane, t0, acc, (char*)smem);
-            else router_k_loop<1, 4, KW>(a, kw, lane, t0, acc);
+            if (a.x_lds) {
+                bf16x8 wv[RT_XLDS_MAX_D / (32 * KW)];
+                router_dma_issue<KW>(a, kw, lane, t0, (char*)smem, wv);
+                // the first batch of the candidate tables (read at the start) goes
+                // to LDS while the token rows arrive
+                table_write<0, 2>(s_t1k, n1, tid, pk);
+                table_write<0, 2>((int32_t*)s_t1q, n1, tid, pq);
+                table_write<0, 1>(s_t1n, E, tid, pn);
+                table_write<0, 1>((int32_t*)s_mask, E, tid, pm);
+                table_write<0, 2>((int32_t*)s_S, nS, tid, ps);
+                router_dma_mma<KW>(a, kw, lane, acc, (const char*)smem, wv);
+            } else {
+                router_k_loop<1, 4, KW>(a, kw, lane, t0, acc);
+            }
         } else if constexpr (NBT == 1) router_k_loop<1, 4, KW>(a, kw, lane, t0 + rg * 16, acc);
         else if constexpr (TB == RT_TB2 && NBT == 2) router_lds_loop<2>(a, kw, lane, tid, t0 + rg * 16, acc, (__bf16*)smem);
         else if constexpr (TB == RT_TB2 && NBT == 4) router_lds_loop<4>(a, kw, lane, tid, t0 + rg * 16, acc, (__bf16*)smem);
@@ -539,11 +562,14 @@ route_select_kernel(const RouteArgs a) {
         table_read<2, 2>(a.t1_k, n1, tid, qk);
         table_read<2, 2>((const int32_t*)a.t1_q, n1, tid, qq);
         table_read<2, 14>((const int32_t*)a.S, nS, tid, qs);
-        table_write<0, 2>(s_t1k, n1, tid, pk);
-        table_write<0, 2>((int32_t*)s_t1q, n1, tid, pq);
-        table_write<0, 1>(s_t1n, E, tid, pn);
-        table_write<0, 1>((int32_t*)s_mask, E, tid, pm);
-        table_write<0, 2>((int32_t*)s_S, nS, tid, ps);
+        // (the LDS-staged router path wrote the first batch already)
+        if (!(NBT == 1 && TB == RT_TB && a.x_lds && a.ksplit == 0 && a.dtype == ORDERMOE_BF16)) {
+            table_write<0, 2>(s_t1k, n1, tid, pk);
+            table_write<0, 2>((int32_t*)s_t1q, n1, tid, pq);
+            table_write<0, 1>(s_t1n, E, tid, pn);
+            table_write<0, 1>((int32_t*)s_mask, E, tid, pm);
+            table_write<0, 2>((int32_t*)s_S, nS, tid, ps);
+        }
         table_write<2, 2>(s_t1k, n1, tid, qk);
         table_write<2, 2>((int32_t*)s_t1q, n1, tid, qq);
         table_write<2, 14>((int32_t*)s_S, nS, tid, qs);
@@ -759,6 +785,17 @@ dispatch_kernel(const int32_t* blk_dst, const int64_t* blk_cnt, int nblk, const 
     __shared__ int32_t s_base[ORDERMOE_MAX_SERVERS], s_tot[ORDERMOE_MAX_SERVERS], s_start[ORDERMOE_MAX_SERVERS];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int b = (int)blockIdx.x;
+    // this thread's slot, read first so that its latency overlaps the totals
+    const int64_t t0 = (int64_t)b * tb;
+    const int n = tb * k;
+    int s_loc = M, s_m = 0;
+    if (tid < n) {
+        const int64_t t = t0 + tid / k;
+        if (t < T) {
+            s_loc = loc_in[t];
+            s_m = exec_m[t * k + tid % k];
+        }
+    }
     for (int m = wave; m < M; m += RT_WAVES) {
         int32_t lo = 0, tot = 0;
         for (int i = lane; i < nblk; i += 64) {
@@ -778,18 +815,7 @@ dispatch_kernel(const int32_t* blk_dst, const int64_t* blk_cnt, int nblk, const 
         for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
         if (lane == 0) counters[wave] = v;
     }
-    const int64_t t0 = (int64_t)b * tb;
-    const int n = tb * k;
-    if (tid < n) {
-        const int64_t t = t0 + tid / k;
-        int dst = -1;
-        if (t < T) {
-            const int s = loc_in[t];
-            const int m = exec_m[t * k + tid % k];
-            if (s < M && m != s) dst = m;
-        }
-        s_dst[tid] = (int8_t)dst;
-    }
+    if (tid < n) s_dst[tid] = (int8_t)(s_loc < M && s_m != s_loc ? s_m : -1);
     __syncthreads();
     if (tid == 0) {
         int32_t acc = 0;
