@@ -546,8 +546,17 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
     // K loop until the first K tile of the next one (a prologue loads sA0, sA1,
     // sB0 and sB1 only), so that the buffers of 256 x 256 tiles fill the LDS
     int* const s_last = (int*)sB2;
-    // down: the gate weights of the tile's rows, for the epilogue
-    __shared__ float s_roww[MODE == 1 ? BM : 1];
+    // down: the gate weights of the tile's rows, for the epilogue; 256-row tiles
+    // keep them in sB2 too (past the flag), so that their buffers fill the LDS
+    constexpr bool ROWW_IN_SB2 = MODE == 1 && (2 * BM + 3 * BN) * 64 * 2 + BM * 4 > 160 * 1024;
+    static_assert(!ROWW_IN_SB2 || 256 + BM * 4 <= BN * 64 * 2, "flag and row weights fit sB2");
+    float* s_roww;
+    if constexpr (ROWW_IN_SB2) {
+        s_roww = (float*)sB2 + 64;
+    } else {
+        __shared__ float s_roww_own[MODE == 1 ? BM : 1];
+        s_roww = s_roww_own;
+    }
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
@@ -911,6 +920,8 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
         // LDS by the workgroup (the barrier also orders it after the previous
         // tile's reads, which precede this tile's K-loop barriers).
         if constexpr (MODE == 1) {
+            // (in sB2: after every wave's last fragment reads of the K loop)
+            if constexpr (ROWW_IN_SB2) lds_barrier();
             if (tid_r < BM) s_roww[tid_r] = roww;
             lds_barrier();
         }
@@ -1235,6 +1246,13 @@ __global__ void __launch_bounds__(256) combine_kernel(const CombineArgs c) {
 
 
 constexpr int GU_BM = 256, GU_BN = 256, DN_BM = 192, DN_BN = 256;   // bf16 GEMM tiles
+// Large batches take 256-row down tiles: when even 256-row tiles would fill
+// the grid DN_TALL_ROUNDS times over by the host's upper bound on the rows,
+// the taller tile's better operand reuse outweighs the rounding of the last
+// tile of each group and the shorter last round; smaller batches keep 192
+// rows, which spread a few thousand rows over more of the 256 CUs.
+constexpr int DN_BM_TALL = 256;
+constexpr int64_t DN_TALL_ROUNDS = 8;
 constexpr int F32_BM = 64, F32_BN = 64;
 // bf16 batches of at most THIN_MAX_T tokens (every expert then has at most that
 // many rows) take the thin GEMM, THIN_PER_CU resident workgroups per CU
@@ -1287,6 +1305,10 @@ int launch_local_forward(const ForwardArgs& f, void* stream) {
     const bool thin = forward_uses_thin(f.dtype, f.T);
     int bm_gu, bn_gu, bm_dn, bn_dn;
     forward_tile_shape(f.dtype, f.T, &bm_gu, &bn_gu, &bm_dn, &bn_dn);
+    const int64_t rows_r = f.rmax_routed, rows_s = has_sh ? f.T : 0;
+    if (!thin && f.dtype == ORDERMOE_BF16 &&
+        ((rows_r + rows_s + DN_BM_TALL - 1) / DN_BM_TALL + G) * (f.d / DN_BN) >= DN_TALL_ROUNDS * SK_MAX_GRID)
+        bm_dn = DN_BM_TALL;
 
     RowsArgs r;
     r.T = f.T; r.k = f.k; r.E = f.E; r.n_local = f.n_local; r.has_shared = has_sh; r.server = f.server;
@@ -1329,7 +1351,6 @@ int launch_local_forward(const ForwardArgs& f, void* stream) {
     g.ntiles = f.tile_info + 0;
     g.Nr = 2 * f.f; g.Kr = f.d; g.Ns = 2 * f.n_shared * f.f; g.Ks = f.d;
     g.Wr = f.w_gu; g.Ws = f.w_sh_gu; g.Ar = nullptr; g.As = nullptr; g.Or = f.act_r; g.Os = f.act_s;
-    const int64_t rows_r = f.rmax_routed, rows_s = has_sh ? f.T : 0;
     int64_t ub_gu = ((rows_r + bm_gu - 1) / bm_gu + f.n_local) * (2 * f.f / bn_gu) +
                     (has_sh ? ((rows_s + bm_gu - 1) / bm_gu + 1) * (2 * f.n_shared * f.f / bn_gu) : 0);
     int64_t ub_dn = ((rows_r + rows_s + bm_dn - 1) / bm_dn + G) * (f.d / bn_dn);
@@ -1366,7 +1387,8 @@ int launch_local_forward(const ForwardArgs& f, void* stream) {
     } else if (f.dtype == ORDERMOE_BF16) {
         {
         KernelTimer kt_("gemm_down", st);
-        ggemm_bf16<DN_BM, DN_BN, 1><<<dim3(bf16_grid(ub_dn)), dim3(256), 0, st>>>(g);
+        if (bm_dn == DN_BM_TALL) ggemm_bf16<DN_BM_TALL, DN_BN, 1><<<dim3(bf16_grid(ub_dn)), dim3(256), 0, st>>>(g);
+        else ggemm_bf16<DN_BM, DN_BN, 1><<<dim3(bf16_grid(ub_dn)), dim3(256), 0, st>>>(g);
         }
     } else {
         {

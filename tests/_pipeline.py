@@ -300,7 +300,7 @@ def with_horizon(sc: StreamCase, H: int, allow_sub: Optional[int] = None) -> Str
 # mirror to know which of their shapes exercise the split.
 def gemm_plan(cfg, rows, n_local: int, cus: int = 256):
     """rows: the forward's row_offsets output [n_local + 2].  Returns
-    {"gate_up": (tiles, grid, rounds, left, split, shared_halves), "down": (...)};
+    {"gate_up": (tiles, grid, rounds, left, split, shared_halves, tile_rows), "down": (...)};
     shared_halves is 1 when the shared tiles are cut into two K halves."""
     R = np.diff(np.asarray(rows, dtype=np.int64))       # rows per group, shared last
     has_sh = cfg.n_shared > 0
@@ -326,9 +326,11 @@ def gemm_plan(cfg, rows, n_local: int, cus: int = 256):
         split = min(grid // left, 4, Kr // 128, Kr // 64 // 16) if left else 0
         if has_sh and Ks != Kr:
             split = 1
-        return tiles, grid, rounds, left, split, halves
+        return tiles, grid, rounds, left, split, halves, bm
 
     ub_gu = (-(-rr // 256) + n_local) * (2 * f // 256) + ((-(-rs // 256) + 1) * (2 * ns * f // 256) if has_sh else 0)
-    ub_dn = (-(-(rr + rs) // 192) + n_local + int(has_sh)) * (d // 256)
+    # down tiles of 256 rows when even those would fill the grid eight times over
+    bm_dn = 256 if (-(-(rr + rs) // 256) + n_local + int(has_sh)) * (d // 256) >= 8 * 256 else 192
+    ub_dn = (-(-(rr + rs) // bm_dn) + n_local + int(has_sh)) * (d // 256)
     return {"gate_up": plan(256, 256, 2 * f, 2 * ns * f, d, d, ub_gu),
-            "down": plan(192, 256, d, d, f, ns * f, ub_dn)}
+            "down": plan(bm_dn, 256, d, d, f, ns * f, ub_dn)}

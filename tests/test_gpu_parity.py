@@ -59,6 +59,8 @@ SPLIT = {"C3split": {"gate_up": 0, "down": 2}, "C4split": {"gate_up": 2, "down":
          "C2": {"gate_up": 2}, "C2x": {"gate_up": 3}}
 # shapes whose down projection cuts its shared tiles into two K halves
 SHARED_HALVES = {"C3sh", "C3"}
+# shapes whose down projection takes 256-row tiles (large batches)
+TALL_DOWN = {"C4"}
 # decode-sized batches (at most 128 tokens): the thin-GEMM path of the forward
 DECODE = {
     "C2d": wl.C2.with_(T=64, T_cal=4096),
@@ -144,11 +146,12 @@ def _check_output(case, dec, y_gpu, tokens, ok, tol):
 def _check_split(name, case, rows):
     """The shapes meant to exercise the split along K do split (host mirror of
     the launch plan, from the GPU's own row counts)."""
-    if name not in SPLIT and name not in SHARED_HALVES:
+    if name not in SPLIT and name not in SHARED_HALVES and name not in TALL_DOWN:
         return
     plan = gemm_plan(case.cfg, rows, len(case.local))
-    print("[%s] GEMM plan (tiles, grid, rounds, left, split, shared halves): %s" % (case.cfg.name, plan),
-          flush=True)
+    print("[%s] GEMM plan (tiles, grid, rounds, left, split, shared halves, tile rows): %s"
+          % (case.cfg.name, plan), flush=True)
+    assert plan["down"][6] == (256 if name in TALL_DOWN else 192), plan["down"]
     for gemm, want in SPLIT.get(name, {}).items():
         assert plan[gemm][4] == want, (gemm, plan[gemm])
     assert plan["down"][5] == int(name in SHARED_HALVES), plan["down"]
@@ -342,11 +345,11 @@ def test_invalid_locations_are_counted_not_routed():
     assert c[:4].sum() == (case.X.shape[0] - 2) * case.cfg.k
 
 
-@pytest.mark.parametrize("name", ["C3s", "C3d", "C3split", "C3sh", "C2"])
+@pytest.mark.parametrize("name", ["C3s", "C3d", "C3split", "C3sh", "C2", "C4"])
 def test_runs_are_bitwise_deterministic(name):
     """Two runs give the same bits; C3split, C3sh and the full C2 layer split
     GEMM tiles along K, whose pieces are summed in K order by whichever
-    workgroup arrives last."""
+    workgroup arrives last; the full C4 layer runs 256-row down tiles."""
     case, tabs = _case(name, {**SMALL, **DECODE, **FULL}[name])
     dl = DeviceLayer(case, tabs)
     x, loc, qh = dl.inputs()
