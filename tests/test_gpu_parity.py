@@ -53,6 +53,9 @@ SMALL = {
     # four shared experts: the down projection's shared K is four times the
     # routed K, so its shared tiles are cut into two K halves
     "C3sh": wl.C3.with_(T=600, d=1024, f=512, n_shared=4, T_cal=4096),
+    # 16-token routing blocks with their token rows staged in LDS (at most one
+    # block per CU, d % 512 == 0), the last block holding 9 tokens
+    "C2xl": wl.C2.with_(T=3001, d=2048, f=1024, T_cal=4096),
 }
 # shapes whose GEMM plan splits leftover tiles along K (checked on the GPU's rows)
 SPLIT = {"C3split": {"gate_up": 0, "down": 2}, "C4split": {"gate_up": 2, "down": 1},
