@@ -3,9 +3,9 @@
 The allocation-free variant takes its workspace from the library's fixed
 per-GPU scratch; its outputs must equal those of the workspace variant bit for
 bit.  Two calls in a row on one GPU, the second with a smaller batch (the
-scratch keeps the first call's contents), for a prefill-sized batch and a
-decode-sized one (whose router is split over K into partial logits held in
-the scratch)."""
+scratch keeps the first call's contents), for prefill-sized batches (32-token
+blocks; 16-token blocks with their token rows in LDS) and a decode-sized one
+(whose router is split over K into partial logits held in the scratch)."""
 import numpy as np
 import pytest
 
@@ -42,6 +42,8 @@ def _compare(dl, x, loc, qh, T):
 
 @pytest.mark.parametrize("cfg,T1,T2", [
     (wl.C4.with_(T=3000, T_cal=4096), 3000, 1100),
+    # 16-token blocks with their token rows staged in LDS (both batches)
+    (wl.C2.with_(T=2049, T_cal=4096), 2049, 1100),
     (wl.C2.with_(T=97, T_cal=4096), 97, 40),
 ])
 def test_noalloc_route_select_equals_the_workspace_variant(cfg, T1, T2):
