@@ -366,7 +366,7 @@ __host__ __device__ inline int64_t wblk_elem(int64_t n, int64_t k, int64_t K) {
 // gate/up: one block per packed row p of the n 2f rows; rows [64b, 64b+32) of
 // an expert <- gate rows [32b, 32b+32), rows [64b+32, 64b+64) <- the matching up
 // rows; bf16 rows then go to their blocked places in 16-byte pieces
-__global__ void pack_gate_up_kernel(int esz, int64_t n, int f, int d, const char* g, const char* u, char* out) {
+__global__ void pack_gate_up_kernel(int esz, int f, int d, const char* g, const char* u, char* out) {
     const int64_t prow = blockIdx.x;                  // over n * 2f rows
     const int64_t ex = prow / (2 * f);
     const int pr = (int)(prow % (2 * f));
@@ -385,7 +385,7 @@ __global__ void pack_gate_up_kernel(int esz, int64_t n, int f, int d, const char
 }
 
 // down: one block per row p of the n d rows of [n][d][f]
-__global__ void pack_down_kernel(int esz, int64_t n, int d, int f, const char* w, char* out) {
+__global__ void pack_down_kernel(int esz, int d, int f, const char* w, char* out) {
     const int64_t row = blockIdx.x;                   // over n * d rows
     const int64_t ex = row / d;
     const int r = (int)(row % d);
@@ -558,8 +558,7 @@ __global__ void __launch_bounds__(256, 1) ggemm_bf16(const GemmArgs p) {
         s_roww = s_roww_own;
     }
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int tid = threadIdx.x;
     const int total = *p.ntiles;
     const int grid = (int)gridDim.x;                // a multiple of 8, at most SK_MAX_GRID
     const int vid = (blockIdx.x & 7) * (grid >> 3) + (blockIdx.x >> 3);
@@ -1415,7 +1414,7 @@ int launch_pack_gate_up(int dtype, int n, int f, int d, const void* g, const voi
     const int64_t rows = (int64_t)n * 2 * f;
     if (rows == 0) return 0;
     hipLaunchKernelGGL(pack_gate_up_kernel, dim3((unsigned)rows), dim3(256), 0, (hipStream_t)stream,
-                       esz, (int64_t)n, f, d, (const char*)g, (const char*)u, (char*)out);
+                       esz, f, d, (const char*)g, (const char*)u, (char*)out);
     return (int)hipGetLastError();
 }
 
@@ -1424,7 +1423,7 @@ int launch_pack_down(int dtype, int n, int d, int f, const void* w, void* out, v
     const int64_t rows = (int64_t)n * d;
     if (rows == 0) return 0;
     hipLaunchKernelGGL(pack_down_kernel, dim3((unsigned)rows), dim3(256), 0, (hipStream_t)stream,
-                       esz, (int64_t)n, d, f, (const char*)w, (char*)out);
+                       esz, d, f, (const char*)w, (char*)out);
     return (int)hipGetLastError();
 }
 
