@@ -56,6 +56,9 @@ SMALL = {
     # 16-token routing blocks with their token rows staged in LDS (at most one
     # block per CU, d % 512 == 0), the last block holding 9 tokens
     "C2xl": wl.C2.with_(T=3001, d=2048, f=1024, T_cal=4096),
+    # a batch large enough for 256-row down tiles (the host's row bound fills
+    # the grid eight times over), over two whole rounds and a partial one
+    "C4tall": wl.C4.with_(T=4700, d=4096, f=256, T_cal=4096),
 }
 # shapes whose GEMM plan splits leftover tiles along K (checked on the GPU's rows)
 SPLIT = {"C3split": {"gate_up": 0, "down": 2}, "C4split": {"gate_up": 2, "down": 1},
@@ -63,7 +66,7 @@ SPLIT = {"C3split": {"gate_up": 0, "down": 2}, "C4split": {"gate_up": 2, "down":
 # shapes whose down projection cuts its shared tiles into two K halves
 SHARED_HALVES = {"C3sh", "C3"}
 # shapes whose down projection takes 256-row tiles (large batches)
-TALL_DOWN = {"C4"}
+TALL_DOWN = {"C4", "C4tall"}
 # decode-sized batches (at most 128 tokens): the thin-GEMM path of the forward
 DECODE = {
     "C2d": wl.C2.with_(T=64, T_cal=4096),
