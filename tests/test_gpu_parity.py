@@ -56,6 +56,9 @@ SMALL = {
     # 16-token routing blocks with their token rows staged in LDS (at most one
     # block per CU, d % 512 == 0), the last block holding 9 tokens
     "C2xl": wl.C2.with_(T=3001, d=2048, f=1024, T_cal=4096),
+    # the same path at its bounds: 16 experts, d = 4096, 16 rows of 8 KB per block
+    "C2xl16": wl.C2.with_(T=4001, f=512, E=16, clusters=8, cluster_size=2, capacity=(8.0,) * 4,
+                          T_cal=4096),
     # a batch large enough for 256-row down tiles (the host's row bound fills
     # the grid eight times over), over two whole rounds and a partial one
     "C4tall": wl.C4.with_(T=4700, d=4096, f=256, T_cal=4096),
